@@ -1,0 +1,75 @@
+"""An independent float64 PyTorch (CPU) formulation of the server block, used
+only to cross-check the oracle.  It shares no code with the oracle: LayerNorm,
+linear layers and the tanh GeLU are torch library routines, the rotary
+encoding is complex multiplication, attention is torch's
+scaled_dot_product_attention with an explicit boolean mask per sequence, and
+every gradient comes from autograd."""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+
+def _mask(L: int, prefix):
+    i = torch.arange(L)[:, None]
+    j = torch.arange(L)[None, :]
+    causal = j <= i
+    if prefix is None:
+        return causal
+    in_prefix = (i < prefix) & (j < prefix)
+    return causal | in_prefix
+
+
+def _rotate(x: torch.Tensor, pos: torch.Tensor, r: int, base: float) -> torch.Tensor:
+    """x [L, nh, d]: leading r dims of each head as r/2 complex numbers
+    (x[i], x[i + r/2]) multiplied by exp(i * p * theta_i)."""
+    half = r // 2
+    theta = base ** (-(2.0 * torch.arange(half, dtype=torch.float64)) / r)
+    ang = pos.to(torch.float64)[:, None] * theta[None, :]
+    rot = torch.polar(torch.ones_like(ang), ang)[:, None, :]
+    z = torch.complex(x[..., :half], x[..., half:r]) * rot
+    return torch.cat([z.real, z.imag, x[..., r:]], dim=-1)
+
+
+def block(p, x, cu_seqlens, prefix_len, shape):
+    T, H = x.shape
+    nh = shape.num_heads
+    d = H // nh
+    u = F.layer_norm(x, (H,), p["ln1_g"], p["ln1_b"], shape.ln_eps)
+    qkv = F.linear(u, p["w_qkv"], p["b_qkv"])
+    q, k, v = qkv.split(H, dim=1)
+    outs = []
+    for s in range(len(cu_seqlens) - 1):
+        r0, r1 = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
+        L = r1 - r0
+        pos = torch.arange(L)
+        qs = _rotate(q[r0:r1].reshape(L, nh, d), pos, shape.rotary_dim, shape.rope_base)
+        ks = _rotate(k[r0:r1].reshape(L, nh, d), pos, shape.rotary_dim, shape.rope_base)
+        vs = v[r0:r1].reshape(L, nh, d)
+        pre = None if prefix_len is None else int(prefix_len[s])
+        o = F.scaled_dot_product_attention(qs.transpose(0, 1), ks.transpose(0, 1), vs.transpose(0, 1),
+                                           attn_mask=_mask(L, pre))
+        outs.append(o.transpose(0, 1).reshape(L, H))
+    o = torch.cat(outs, dim=0)
+    h = x + F.linear(o, p["w_o"], p["b_o"])
+    w = F.layer_norm(h, (H,), p["ln2_g"], p["ln2_b"], shape.ln_eps)
+    g = F.gelu(F.linear(w, p["w_1"], p["b_1"]), approximate="tanh")
+    return h + F.linear(g, p["w_2"], p["b_2"])
+
+
+def stack_fwd_bwd(layers, x, dy, batch, shape):
+    """Returns y, dx and per-layer grads (numpy float64) via autograd."""
+    tl = [{k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in lp.items()}
+          for lp in layers]
+    tx = torch.tensor(np.asarray(x, np.float64), requires_grad=True)
+    cur = tx
+    pre = batch.prefix_len if batch.mask == "prefix" else None
+    for lp in tl:
+        cur = block(lp, cur, batch.cu_seqlens, pre, shape)
+    (cur * torch.tensor(np.asarray(dy, np.float64))).sum().backward()
+    grads = [{k: v.grad.numpy() for k, v in lp.items()} for lp in tl]
+    return cur.detach().numpy(), tx.grad.numpy(), grads
