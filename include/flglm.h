@@ -1,0 +1,176 @@
+/*
+ * flglm.h - C ABI of the FL-GLM server-stack library (MI355X / gfx950).
+ *
+ * What it computes.  In FL-GLM the model is split into three parts; the
+ * server holds the middle blocks 1..N-2 and maps the clients' smashed data
+ * h_0 to h_{N-2} = Block_(1,N-2)(h_0) (Section 3.1, Model Split).  With
+ * client-batch parallel training the server stacks the smashed data of M
+ * clients into one batch (Section 3.3, Parallel Acceleration); here the
+ * stacked batch is packed without padding: rows of client 0's sequences,
+ * then client 1's, and so on, with per-sequence offsets.  In the backward
+ * pass the server receives dL/dh_{N-2}, returns dL/dh_0 to every client and
+ * accumulates the gradients of its own weights (split learning, Section 1
+ * and Section 3.1).
+ *
+ * Each block is a pre-LayerNorm transformer layer (Section 3.1: multi-head
+ * self-attention followed by a feed-forward network; Appendix A: scores
+ * softmax(Q K^T / sqrt(d_h))):
+ *     u = LN1(x);  [q|k|v] = u W_qkv^T + b_qkv;  q, k rotated on the first
+ *     rotary_dim dims of every head (pairs (i, i + rotary_dim/2), angle
+ *     p * rope_base^(-2i/rotary_dim), p = position inside the sequence);
+ *     h = x + Attn(q, k, v) W_o^T + b_o;   w = LN2(h);
+ *     y = h + gelu_tanh(w W_1^T + b_1) W_2^T + b_2.
+ * Attention never crosses a sequence boundary (hence never a client
+ * boundary).  Mask: causal, or prefix-LM where key j is visible to query i
+ * iff j <= max(i, P_s - 1).
+ *
+ * Conventions (all entry points):
+ *   - Return 0 (FL_OK) or a negative FL_ERR_* code; fl_last_error() gives a
+ *     thread-local message for the last failure.  Nothing is enqueued and no
+ *     output is written when an entry point returns an error from its
+ *     validation step.
+ *   - "host" pointers are read during the call only; "device" pointers are
+ *     caller-owned device memory (hipMalloc / torch), 16-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  All device work
+ *     is asynchronous on that stream; execution errors surface at the
+ *     caller's next synchronisation.  One stream per handle at a time.
+ *   - Element type of activations and weights is the handle's dtype (bf16 or
+ *     fp32); statistics, softmax and all accumulation are fp32; weight
+ *     gradients are fp32 and are accumulated (+=), never zeroed.
+ *   - Results are deterministic: identical inputs give bitwise-identical
+ *     outputs (no atomics).
+ */
+#ifndef FLGLM_H_
+#define FLGLM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FL_OK 0
+#define FL_ERR_NULL (-1)        /* a required pointer is NULL */
+#define FL_ERR_SHAPE (-2)       /* unsupported or inconsistent stack shape */
+#define FL_ERR_SEQLENS (-3)     /* cu_seqlens / total_tokens / max_seqlen inconsistent, or an empty sequence */
+#define FL_ERR_CLIENTS (-4)     /* client_seq_ptr inconsistent, or a client without sequences */
+#define FL_ERR_PREFIX (-5)      /* bad mask kind or prefix length */
+#define FL_ERR_WORKSPACE (-6)   /* workspace or saved buffer too small */
+#define FL_ERR_ALIAS (-7)       /* an output overlaps an input it must not overlap */
+#define FL_ERR_ALIGN (-8)       /* a device pointer is not 16-byte aligned */
+#define FL_ERR_HIP (-9)         /* a HIP runtime call or kernel launch failed */
+#define FL_ERR_ARG (-10)        /* other invalid argument */
+
+#define FL_BF16 0
+#define FL_F32 1
+
+#define FL_MASK_CAUSAL 0
+#define FL_MASK_PREFIX 1
+
+/* Shape of the server-held stack; all blocks are identical.  Supported:
+ * hidden % 256 == 0, hidden / num_heads in {64, 128}, ffn_hidden % 256 == 0,
+ * rotary_dim % 32 == 0 and <= head dim, hidden <= 4096, ln_eps > 0. */
+typedef struct fl_stack_desc {
+  int32_t num_layers;   /* N server blocks (26 for ChatGLM-6B's server part) */
+  int32_t hidden;       /* H */
+  int32_t num_heads;    /* n_h; head dim d = H / n_h */
+  int32_t ffn_hidden;   /* F */
+  int32_t rotary_dim;   /* r: leading dims of each head that are rotated */
+  float rope_base;      /* 10000 */
+  float ln_eps;         /* 1e-5 */
+  int32_t dtype;        /* FL_BF16 or FL_F32 */
+} fl_stack_desc;
+
+/* A packed batch of clients (host arrays).  Sequence s covers packed rows
+ * [cu_seqlens[s], cu_seqlens[s+1]); client c owns sequences
+ * [client_seq_ptr[c], client_seq_ptr[c+1]), i.e. rows
+ * [cu_seqlens[client_seq_ptr[c]], cu_seqlens[client_seq_ptr[c+1]]). */
+typedef struct fl_batch_desc {
+  int32_t num_clients;            /* C >= 1 */
+  int32_t num_seqs;               /* S >= C */
+  int64_t total_tokens;           /* T = cu_seqlens[S] */
+  int32_t max_seqlen;             /* max_s (cu_seqlens[s+1] - cu_seqlens[s]) */
+  const int32_t* cu_seqlens;      /* host [S+1]: cu[0] = 0, strictly increasing */
+  const int32_t* client_seq_ptr;  /* host [C+1]: csp[0] = 0, strictly increasing, csp[C] = S */
+  int32_t mask_kind;              /* FL_MASK_CAUSAL or FL_MASK_PREFIX */
+  const int32_t* prefix_len;      /* host [S], 0 <= P_s <= L_s; NULL unless FL_MASK_PREFIX */
+} fl_batch_desc;
+
+/* One block's parameters (device, handle dtype).  Weights are
+ * out-features-major (y = x W^T + b): w_qkv [3H, H] (rows [0,H) query,
+ * [H,2H) key, [2H,3H) value; head h owns rows h*d .. h*d+d-1 of each),
+ * b_qkv [3H], w_o [H, H], b_o [H], w_1 [F, H], b_1 [F], w_2 [H, F], b_2 [H],
+ * ln1_g, ln1_b, ln2_g, ln2_b [H]. */
+typedef struct fl_layer_params {
+  const void *w_qkv, *b_qkv, *w_o, *b_o, *w_1, *b_1, *w_2, *b_2;
+  const void *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+} fl_layer_params;
+
+/* One block's gradient accumulators (device fp32, same shapes as the
+ * parameters).  The backward adds into them. */
+typedef struct fl_layer_grads {
+  float *w_qkv, *b_qkv, *w_o, *b_o, *w_1, *b_1, *w_2, *b_2;
+  float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+} fl_layer_grads;
+
+typedef struct fl_stack fl_stack;
+
+/* Creates a handle for a stack shape (validated; FL_ERR_SHAPE if
+ * unsupported).  Host-only: no HIP call.  On its first device call the
+ * handle creates a few events and a small pinned host staging area used to
+ * upload per-call batch descriptors; it never owns device memory. */
+int fl_stack_create(const fl_stack_desc* desc, fl_stack** out);
+/* Releases the handle.  Waits for uploads still in flight. NULL is a no-op. */
+int fl_stack_destroy(fl_stack* stack);
+
+/* Bytes of the `saved` buffer fl_server_stack_forward fills for the
+ * backward: with recompute = 0 every block's intermediates; with
+ * recompute = 1 only the inputs of blocks 2..N (the backward recomputes each
+ * block's forward from its input). */
+int fl_stack_saved_bytes(const fl_stack* stack, const fl_batch_desc* batch, int recompute, size_t* bytes);
+/* Bytes of device workspace needed by forward / backward / pack calls for
+ * this batch (one size serves all of them). */
+int fl_stack_workspace_bytes(const fl_stack* stack, const fl_batch_desc* batch, int recompute, size_t* bytes);
+
+/* Forward through the N server blocks (Section 3.1, h_{N-2} =
+ * Block_(1,N-2)(h_0)) over the packed client batch.
+ *   x  device [T, H]  packed smashed data h_0 (not modified)
+ *   y  device [T, H]  output h_{N-2}; must not overlap x
+ *   saved  device, fl_stack_saved_bytes(recompute) bytes, or NULL for a
+ *          forward-only (inference) call
+ *   workspace  device, >= fl_stack_workspace_bytes bytes, contents scratch */
+int fl_server_stack_forward(fl_stack* stack, const fl_batch_desc* batch, const fl_layer_params* layers,
+                            const void* x, void* y, void* saved, int recompute, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/* Backward through blocks N..1 after a forward with the same batch, params,
+ * x and recompute flag that filled `saved`.
+ *   dy  device [T, H]  dL/dh_{N-2} from the clients (not modified)
+ *   dx  device [T, H]  dL/dh_0, returned to the clients; must not overlap dy or x
+ *   grads  [N] accumulators (+=) */
+int fl_server_stack_backward(fl_stack* stack, const fl_batch_desc* batch, const fl_layer_params* layers,
+                             const fl_layer_grads* grads, const void* x, const void* saved, const void* dy,
+                             void* dx, int recompute, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Host only: packed row range [begin, end) of client `client`. */
+int fl_client_token_range(const fl_batch_desc* batch, int32_t client, int64_t* begin, int64_t* end);
+
+/* Client batching (Section 3.3): gather the clients' sequence-first tensors
+ * client_bufs[c] (device [Lmax_c, B_c, H], Lmax_c = the client's longest
+ * sequence, B_c = its number of sequences; positions beyond a sequence's
+ * length are ignored) into the packed [T, H] buffer, or scatter the packed
+ * buffer back (unpack zero-fills the padded positions).  Byte copies: exact. */
+int fl_pack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* const* client_bufs, void* packed,
+                    void* workspace, size_t workspace_bytes, void* stream);
+int fl_unpack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* packed, void* const* client_bufs,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Thread-local description of the last error returned on this thread. */
+const char* fl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLGLM_H_ */

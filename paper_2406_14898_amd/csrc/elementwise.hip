@@ -1,0 +1,357 @@
+// Memory-bound kernels of the block: LayerNorm forward/backward, rotary
+// position encoding, deterministic column sums (bias and LayerNorm parameter
+// gradients), packed-batch bookkeeping and client packing.  All of them move
+// 16-byte vectors along the contiguous hidden dimension.
+#include "common.h"
+#include "kernels.h"
+
+namespace flglm {
+
+// ---------------------------------------------------------------------------
+// Positions and rotary table
+// ---------------------------------------------------------------------------
+__global__ void seq_positions_kernel(const int32_t* cu, int32_t* pos) {
+  const int s = blockIdx.x;
+  const int r0 = cu[s], r1 = cu[s + 1];
+  for (int r = r0 + (int)threadIdx.x; r < r1; r += blockDim.x) pos[r] = r - r0;
+}
+
+hipError_t seq_positions(const int32_t* cu, int S, int32_t* pos, hipStream_t st) {
+  if (S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(seq_positions_kernel, dim3(S), dim3(256), 0, st, cu, pos);
+  return hipGetLastError();
+}
+
+__global__ void rope_table_kernel(float* ct, float* stbl, int max_pos, int r, double base) {
+  const int half = r / 2;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)max_pos * half) return;
+  const int p = (int)(idx / half), i = (int)(idx % half);
+  const double theta = pow(base, -2.0 * (double)i / (double)r);
+  const double ang = (double)p * theta;
+  ct[idx] = (float)cos(ang);
+  stbl[idx] = (float)sin(ang);
+}
+
+hipError_t rope_table(float* ct, float* stbl, int max_pos, int r, float base, hipStream_t st) {
+  const long n = (long)max_pos * (r / 2);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, ct, stbl, max_pos,
+                     r, (double)base);
+  return hipGetLastError();
+}
+
+// One thread rotates 4 pairs (i, i + r/2), i..i+3, of one head of q or k.
+template <typename T>
+__global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
+                               int H, int d, int r) {
+  const int half = r / 2, groups = half / 4;
+  const int nh = H / d;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long per_row = 2L * nh * groups;
+  if (idx >= (long)T_ * per_row) return;
+  const int t = (int)(idx / per_row);
+  int rem = (int)(idx % per_row);
+  const int part = rem / (nh * groups);
+  rem %= nh * groups;
+  const int h = rem / groups, i = (rem % groups) * 4;
+  T* base = qkv + (long)t * ld + part * H + h * d;
+  const int p = pos[t];
+  Vec4<T> a, b;
+  a.load(base + i);
+  b.load(base + half + i);
+  const float* c = ct + (long)p * half + i;
+  const float* s = stbl + (long)p * half + i;
+  float ya[4], yb[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x1 = a.get(e), x2 = b.get(e);
+    ya[e] = x1 * c[e] - x2 * s[e];
+    yb[e] = x2 * c[e] + x1 * s[e];
+  }
+  a.set(ya);
+  b.set(yb);
+  a.store(base + i);
+  b.store(base + half + i);
+}
+
+hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
+                   int H, int d, int r, hipStream_t st) {
+  const long n = (long)T_ * 2 * (H / d) * (r / 8);
+  if (n <= 0) return hipSuccess;
+  dim3 g((unsigned)((n + 255) / 256));
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, ct, stbl, T_, H, d, r);
+  else
+    hipLaunchKernelGGL(rope_qk_kernel<float>, g, dim3(256), 0, st, (float*)qkv, ld, pos, ct, stbl, T_, H, d, r);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm: one wave per row, the row held in registers (MAXC 8-element
+// chunks per lane, H <= 512 * MAXC).
+// ---------------------------------------------------------------------------
+template <typename T, int MAXC>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, const T* b, T* y, float* mean,
+                                                     float* rstd, int T_, int H, float eps) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= T_) return;
+  const int nch = H / 8;
+  const T* xr = x + (long)row * H;
+  float v[MAXC][8];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int idx = lane + 64 * c;
+    if (idx < nch) {
+      Vec8<T> t;
+      t.load(xr + idx * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { v[c][e] = t.get(e); s += v[c][e]; }
+    }
+  }
+  const float mu = wave_sum(s) / (float)H;
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    if (lane + 64 * c < nch) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { const float dlt = v[c][e] - mu; ss += dlt * dlt; }
+    }
+  }
+  const float rs = 1.0f / sqrtf(wave_sum(ss) / (float)H + eps);
+  T* yr = y + (long)row * H;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int idx = lane + 64 * c;
+    if (idx < nch) {
+      Vec8<T> gg, bb, o;
+      gg.load(g + idx * 8);
+      bb.load(b + idx * 8);
+      float out[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[e] = (v[c][e] - mu) * rs * gg.get(e) + bb.get(e);
+      o.set(out);
+      o.store(yr + idx * 8);
+    }
+  }
+  if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
+}
+
+template <typename T, int MAXC>
+__global__ void __launch_bounds__(256) ln_bwd_dx_kernel(const T* dy, const T* x, const float* mean,
+                                                        const float* rstd, const T* g, const T* dres, T* dx, int T_,
+                                                        int H) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= T_) return;
+  const int nch = H / 8;
+  const float mu = mean[row], rs = rstd[row];
+  const long off = (long)row * H;
+  float dxh[MAXC][8], xh[MAXC][8];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int idx = lane + 64 * c;
+    if (idx < nch) {
+      Vec8<T> a, xx, gg;
+      a.load(dy + off + idx * 8);
+      xx.load(x + off + idx * 8);
+      gg.load(g + idx * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        xh[c][e] = (xx.get(e) - mu) * rs;
+        dxh[c][e] = a.get(e) * gg.get(e);
+        s1 += dxh[c][e];
+        s2 += dxh[c][e] * xh[c][e];
+      }
+    }
+  }
+  const float m1 = wave_sum(s1) / (float)H;
+  const float m2 = wave_sum(s2) / (float)H;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int idx = lane + 64 * c;
+    if (idx < nch) {
+      Vec8<T> r, o;
+      r.load(dres + off + idx * 8);
+      float out[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[e] = r.get(e) + rs * (dxh[c][e] - m1 - xh[c][e] * m2);
+      o.set(out);
+      o.store(dx + off + idx * 8);
+    }
+  }
+}
+
+template <typename T>
+static hipError_t ln_fwd_t(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd, int T_,
+                           int H, float eps, hipStream_t st) {
+  dim3 grid((T_ + 3) / 4), blk(256);
+  const int nch = H / 8;
+  if (nch <= 64)
+    hipLaunchKernelGGL((ln_fwd_kernel<T, 1>), grid, blk, 0, st, (const T*)x, (const T*)g, (const T*)b, (T*)y, mean,
+                       rstd, T_, H, eps);
+  else if (nch <= 256)
+    hipLaunchKernelGGL((ln_fwd_kernel<T, 4>), grid, blk, 0, st, (const T*)x, (const T*)g, (const T*)b, (T*)y, mean,
+                       rstd, T_, H, eps);
+  else if (nch <= 512)
+    hipLaunchKernelGGL((ln_fwd_kernel<T, 8>), grid, blk, 0, st, (const T*)x, (const T*)g, (const T*)b, (T*)y, mean,
+                       rstd, T_, H, eps);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t ln_bwd_t(const void* dy, const void* x, const float* mean, const float* rstd, const void* g,
+                           const void* dres, void* dx, int T_, int H, hipStream_t st) {
+  dim3 grid((T_ + 3) / 4), blk(256);
+  const int nch = H / 8;
+  if (nch <= 64)
+    hipLaunchKernelGGL((ln_bwd_dx_kernel<T, 1>), grid, blk, 0, st, (const T*)dy, (const T*)x, mean, rstd,
+                       (const T*)g, (const T*)dres, (T*)dx, T_, H);
+  else if (nch <= 256)
+    hipLaunchKernelGGL((ln_bwd_dx_kernel<T, 4>), grid, blk, 0, st, (const T*)dy, (const T*)x, mean, rstd,
+                       (const T*)g, (const T*)dres, (T*)dx, T_, H);
+  else if (nch <= 512)
+    hipLaunchKernelGGL((ln_bwd_dx_kernel<T, 8>), grid, blk, 0, st, (const T*)dy, (const T*)x, mean, rstd,
+                       (const T*)g, (const T*)dres, (T*)dx, T_, H);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,
+                         int T_, int H, float eps, hipStream_t st) {
+  if (T_ <= 0) return hipSuccess;
+  return dt == DT_BF16 ? ln_fwd_t<bf16>(x, g, b, y, mean, rstd, T_, H, eps, st)
+                       : ln_fwd_t<float>(x, g, b, y, mean, rstd, T_, H, eps, st);
+}
+
+hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
+                            const void* g, const void* dres, void* dx, int T_, int H, hipStream_t st) {
+  if (T_ <= 0) return hipSuccess;
+  return dt == DT_BF16 ? ln_bwd_t<bf16>(dy, x, mean, rstd, g, dres, dx, T_, H, st)
+                       : ln_bwd_t<float>(dy, x, mean, rstd, g, dres, dx, T_, H, st);
+}
+
+// ---------------------------------------------------------------------------
+// Column sums.  Workgroup (cb, rb): columns cb*512 .. +511 (8 per lane), rows
+// rb*kColsumRows .. ; wave w takes every 4th row; the four waves combine in
+// LDS in a fixed order.
+// ---------------------------------------------------------------------------
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256) colsum_partial_kernel(const T* X, long ldx, const T* Y, const float* mean,
+                                                             const float* rstd, int T_, int N, float* part,
+                                                             float* part2) {
+  __shared__ float sh[2][4][512];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = blockIdx.x * 512 + lane * 8;
+  const int r0 = blockIdx.y * kColsumRows;
+  const int r1 = min(r0 + kColsumRows, T_);
+  float a1[8], a2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) { a1[e] = 0.f; a2[e] = 0.f; }
+  if (col < N) {
+    for (int r = r0 + w; r < r1; r += 4) {
+      Vec8<T> xv;
+      xv.load(X + (long)r * ldx + col);
+      if constexpr (MODE == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a1[e] += xv.get(e);
+      } else {
+        Vec8<T> yv;
+        yv.load(Y + (long)r * ldx + col);
+        const float mu = mean[r], rs = rstd[r];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          a1[e] += xv.get(e) * ((yv.get(e) - mu) * rs);
+          a2[e] += xv.get(e);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    sh[0][w][lane * 8 + e] = a1[e];
+    sh[1][w][lane * 8 + e] = a2[e];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < 512; c += 256) {
+    const int n = blockIdx.x * 512 + c;
+    if (n < N) {
+      part[(long)blockIdx.y * N + n] = ((sh[0][0][c] + sh[0][1][c]) + sh[0][2][c]) + sh[0][3][c];
+      if constexpr (MODE == 1)
+        part2[(long)blockIdx.y * N + n] = ((sh[1][0][c] + sh[1][1][c]) + sh[1][2][c]) + sh[1][3][c];
+    }
+  }
+}
+
+hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const void* Y, const float* mean,
+                          const float* rstd, int T_, int N, float* part, float* part2, hipStream_t st) {
+  if (T_ <= 0 || N <= 0) return hipSuccess;
+  dim3 grid((N + 511) / 512, colsum_blocks(T_)), blk(256);
+  if (dt == DT_BF16) {
+    if (mode == 0)
+      hipLaunchKernelGGL((colsum_partial_kernel<bf16, 0>), grid, blk, 0, st, (const bf16*)X, ldx, (const bf16*)Y,
+                         mean, rstd, T_, N, part, part2);
+    else
+      hipLaunchKernelGGL((colsum_partial_kernel<bf16, 1>), grid, blk, 0, st, (const bf16*)X, ldx, (const bf16*)Y,
+                         mean, rstd, T_, N, part, part2);
+  } else {
+    if (mode == 0)
+      hipLaunchKernelGGL((colsum_partial_kernel<float, 0>), grid, blk, 0, st, (const float*)X, ldx,
+                         (const float*)Y, mean, rstd, T_, N, part, part2);
+    else
+      hipLaunchKernelGGL((colsum_partial_kernel<float, 1>), grid, blk, 0, st, (const float*)X, ldx,
+                         (const float*)Y, mean, rstd, T_, N, part, part2);
+  }
+  return hipGetLastError();
+}
+
+__global__ void colsum_finish_kernel(const float* part, int nblk, int N, float* out) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float s = 0.f;
+  for (int b = 0; b < nblk; ++b) s += part[(long)b * N + n];
+  out[n] += s;
+}
+
+hipError_t colsum_finish(const float* part, int nblk, int N, float* out, hipStream_t st) {
+  if (N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 255) / 256), dim3(256), 0, st, part, nblk, N, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Client packing (byte copies, 16-byte vectors).
+// ---------------------------------------------------------------------------
+__global__ void pack_client_kernel(const char* client, char* packed, const int32_t* cu, int s0, int nseq,
+                                   int row_bytes, bool unpack) {
+  const int p = blockIdx.x, b = blockIdx.y;
+  const int s = s0 + b;
+  const int r0 = cu[s], L = cu[s + 1] - r0;
+  const long crow = ((long)p * nseq + b) * row_bytes;
+  const long prow = (long)(r0 + p) * row_bytes;
+  for (int o = threadIdx.x * 16; o < row_bytes; o += blockDim.x * 16) {
+    if (p < L) {
+      if (unpack) st16((void*)(const_cast<char*>(client) + crow + o), ld16(packed + prow + o));
+      else st16(packed + prow + o, ld16(client + crow + o));
+    } else if (unpack) {
+      st16((void*)(const_cast<char*>(client) + crow + o), u32x4{0, 0, 0, 0});
+    }
+  }
+}
+
+hipError_t pack_client(DType dt, const void* client, void* packed, const int32_t* cu, int s0, int nseq, int Lmax,
+                       int H, bool unpack, hipStream_t st) {
+  if (Lmax <= 0 || nseq <= 0) return hipSuccess;
+  const int row_bytes = H * (dt == DT_BF16 ? 2 : 4);
+  hipLaunchKernelGGL(pack_client_kernel, dim3(Lmax, nseq), dim3(128), 0, st, (const char*)client, (char*)packed,
+                     cu, s0, nseq, row_bytes, unpack);
+  return hipGetLastError();
+}
+
+}  // namespace flglm

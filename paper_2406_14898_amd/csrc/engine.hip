@@ -1,0 +1,602 @@
+// The server-stack engine behind the C ABI: descriptor validation, memory
+// plan (saved activations and workspace carving), batch-plan upload, and the
+// per-block kernel sequence of the forward and backward passes, all enqueued
+// on the caller's stream with no host synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/flglm.h"
+#include "kernels.h"
+
+using namespace flglm;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_OK(expr)                                                                      \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess) return fail(FL_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Bump allocator over a caller-provided region (or a dry run for sizing).
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return p;
+  }
+};
+
+// Per-block forward intermediates.
+struct Acts {
+  void *u, *qkv, *o, *h, *w, *z, *g;
+  float *lse, *mean1, *rstd1, *mean2, *rstd2;
+};
+
+}  // namespace
+
+struct fl_stack {
+  fl_stack_desc d;
+  int E;   // element bytes
+  int hd;  // head dim
+  static constexpr int kRing = 4;
+  void* stage[kRing] = {};
+  size_t stage_cap[kRing] = {};
+  hipEvent_t ev[kRing] = {};
+  bool ev_made[kRing] = {};
+  bool ev_used[kRing] = {};
+  int next = 0;
+};
+
+namespace {
+
+struct BatchInfo {
+  int T, S, C, maxL;
+  bool prefix;
+};
+
+int validate_batch(const fl_batch_desc* b, BatchInfo* bi) {
+  if (!b) return fail(FL_ERR_NULL, "batch descriptor is NULL");
+  if (!b->cu_seqlens || !b->client_seq_ptr) return fail(FL_ERR_NULL, "cu_seqlens / client_seq_ptr is NULL");
+  if (b->num_seqs < 1) return fail(FL_ERR_SEQLENS, "num_seqs must be >= 1 (got %d)", b->num_seqs);
+  if (b->num_clients < 1) return fail(FL_ERR_CLIENTS, "num_clients must be >= 1 (got %d)", b->num_clients);
+  if (b->num_clients > b->num_seqs)
+    return fail(FL_ERR_CLIENTS, "num_clients %d > num_seqs %d", b->num_clients, b->num_seqs);
+  if (b->total_tokens < 1 || b->total_tokens > (int64_t)(1 << 26))
+    return fail(FL_ERR_SEQLENS, "total_tokens %lld out of range [1, 2^26]", (long long)b->total_tokens);
+  const int32_t* cu = b->cu_seqlens;
+  if (cu[0] != 0) return fail(FL_ERR_SEQLENS, "cu_seqlens[0] must be 0");
+  int maxL = 0;
+  for (int s = 0; s < b->num_seqs; ++s) {
+    const int L = cu[s + 1] - cu[s];
+    if (L < 1) return fail(FL_ERR_SEQLENS, "sequence %d has length %d (must be >= 1)", s, L);
+    maxL = std::max(maxL, L);
+  }
+  if ((int64_t)cu[b->num_seqs] != b->total_tokens)
+    return fail(FL_ERR_SEQLENS, "cu_seqlens[S] = %d != total_tokens %lld", cu[b->num_seqs],
+                (long long)b->total_tokens);
+  if (b->max_seqlen != maxL) return fail(FL_ERR_SEQLENS, "max_seqlen %d != longest sequence %d", b->max_seqlen, maxL);
+  const int32_t* csp = b->client_seq_ptr;
+  if (csp[0] != 0) return fail(FL_ERR_CLIENTS, "client_seq_ptr[0] must be 0");
+  for (int c = 0; c < b->num_clients; ++c)
+    if (csp[c + 1] <= csp[c]) return fail(FL_ERR_CLIENTS, "client %d owns no sequences", c);
+  if (csp[b->num_clients] != b->num_seqs)
+    return fail(FL_ERR_CLIENTS, "client_seq_ptr[C] = %d != num_seqs %d", csp[b->num_clients], b->num_seqs);
+  if (b->mask_kind != FL_MASK_CAUSAL && b->mask_kind != FL_MASK_PREFIX)
+    return fail(FL_ERR_PREFIX, "unknown mask_kind %d", b->mask_kind);
+  if (b->mask_kind == FL_MASK_PREFIX) {
+    if (!b->prefix_len) return fail(FL_ERR_NULL, "prefix_len is NULL with FL_MASK_PREFIX");
+    for (int s = 0; s < b->num_seqs; ++s) {
+      const int L = cu[s + 1] - cu[s];
+      if (b->prefix_len[s] < 0 || b->prefix_len[s] > L)
+        return fail(FL_ERR_PREFIX, "prefix_len[%d] = %d outside [0, %d]", s, b->prefix_len[s], L);
+    }
+  }
+  bi->T = (int)b->total_tokens;
+  bi->S = b->num_seqs;
+  bi->C = b->num_clients;
+  bi->maxL = maxL;
+  bi->prefix = b->mask_kind == FL_MASK_PREFIX;
+  return FL_OK;
+}
+
+int validate_desc(const fl_stack_desc* d) {
+  if (!d) return fail(FL_ERR_NULL, "stack descriptor is NULL");
+  if (d->dtype != FL_BF16 && d->dtype != FL_F32) return fail(FL_ERR_SHAPE, "unknown dtype %d", d->dtype);
+  if (d->num_layers < 1) return fail(FL_ERR_SHAPE, "num_layers must be >= 1");
+  if (d->hidden < 256 || d->hidden % 256 != 0 || d->hidden > 4096)
+    return fail(FL_ERR_SHAPE, "hidden %d must be a multiple of 256 in [256, 4096]", d->hidden);
+  if (d->num_heads < 1 || d->hidden % d->num_heads != 0) return fail(FL_ERR_SHAPE, "hidden %% num_heads != 0");
+  const int hd = d->hidden / d->num_heads;
+  if (hd != 64 && hd != 128) return fail(FL_ERR_SHAPE, "head dim %d not in {64, 128}", hd);
+  if (d->ffn_hidden < 256 || d->ffn_hidden % 256 != 0)
+    return fail(FL_ERR_SHAPE, "ffn_hidden %d must be a positive multiple of 256", d->ffn_hidden);
+  if (d->rotary_dim < 0 || d->rotary_dim > hd || d->rotary_dim % 32 != 0)
+    return fail(FL_ERR_SHAPE, "rotary_dim %d must be a multiple of 32 in [0, head dim]", d->rotary_dim);
+  if (!(d->rope_base > 0.f)) return fail(FL_ERR_SHAPE, "rope_base must be > 0");
+  if (!(d->ln_eps > 0.f)) return fail(FL_ERR_SHAPE, "ln_eps must be > 0");
+  return FL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Memory plan
+// ---------------------------------------------------------------------------
+struct Plan {
+  int32_t* cu;
+  int32_t* prefix;
+  int32_t* pos;
+  float* cos_t;
+  float* sin_t;
+};
+
+void carve_plan(Carver& cv, const BatchInfo& bi, int rotary_dim, Plan* p) {
+  p->cu = (int32_t*)cv.take(sizeof(int32_t) * (bi.S + 1));
+  p->prefix = (int32_t*)cv.take(sizeof(int32_t) * bi.S);
+  p->pos = (int32_t*)cv.take(sizeof(int32_t) * bi.T);
+  const size_t tab = sizeof(float) * (size_t)bi.maxL * std::max(rotary_dim / 2, 1);
+  p->cos_t = (float*)cv.take(tab);
+  p->sin_t = (float*)cv.take(tab);
+}
+
+void carve_acts(Carver& cv, const fl_stack* st, int T, Acts* a) {
+  const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, nh = st->d.num_heads;
+  a->u = cv.take(E * T * H);
+  a->qkv = cv.take(E * T * 3 * H);
+  a->o = cv.take(E * T * H);
+  a->h = cv.take(E * T * H);
+  a->w = cv.take(E * T * H);
+  a->z = cv.take(E * T * F);
+  a->g = cv.take(E * T * F);
+  a->lse = (float*)cv.take(sizeof(float) * T * nh);
+  a->mean1 = (float*)cv.take(sizeof(float) * T);
+  a->rstd1 = (float*)cv.take(sizeof(float) * T);
+  a->mean2 = (float*)cv.take(sizeof(float) * T);
+  a->rstd2 = (float*)cv.take(sizeof(float) * T);
+}
+
+// saved = [acts_0 .. acts_{N-1}] (recompute == 0), then x_1 .. x_{N-1}.
+struct Saved {
+  std::vector<Acts> acts;
+  std::vector<void*> xin;  // xin[l] = input of block l (xin[0] unused: the caller's x)
+};
+void carve_saved(Carver& cv, const fl_stack* st, int T, bool recompute, Saved* s) {
+  const int N = st->d.num_layers;
+  s->acts.assign(N, Acts{});
+  s->xin.assign(N, nullptr);
+  if (!recompute)
+    for (int l = 0; l < N; ++l) carve_acts(cv, st, T, &s->acts[l]);
+  for (int l = 1; l < N; ++l) s->xin[l] = cv.take((size_t)st->E * T * st->d.hidden);
+}
+
+struct Work {
+  Plan plan;
+  Acts acts;      // forward intermediates when not saved / recomputed in backward
+  void* ping[2];  // block outputs (inference) / gradient ping-pong (backward)
+  void *dz, *dh, *tmp, *dqkv;
+  float* delta;
+  float *part, *part2;
+};
+void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
+  const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, T = bi.T;
+  carve_plan(cv, bi, st->d.rotary_dim, &w->plan);
+  carve_acts(cv, st, bi.T, &w->acts);
+  w->ping[0] = cv.take(E * T * H);
+  w->ping[1] = cv.take(E * T * H);
+  w->dz = cv.take(E * T * F);
+  w->dh = cv.take(E * T * H);
+  w->tmp = cv.take(E * T * H);
+  w->dqkv = cv.take(E * T * 3 * H);
+  w->delta = (float*)cv.take(sizeof(float) * T * st->d.num_heads);
+  const size_t nmax = std::max(F, 3 * H);
+  w->part = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
+  w->part2 = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
+}
+
+size_t saved_bytes(const fl_stack* st, const BatchInfo& bi, bool recompute) {
+  Carver cv(nullptr);
+  Saved s;
+  carve_saved(cv, st, bi.T, recompute, &s);
+  return cv.off;
+}
+size_t work_bytes(const fl_stack* st, const BatchInfo& bi) {
+  Carver cv(nullptr);
+  Work w;
+  carve_work(cv, st, bi, &w);
+  return cv.off;
+}
+
+// ---------------------------------------------------------------------------
+// Checks on device pointers
+// ---------------------------------------------------------------------------
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+int check_params(const fl_stack* st, const fl_layer_params* layers) {
+  if (!layers) return fail(FL_ERR_NULL, "layers is NULL");
+  for (int l = 0; l < st->d.num_layers; ++l) {
+    const void* ps[12] = {layers[l].w_qkv, layers[l].b_qkv, layers[l].w_o, layers[l].b_o,
+                          layers[l].w_1,   layers[l].b_1,   layers[l].w_2, layers[l].b_2,
+                          layers[l].ln1_g, layers[l].ln1_b, layers[l].ln2_g, layers[l].ln2_b};
+    for (int i = 0; i < 12; ++i) {
+      if (!ps[i]) return fail(FL_ERR_NULL, "layer %d parameter %d is NULL", l, i);
+      if (!aligned16(ps[i])) return fail(FL_ERR_ALIGN, "layer %d parameter %d is not 16-byte aligned", l, i);
+    }
+  }
+  return FL_OK;
+}
+
+int check_grads(const fl_stack* st, const fl_layer_grads* grads) {
+  if (!grads) return fail(FL_ERR_NULL, "grads is NULL");
+  for (int l = 0; l < st->d.num_layers; ++l) {
+    const float* ps[12] = {grads[l].w_qkv, grads[l].b_qkv, grads[l].w_o, grads[l].b_o,
+                           grads[l].w_1,   grads[l].b_1,   grads[l].w_2, grads[l].b_2,
+                           grads[l].ln1_g, grads[l].ln1_b, grads[l].ln2_g, grads[l].ln2_b};
+    for (int i = 0; i < 12; ++i) {
+      if (!ps[i]) return fail(FL_ERR_NULL, "layer %d gradient %d is NULL", l, i);
+      if (!aligned16(ps[i])) return fail(FL_ERR_ALIGN, "layer %d gradient %d is not 16-byte aligned", l, i);
+    }
+  }
+  return FL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Plan upload: host descriptor arrays -> pinned staging ring -> workspace.
+// ---------------------------------------------------------------------------
+int upload_plan(fl_stack* st, const fl_batch_desc* b, const BatchInfo& bi, const Plan& p, hipStream_t stream) {
+  const size_t ncu = bi.S + 1, npre = bi.S;
+  const size_t bytes = sizeof(int32_t) * (ncu + npre);
+  const int k = st->next;
+  st->next = (st->next + 1) % fl_stack::kRing;
+  if (!st->ev_made[k]) {
+    HIP_OK(hipEventCreateWithFlags(&st->ev[k], hipEventDisableTiming));
+    st->ev_made[k] = true;
+  }
+  if (st->ev_used[k]) HIP_OK(hipEventSynchronize(st->ev[k]));
+  if (st->stage_cap[k] < bytes) {
+    if (st->stage[k]) HIP_OK(hipHostFree(st->stage[k]));
+    st->stage[k] = nullptr;
+    st->stage_cap[k] = 0;
+    HIP_OK(hipHostMalloc(&st->stage[k], std::max(bytes, (size_t)4096), hipHostMallocDefault));
+    st->stage_cap[k] = std::max(bytes, (size_t)4096);
+  }
+  int32_t* h = (int32_t*)st->stage[k];
+  std::memcpy(h, b->cu_seqlens, sizeof(int32_t) * ncu);
+  if (bi.prefix) std::memcpy(h + ncu, b->prefix_len, sizeof(int32_t) * npre);
+  else std::memset(h + ncu, 0, sizeof(int32_t) * npre);
+  HIP_OK(hipMemcpyAsync(p.cu, h, sizeof(int32_t) * ncu, hipMemcpyHostToDevice, stream));
+  HIP_OK(hipMemcpyAsync(p.prefix, h + ncu, sizeof(int32_t) * npre, hipMemcpyHostToDevice, stream));
+  HIP_OK(hipEventRecord(st->ev[k], stream));
+  st->ev_used[k] = true;
+  HIP_OK(seq_positions(p.cu, bi.S, p.pos, stream));
+  HIP_OK(rope_table(p.cos_t, p.sin_t, bi.maxL, st->d.rotary_dim, st->d.rope_base, stream));
+  return FL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// One block forward.  `out` may be NULL (recompute for the backward: the
+// final projection is not needed).
+// ---------------------------------------------------------------------------
+int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_layer_params& p, const void* x,
+                  const Acts& a, void* out, hipStream_t s) {
+  const DType dt = (DType)st->d.dtype;
+  const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
+  HIP_OK(layernorm_fwd(dt, x, p.ln1_g, p.ln1_b, a.u, a.mean1, a.rstd1, T, H, st->d.ln_eps, s));
+  GemmDesc g;
+  g.A = a.u; g.B = p.w_qkv; g.C = a.qkv; g.M = T; g.N = 3 * H; g.K = H;
+  g.lda = H; g.ldb = H; g.ldc = 3 * H; g.bias = p.b_qkv;
+  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS, g, s));
+  HIP_OK(rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
+  AttnDesc ad;
+  ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
+  ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;
+  ad.num_seqs = bi.S; ad.max_seqlen = bi.maxL; ad.num_heads = st->d.num_heads; ad.head_dim = st->hd;
+  ad.hidden = H; ad.total_tokens = T;
+  HIP_OK(attn_fwd(dt, ad, s));
+  g = GemmDesc();
+  g.A = a.o; g.B = p.w_o; g.C = a.h; g.M = T; g.N = H; g.K = H;
+  g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.R = x; g.ldr = H;
+  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+  HIP_OK(layernorm_fwd(dt, a.h, p.ln2_g, p.ln2_b, a.w, a.mean2, a.rstd2, T, H, st->d.ln_eps, s));
+  g = GemmDesc();
+  g.A = a.w; g.B = p.w_1; g.C = a.z; g.C2 = a.g; g.M = T; g.N = F; g.K = H;
+  g.lda = H; g.ldb = H; g.ldc = F; g.ldc2 = F; g.bias = p.b_1;
+  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_GELU, g, s));
+  if (out) {
+    g = GemmDesc();
+    g.A = a.g; g.B = p.w_2; g.C = out; g.M = T; g.N = H; g.K = F;
+    g.lda = F; g.ldb = F; g.ldc = H; g.bias = p.b_2; g.R = a.h; g.ldr = H;
+    HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+  }
+  return FL_OK;
+}
+
+int colsum_into(DType dt, const void* X, long ldx, int T, int N, float* out, const Work& w, hipStream_t s) {
+  HIP_OK(colsum_partial(dt, 0, X, ldx, nullptr, nullptr, nullptr, T, N, w.part, nullptr, s));
+  HIP_OK(colsum_finish(w.part, colsum_blocks(T), N, out, s));
+  return FL_OK;
+}
+
+// One block backward: dy -> dx, gradients += .
+int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Work& w, const fl_layer_params& p,
+                   const fl_layer_grads& gr, const void* x, const Acts& a, const void* dy, void* dx, hipStream_t s) {
+  const DType dt = (DType)st->d.dtype;
+  const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
+  int rc;
+  // y = h + g W_2^T + b_2
+  if ((rc = colsum_into(dt, dy, H, T, H, gr.b_2, w, s))) return rc;
+  GemmDesc g;
+  g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
+  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  g = GemmDesc();
+  g.A = dy; g.B = p.w_2; g.C = w.dz; g.M = T; g.N = F; g.K = H; g.lda = H; g.ldb = F; g.ldc = F;
+  g.Z = a.z; g.ldz = F;
+  HIP_OK(gemm(dt, GEMM_NN, EPI_GELU_BWD, g, s));
+  // z = w W_1^T + b_1
+  if ((rc = colsum_into(dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
+  g = GemmDesc();
+  g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  g = GemmDesc();
+  g.A = w.dz; g.B = p.w_1; g.C = w.tmp; g.M = T; g.N = H; g.K = F; g.lda = F; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  // w = LN2(h); h also feeds y directly
+  HIP_OK(layernorm_bwd_dx(dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, T, H, s));
+  HIP_OK(colsum_partial(dt, 1, w.tmp, H, a.h, a.mean2, a.rstd2, T, H, w.part, w.part2, s));
+  HIP_OK(colsum_finish(w.part, colsum_blocks(T), H, gr.ln2_g, s));
+  HIP_OK(colsum_finish(w.part2, colsum_blocks(T), H, gr.ln2_b, s));
+  // h = x + o W_o^T + b_o
+  if ((rc = colsum_into(dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
+  g = GemmDesc();
+  g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  g = GemmDesc();
+  g.A = w.dh; g.B = p.w_o; g.C = w.tmp; g.M = T; g.N = H; g.K = H; g.lda = H; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  // attention (dq, dk, dv with the inverse rotation applied)
+  AttnDesc ad;
+  ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
+  ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;
+  ad.num_seqs = bi.S; ad.max_seqlen = bi.maxL; ad.num_heads = st->d.num_heads; ad.head_dim = st->hd;
+  ad.hidden = H; ad.total_tokens = T;
+  ad.dout = w.tmp; ad.ld_dout = H; ad.delta = w.delta; ad.dqkv = w.dqkv; ad.ld_dqkv = 3 * H;
+  ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t; ad.rotary_dim = st->d.rotary_dim;
+  HIP_OK(attn_bwd(dt, ad, s));
+  // qkv = u W_qkv^T + b_qkv
+  if ((rc = colsum_into(dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
+  g = GemmDesc();
+  g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  g = GemmDesc();
+  g.A = w.dqkv; g.B = p.w_qkv; g.C = w.tmp; g.M = T; g.N = H; g.K = 3 * H; g.lda = 3 * H; g.ldb = H; g.ldc = H;
+  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  // u = LN1(x); x also feeds h directly
+  HIP_OK(layernorm_bwd_dx(dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, w.dh, dx, T, H, s));
+  HIP_OK(colsum_partial(dt, 1, w.tmp, H, x, a.mean1, a.rstd1, T, H, w.part, w.part2, s));
+  HIP_OK(colsum_finish(w.part, colsum_blocks(T), H, gr.ln1_g, s));
+  HIP_OK(colsum_finish(w.part2, colsum_blocks(T), H, gr.ln1_b, s));
+  return FL_OK;
+}
+
+}  // namespace
+
+namespace flglm {
+int set_error(int code, const char* msg) { return fail(code, "%s", msg); }
+}  // namespace flglm
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* fl_last_error(void) { return g_err.c_str(); }
+
+int fl_stack_create(const fl_stack_desc* desc, fl_stack** out) {
+  if (!out) return fail(FL_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  int rc = validate_desc(desc);
+  if (rc) return rc;
+  fl_stack* st = new fl_stack();
+  st->d = *desc;
+  st->E = desc->dtype == FL_BF16 ? 2 : 4;
+  st->hd = desc->hidden / desc->num_heads;
+  *out = st;
+  return FL_OK;
+}
+
+int fl_stack_destroy(fl_stack* st) {
+  if (!st) return FL_OK;
+  int rc = FL_OK;
+  for (int k = 0; k < fl_stack::kRing; ++k) {
+    if (st->ev_used[k] && hipEventSynchronize(st->ev[k]) != hipSuccess) rc = FL_ERR_HIP;
+    if (st->stage[k] && hipHostFree(st->stage[k]) != hipSuccess) rc = FL_ERR_HIP;
+    if (st->ev_made[k] && hipEventDestroy(st->ev[k]) != hipSuccess) rc = FL_ERR_HIP;
+  }
+  delete st;
+  if (rc) return fail(rc, "HIP error while releasing the handle");
+  return FL_OK;
+}
+
+int fl_stack_saved_bytes(const fl_stack* st, const fl_batch_desc* b, int recompute, size_t* bytes) {
+  if (!st || !bytes) return fail(FL_ERR_NULL, "stack / bytes is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  *bytes = saved_bytes(st, bi, recompute != 0);
+  return FL_OK;
+}
+
+int fl_stack_workspace_bytes(const fl_stack* st, const fl_batch_desc* b, int recompute, size_t* bytes) {
+  (void)recompute;
+  if (!st || !bytes) return fail(FL_ERR_NULL, "stack / bytes is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  *bytes = work_bytes(st, bi);
+  return FL_OK;
+}
+
+int fl_client_token_range(const fl_batch_desc* b, int32_t client, int64_t* begin, int64_t* end) {
+  if (!begin || !end) return fail(FL_ERR_NULL, "begin / end is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  if (client < 0 || client >= bi.C) return fail(FL_ERR_ARG, "client %d outside [0, %d)", client, bi.C);
+  *begin = b->cu_seqlens[b->client_seq_ptr[client]];
+  *end = b->cu_seqlens[b->client_seq_ptr[client + 1]];
+  return FL_OK;
+}
+
+int fl_server_stack_forward(fl_stack* st, const fl_batch_desc* b, const fl_layer_params* layers, const void* x,
+                            void* y, void* saved, int recompute, void* ws, size_t ws_bytes, void* stream) {
+  if (!st) return fail(FL_ERR_NULL, "stack is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  if ((rc = check_params(st, layers))) return rc;
+  if (!x || !y || !ws) return fail(FL_ERR_NULL, "x / y / workspace is NULL");
+  if (!aligned16(x) || !aligned16(y) || !aligned16(ws) || (saved && !aligned16(saved)))
+    return fail(FL_ERR_ALIGN, "x / y / saved / workspace must be 16-byte aligned");
+  const size_t need_ws = work_bytes(st, bi);
+  if (ws_bytes < need_ws) return fail(FL_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need_ws);
+  const size_t act = (size_t)st->E * bi.T * st->d.hidden;
+  const size_t nsaved = saved ? saved_bytes(st, bi, recompute != 0) : 0;
+  if (overlap(x, act, y, act)) return fail(FL_ERR_ALIAS, "y overlaps x");
+  if (overlap(ws, ws_bytes, x, act) || overlap(ws, ws_bytes, y, act) || overlap(ws, ws_bytes, saved, nsaved))
+    return fail(FL_ERR_ALIAS, "workspace overlaps x / y / saved");
+  if (overlap(saved, nsaved, x, act) || overlap(saved, nsaved, y, act))
+    return fail(FL_ERR_ALIAS, "saved overlaps x / y");
+
+  hipStream_t s = (hipStream_t)stream;
+  Carver cw(ws);
+  Work w;
+  carve_work(cw, st, bi, &w);
+  Saved sv;
+  if (saved) {
+    Carver cs(saved);
+    carve_saved(cs, st, bi.T, recompute != 0, &sv);
+  }
+  if ((rc = upload_plan(st, b, bi, w.plan, s))) return rc;
+  const int N = st->d.num_layers;
+  const void* cur = x;
+  for (int l = 0; l < N; ++l) {
+    const Acts& a = (saved && !recompute) ? sv.acts[l] : w.acts;
+    void* out = (l == N - 1) ? y : (saved ? sv.xin[l + 1] : w.ping[l & 1]);
+    if ((rc = block_forward(st, bi, w.plan, layers[l], cur, a, out, s))) return rc;
+    cur = out;
+  }
+  return FL_OK;
+}
+
+int fl_server_stack_backward(fl_stack* st, const fl_batch_desc* b, const fl_layer_params* layers,
+                             const fl_layer_grads* grads, const void* x, const void* saved, const void* dy, void* dx,
+                             int recompute, void* ws, size_t ws_bytes, void* stream) {
+  if (!st) return fail(FL_ERR_NULL, "stack is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  if ((rc = check_params(st, layers))) return rc;
+  if ((rc = check_grads(st, grads))) return rc;
+  if (!x || !saved || !dy || !dx || !ws) return fail(FL_ERR_NULL, "x / saved / dy / dx / workspace is NULL");
+  if (!aligned16(x) || !aligned16(saved) || !aligned16(dy) || !aligned16(dx) || !aligned16(ws))
+    return fail(FL_ERR_ALIGN, "x / saved / dy / dx / workspace must be 16-byte aligned");
+  const size_t need_ws = work_bytes(st, bi);
+  if (ws_bytes < need_ws) return fail(FL_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need_ws);
+  const size_t act = (size_t)st->E * bi.T * st->d.hidden;
+  const size_t nsaved = saved_bytes(st, bi, recompute != 0);
+  if (overlap(dx, act, dy, act) || overlap(dx, act, x, act) || overlap(dx, act, saved, nsaved))
+    return fail(FL_ERR_ALIAS, "dx overlaps dy / x / saved");
+  if (overlap(ws, ws_bytes, x, act) || overlap(ws, ws_bytes, dy, act) || overlap(ws, ws_bytes, dx, act) ||
+      overlap(ws, ws_bytes, saved, nsaved))
+    return fail(FL_ERR_ALIAS, "workspace overlaps x / saved / dy / dx");
+
+  hipStream_t s = (hipStream_t)stream;
+  Carver cw(ws);
+  Work w;
+  carve_work(cw, st, bi, &w);
+  Saved sv;
+  Carver cs(const_cast<void*>(saved));
+  carve_saved(cs, st, bi.T, recompute != 0, &sv);
+  if ((rc = upload_plan(st, b, bi, w.plan, s))) return rc;
+  const int N = st->d.num_layers;
+  const void* gcur = dy;
+  for (int l = N - 1; l >= 0; --l) {
+    const void* xin = (l == 0) ? x : sv.xin[l];
+    const Acts* a = &sv.acts[l];
+    if (recompute) {
+      if ((rc = block_forward(st, bi, w.plan, layers[l], xin, w.acts, nullptr, s))) return rc;
+      a = &w.acts;
+    }
+    void* gout = (l == 0) ? dx : w.ping[(N - 1 - l) & 1];
+    if ((rc = block_backward(st, bi, w.plan, w, layers[l], grads[l], xin, *a, gcur, gout, s))) return rc;
+    gcur = gout;
+  }
+  return FL_OK;
+}
+
+static int pack_impl(fl_stack* st, const fl_batch_desc* b, const void* const* cbufs, void* packed, void* ws,
+                     size_t ws_bytes, void* stream, bool unpack) {
+  if (!st) return fail(FL_ERR_NULL, "stack is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  if (!cbufs || !packed || !ws) return fail(FL_ERR_NULL, "client buffers / packed / workspace is NULL");
+  if (!aligned16(packed) || !aligned16(ws)) return fail(FL_ERR_ALIGN, "packed / workspace must be 16-byte aligned");
+  for (int c = 0; c < bi.C; ++c) {
+    if (!cbufs[c]) return fail(FL_ERR_NULL, "client buffer %d is NULL", c);
+    if (!aligned16(cbufs[c])) return fail(FL_ERR_ALIGN, "client buffer %d is not 16-byte aligned", c);
+  }
+  const size_t need_ws = work_bytes(st, bi);
+  if (ws_bytes < need_ws) return fail(FL_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need_ws);
+  hipStream_t s = (hipStream_t)stream;
+  Carver cw(ws);
+  Work w;
+  carve_work(cw, st, bi, &w);
+  if ((rc = upload_plan(st, b, bi, w.plan, s))) return rc;
+  for (int c = 0; c < bi.C; ++c) {
+    const int s0 = b->client_seq_ptr[c], s1 = b->client_seq_ptr[c + 1];
+    int Lmax = 0;
+    for (int q = s0; q < s1; ++q) Lmax = std::max(Lmax, b->cu_seqlens[q + 1] - b->cu_seqlens[q]);
+    HIP_OK(pack_client((DType)st->d.dtype, cbufs[c], packed, w.plan.cu, s0, s1 - s0, Lmax, st->d.hidden, unpack, s));
+  }
+  return FL_OK;
+}
+
+int fl_pack_clients(fl_stack* st, const fl_batch_desc* b, const void* const* cbufs, void* packed, void* ws,
+                    size_t ws_bytes, void* stream) {
+  return pack_impl(st, b, cbufs, packed, ws, ws_bytes, stream, false);
+}
+
+int fl_unpack_clients(fl_stack* st, const fl_batch_desc* b, const void* packed, void* const* cbufs, void* ws,
+                      size_t ws_bytes, void* stream) {
+  return pack_impl(st, b, (const void* const*)cbufs, const_cast<void*>(packed), ws, ws_bytes, stream, true);
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Host-side launch functions of the device kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flglm {
+
+enum DType : int { DT_BF16 = 0, DT_F32 = 1 };
+enum GemmLayout : int { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
+
+// C[m, n] (op)= sum_k A(m, k) B(n, k); see gemm.hip for layouts and epilogues.
+struct GemmDesc {
+  const void* A = nullptr;
+  const void* B = nullptr;
+  void* C = nullptr;
+  int M = 0, N = 0, K = 0;
+  long lda = 0, ldb = 0, ldc = 0;
+  const void* bias = nullptr;
+  const void* R = nullptr;
+  long ldr = 0;
+  void* C2 = nullptr;
+  long ldc2 = 0;
+  const void* Z = nullptr;
+  long ldz = 0;
+};
+enum GemmEpi : int {
+  EPI_STORE = 0,      // C = acc
+  EPI_BIAS = 1,       // C = acc + bias
+  EPI_BIAS_RES = 2,   // C = acc + bias + R
+  EPI_BIAS_GELU = 3,  // C = z = acc + bias; C2 = gelu(z)
+  EPI_GELU_BWD = 4,   // C = acc * gelu'(Z)
+  EPI_ACC_F32 = 5,    // Cf += acc (fp32 output)
+};
+hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
+
+// Batch bookkeeping: position of every packed row inside its own sequence.
+hipError_t seq_positions(const int32_t* cu_seqlens, int num_seqs, int32_t* pos, hipStream_t st);
+// cos / sin (p * theta_i), theta_i = base^(-2i/r), p < max_pos, i < r/2 (computed in double).
+hipError_t rope_table(float* cos_t, float* sin_t, int max_pos, int rotary_dim, float base, hipStream_t st);
+// In-place rotation of the q and k parts of qkv [T, 3H] (row stride ld).
+hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* cos_t, const float* sin_t,
+                   int T, int H, int head_dim, int rotary_dim, hipStream_t st);
+
+// LayerNorm forward: y = (x - mean) * rstd * g + b, saving mean and rstd.
+hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
+                         float* rstd, int T, int H, float eps, hipStream_t st);
+// LayerNorm backward (input grad only): dx = dres + rstd*(dxh - mean(dxh) - xh*mean(dxh*xh)),
+// dxh = dy * g, xh = (x - mean) * rstd.  dres may alias nothing written here.
+hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
+                            const void* g, const void* dres, void* dx, int T, int H, hipStream_t st);
+
+// Deterministic column sums over T rows, two stages.  Stage 1 writes
+// partial[blk][n] for row blocks of kColsumRows rows; stage 2 adds the sum
+// over blocks (fixed order) into out[n] (fp32, +=).
+constexpr int kColsumRows = 256;
+inline int colsum_blocks(int T) { return (T + kColsumRows - 1) / kColsumRows; }
+// mode 0: sum_t X[t][n].  mode 1: sum_t X[t][n] * (Y[t][n] - mean[t]) * rstd[t]
+// (the LayerNorm gain gradient), written to partial; mode 1 also writes the
+// plain sum of X to partial2.
+hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const void* Y, const float* mean,
+                          const float* rstd, int T, int N, float* partial, float* partial2, hipStream_t st);
+hipError_t colsum_finish(const float* partial, int nblk, int N, float* out, hipStream_t st);
+
+// Attention over packed ragged sequences.  qkv rows are [q | k | v] (each H
+// wide, head h at columns h*d); o is [T, H]; lse is [T, nh] fp32.
+struct AttnDesc {
+  const void* qkv = nullptr;
+  long ld_qkv = 0;
+  void* o = nullptr;
+  long ld_o = 0;
+  float* lse = nullptr;  // natural-log sum-exp of scaled scores, [T, nh]
+  const int32_t* cu_seqlens = nullptr;  // device [S+1]
+  const int32_t* prefix_len = nullptr;  // device [S] or null (causal)
+  int num_seqs = 0, max_seqlen = 0, num_heads = 0, head_dim = 0, hidden = 0;
+  // backward
+  const void* dout = nullptr;
+  long ld_dout = 0;
+  float* delta = nullptr;  // [T, nh] scratch: rowsum(dO * O)
+  void* dqkv = nullptr;    // [T, 3H]
+  long ld_dqkv = 0;
+  const int32_t* pos = nullptr;  // per-row position (inverse rotary of dq, dk)
+  const float* cos_t = nullptr;
+  const float* sin_t = nullptr;
+  int rotary_dim = 0;
+  int total_tokens = 0;
+};
+hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st);
+hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st);
+
+// Client packing: client tensor [Lmax, nseq, H] (sequence-first) <-> packed
+// rows of sequences s0 .. s0+nseq-1.  Unpacking zero-fills padded positions.
+hipError_t pack_client(DType dt, const void* client, void* packed, const int32_t* cu_dev, int s0, int nseq,
+                       int Lmax, int H, bool unpack, hipStream_t st);
+
+}  // namespace flglm

@@ -1,0 +1,154 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the
+headers declare, and rejects malformed descriptors with the documented
+error codes before any device work (validation is host-only)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2406_14898_amd import flglm as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    if not os.path.exists(F.LIB_PATH):
+        from paper_2406_14898_amd import build
+        build.build()
+    return F.load()
+
+
+def _declared():
+    names = set()
+    for h in ("flglm.h", "flglm_testing.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        names |= set(re.findall(r"^\s*(?:const\s+char\s*\*|int)\s+(fl_\w+)\s*\(", src, re.M))
+    return names
+
+
+def test_exports_every_declared_symbol():
+    lib = _lib()
+    decl = _declared()
+    assert len(decl) >= 17
+    assert decl == set(F.EXPORTS)
+    for n in decl:
+        assert hasattr(lib, n), n
+
+
+def _tiny_handle(dtype=F.FL_BF16):
+    _lib()
+    return F.fl_stack_create(F.stack_desc(2, 256, 4, 1024, 32, dtype))
+
+
+@pytest.mark.parametrize("desc,code", [
+    (dict(hidden=250), F.FL_ERR_SHAPE), (dict(num_heads=3), F.FL_ERR_SHAPE),
+    (dict(num_heads=8), F.FL_ERR_SHAPE),  # head dim 32
+    (dict(ffn_hidden=1000), F.FL_ERR_SHAPE), (dict(rotary_dim=48), F.FL_ERR_SHAPE),
+    (dict(rotary_dim=96), F.FL_ERR_SHAPE), (dict(num_layers=0), F.FL_ERR_SHAPE),
+    (dict(dtype=7), F.FL_ERR_SHAPE), (dict(ln_eps=0.0), F.FL_ERR_SHAPE),
+])
+def test_stack_desc_validation(desc, code):
+    _lib()
+    base = dict(num_layers=2, hidden=256, num_heads=4, ffn_hidden=1024, rotary_dim=32, dtype=F.FL_BF16)
+    base.update(desc)
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_stack_create(F.stack_desc(**base))
+    assert e.value.code == code
+
+
+@pytest.mark.parametrize("cu,csp,pre,code", [
+    ([0, 3, 3, 7], [0, 1, 3], None, F.FL_ERR_SEQLENS),      # empty sequence
+    ([1, 3, 7], [0, 1, 2], None, F.FL_ERR_SEQLENS),         # cu[0] != 0
+    ([0, 3, 7], [0, 2, 2], None, F.FL_ERR_CLIENTS),         # client without sequences
+    ([0, 3, 7], [0, 1, 3], None, F.FL_ERR_CLIENTS),         # csp[C] != S
+    ([0, 3, 7], [1, 2], None, F.FL_ERR_CLIENTS),            # csp[0] != 0
+    ([0, 3, 7], [0, 1, 2], [0, 5], F.FL_ERR_PREFIX),        # prefix longer than its sequence
+    ([0, 3, 7], [0, 1, 2], [-1, 2], F.FL_ERR_PREFIX),
+])
+def test_batch_validation(cu, csp, pre, code):
+    h = _tiny_handle()
+    b = F.BatchDesc(cu, csp, pre)
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_stack_workspace_bytes(h, b, False)
+    assert e.value.code == code
+    F.fl_stack_destroy(h)
+
+
+def test_batch_validation_totals():
+    h = _tiny_handle()
+    b = F.BatchDesc([0, 3, 7], [0, 1, 2])
+    b.desc.total_tokens = 8
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_stack_saved_bytes(h, b, False)
+    assert e.value.code == F.FL_ERR_SEQLENS
+    b = F.BatchDesc([0, 3, 7], [0, 1, 2], max_seqlen=5)
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_stack_saved_bytes(h, b, False)
+    assert e.value.code == F.FL_ERR_SEQLENS
+    F.fl_stack_destroy(h)
+
+
+def test_client_token_range_host_only():
+    _lib()
+    b = F.BatchDesc([0, 3, 8, 12, 20], [0, 2, 3, 4])
+    assert F.fl_client_token_range(b, 0) == (0, 8)
+    assert F.fl_client_token_range(b, 1) == (8, 12)
+    assert F.fl_client_token_range(b, 2) == (12, 20)
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_client_token_range(b, 3)
+    assert e.value.code == F.FL_ERR_ARG
+
+
+def test_sizes_scale_with_tokens_and_recompute():
+    h = _tiny_handle()
+    b1 = F.BatchDesc([0, 64, 128], [0, 1, 2])
+    b2 = F.BatchDesc([0, 128, 256], [0, 1, 2])
+    s1 = F.fl_stack_saved_bytes(h, b1, False)
+    s2 = F.fl_stack_saved_bytes(h, b2, False)
+    r1 = F.fl_stack_saved_bytes(h, b1, True)
+    assert s2 > s1 > r1 > 0
+    # recompute keeps only the inputs of blocks 2..N: (N-1) * T * H * 2 bytes
+    assert r1 == 1 * 128 * 256 * 2
+    assert F.fl_stack_workspace_bytes(h, b2, False) > F.fl_stack_workspace_bytes(h, b1, False)
+    F.fl_stack_destroy(h)
+
+
+def test_forward_rejects_before_any_device_work():
+    """Bad arguments are caught on the host: no stream, no device memory
+    needed to get the error codes."""
+    h = _tiny_handle()
+    b = F.BatchDesc([0, 64, 128], [0, 1, 2])
+    ws_n = F.fl_stack_workspace_bytes(h, b, False)
+    L = F.fl_layer_params(*([16] * 12))
+    lib = F.load()
+    arr = (F.fl_layer_params * 2)(L, L)
+    # NULL x
+    rc = lib.fl_server_stack_forward(h, ctypes.byref(b.desc), arr, None, 4096, None, 0, 1 << 20, ws_n, None)
+    assert rc == F.FL_ERR_NULL
+    # misaligned y
+    rc = lib.fl_server_stack_forward(h, ctypes.byref(b.desc), arr, 1 << 30, (1 << 31) + 4, None, 0, 1 << 34, ws_n,
+                                     None)
+    assert rc == F.FL_ERR_ALIGN
+    # overlapping x / y
+    rc = lib.fl_server_stack_forward(h, ctypes.byref(b.desc), arr, 1 << 30, (1 << 30) + 4096, None, 0, 1 << 34,
+                                     ws_n, None)
+    assert rc == F.FL_ERR_ALIAS
+    # workspace too small
+    rc = lib.fl_server_stack_forward(h, ctypes.byref(b.desc), arr, 1 << 30, 1 << 31, None, 0, 1 << 34, ws_n - 1,
+                                     None)
+    assert rc == F.FL_ERR_WORKSPACE
+    # NULL parameter pointer
+    bad = (F.fl_layer_params * 2)(L, F.fl_layer_params(*([16] * 11 + [0])))
+    rc = lib.fl_server_stack_forward(h, ctypes.byref(b.desc), bad, 1 << 30, 1 << 31, None, 0, 1 << 34, ws_n, None)
+    assert rc == F.FL_ERR_NULL
+    assert "NULL" in F.fl_last_error()
+    # backward: dx overlapping dy
+    G = F.fl_layer_grads(*([16] * 12))
+    garr = (F.fl_layer_grads * 2)(G, G)
+    rc = lib.fl_server_stack_backward(h, ctypes.byref(b.desc), arr, garr, 1 << 30, 1 << 35, 1 << 31, 1 << 31, 0,
+                                      1 << 34, ws_n, None)
+    assert rc == F.FL_ERR_ALIAS
+    F.fl_stack_destroy(h)

@@ -1,0 +1,251 @@
+"""Per-kernel parity: every HIP kernel of the block against the oracle step
+it computes (or, for a bare GEMM, its plain definition), through the
+test-only C entry points.  Sizes span several tiles plus a ragged tail."""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_helpers import DTYPES, TOL, dev, dev_i32, host, rel_l2, rnd, sync
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2406_14898_amd import flglm as F  # noqa: E402
+
+DT = ["bf16", "f32"]
+
+
+# ---------------------------------------------------------------------------
+# GEMM: three layouts, every epilogue
+# ---------------------------------------------------------------------------
+
+def _gelu(z):
+    return oracle.gelu(z)
+
+
+@pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("epi", [F.FL_EPI_STORE, F.FL_EPI_BIAS, F.FL_EPI_BIAS_RES, F.FL_EPI_BIAS_GELU])
+@pytest.mark.parametrize("N", [512, 384])
+def test_gemm_nt(dt, epi, N):
+    code, tdt = DTYPES[dt]
+    M, K = 300, 320
+    A, B = rnd((M, K), 1, dt=dt), rnd((N, K), 2, 0.1, dt=dt)
+    bias, R = rnd((N,), 3, dt=dt), rnd((M, N), 4, dt=dt)
+    ref = A.astype(np.float64) @ B.astype(np.float64).T
+    if epi != F.FL_EPI_STORE:
+        ref = ref + bias
+    if epi == F.FL_EPI_BIAS_RES:
+        ref = ref + R
+    dA, dB, dbias, dR = dev(A, dt), dev(B, dt), dev(bias, dt), dev(R, dt)
+    C = torch.full((M, N), float("nan"), dtype=tdt, device="cuda")
+    C2 = torch.full((M, N), float("nan"), dtype=tdt, device="cuda")
+    F.fl_test_gemm(code, F.FL_GEMM_NT, epi, dA, dB, C, M, N, K, K, K, N, bias=dbias, R=dR, ldr=N, C2=C2, ldc2=N)
+    sync()
+    assert rel_l2(host(C), ref) < TOL[dt] / 4
+    if epi == F.FL_EPI_BIAS_GELU:
+        assert rel_l2(host(C2), _gelu(ref)) < TOL[dt] / 4
+
+
+@pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("epi", [F.FL_EPI_STORE, F.FL_EPI_GELU_BWD])
+def test_gemm_nn(dt, epi):
+    code, tdt = DTYPES[dt]
+    M, N, K = 200, 384, 448
+    A, B, Z = rnd((M, K), 5, dt=dt), rnd((K, N), 6, 0.1, dt=dt), rnd((M, N), 7, dt=dt)
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    if epi == F.FL_EPI_GELU_BWD:
+        ref = ref * oracle.gelu_grad(Z.astype(np.float64))
+    C = torch.full((M, N), float("nan"), dtype=tdt, device="cuda")
+    F.fl_test_gemm(code, F.FL_GEMM_NN, epi, dev(A, dt), dev(B, dt), C, M, N, K, K, N, N, Z=dev(Z, dt), ldz=N)
+    sync()
+    assert rel_l2(host(C), ref) < TOL[dt] / 4
+
+
+@pytest.mark.parametrize("dt", DT)
+def test_gemm_tn_accumulates(dt):
+    code, tdt = DTYPES[dt]
+    M, N, K = 272, 512, 300  # K (tokens) ragged
+    A, B = rnd((K, M), 8, dt=dt), rnd((K, N), 9, dt=dt)
+    C0 = rnd((M, N), 10, dt="f32")
+    ref = C0.astype(np.float64) + A.astype(np.float64).T @ B.astype(np.float64)
+    C = torch.from_numpy(C0).cuda()
+    F.fl_test_gemm(code, F.FL_GEMM_TN, F.FL_EPI_ACC_F32, dev(A, dt), dev(B, dt), C, M, N, K, M, N, N)
+    sync()
+    assert rel_l2(host(C), ref) < (1e-5 if dt == "f32" else 5e-3)
+
+
+def test_gemm_rejects_bad_shapes():
+    A = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(F.FlglmError):
+        F.fl_test_gemm(F.FL_BF16, F.FL_GEMM_NT, F.FL_EPI_STORE, A, A, A, 64, 100, 64, 64, 64, 100)
+    with pytest.raises(F.FlglmError):  # K not a multiple of 64 with a K-contiguous operand
+        F.fl_test_gemm(F.FL_BF16, F.FL_GEMM_NT, F.FL_EPI_STORE, A, A, A, 64, 128, 40, 64, 64, 128)
+    with pytest.raises(F.FlglmError):  # unsupported layout / epilogue pair
+        F.fl_test_gemm(F.FL_BF16, F.FL_GEMM_TN, F.FL_EPI_BIAS, A, A, A, 64, 128, 64, 64, 128, 128)
+
+
+# ---------------------------------------------------------------------------
+# LayerNorm and column sums
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("H", [256, 4096])
+def test_layernorm_fwd_bwd(dt, H):
+    code, tdt = DTYPES[dt]
+    T = 37
+    x = rnd((T, H), 11, 2.0, dt=dt) + np.float32(0.5)
+    x = synth.bf16_round(x) if dt == "bf16" else x
+    g = rnd((H,), 12, 0.1, dt=dt) + np.float32(1.0)
+    g = synth.bf16_round(g) if dt == "bf16" else g
+    b = rnd((H,), 13, 0.1, dt=dt)
+    y_ref, xhat, rstd = oracle.layer_norm(x.astype(np.float64), g, b, 1e-5)
+    dx_, dg_, db_ = dev(x, dt), dev(g, dt), dev(b, dt)
+    y = torch.empty((T, H), dtype=tdt, device="cuda")
+    mean = torch.empty(T, dtype=torch.float32, device="cuda")
+    rs = torch.empty(T, dtype=torch.float32, device="cuda")
+    F.fl_test_layernorm_fwd(code, dx_, dg_, db_, y, mean, rs, T, H, 1e-5)
+    sync()
+    assert rel_l2(host(y), y_ref) < TOL[dt] / 4
+    assert rel_l2(host(rs), rstd[:, 0]) < 1e-5
+    assert rel_l2(host(mean), x.astype(np.float64).mean(1)) < 1e-5
+
+    dy = rnd((T, H), 14, dt=dt)
+    dres = rnd((T, H), 15, dt=dt)
+    dxr, dgr, dbr = oracle.layer_norm_backward(dy.astype(np.float64), xhat, rstd, g.astype(np.float64))
+    out = torch.empty((T, H), dtype=tdt, device="cuda")
+    F.fl_test_layernorm_bwd(code, dev(dy, dt), dx_, mean, rs, dg_, dev(dres, dt), out, T, H)
+    sync()
+    assert rel_l2(host(out), dxr + dres) < TOL[dt] / 4
+    og = torch.zeros(H, dtype=torch.float32, device="cuda")
+    ob = torch.ones(H, dtype=torch.float32, device="cuda")
+    part = torch.empty(2 * H * ((T + 255) // 256), dtype=torch.float32, device="cuda")
+    F.fl_test_colsum(code, 1, dev(dy, dt), dx_, mean, rs, T, H, og, ob, part)
+    sync()
+    assert rel_l2(host(og), dgr) < 1e-4
+    assert rel_l2(host(ob), dbr + 1.0) < 1e-5
+
+
+@pytest.mark.parametrize("dt", DT)
+def test_colsum_many_blocks(dt):
+    code, _ = DTYPES[dt]
+    T, N = 1000, 1536
+    X = rnd((T, N), 16, dt=dt)
+    out = torch.zeros(N, dtype=torch.float32, device="cuda")
+    part = torch.empty(2 * N * ((T + 255) // 256), dtype=torch.float32, device="cuda")
+    F.fl_test_colsum(code, 0, dev(X, dt), None, None, None, T, N, out, None, part)
+    F.fl_test_colsum(code, 0, dev(X, dt), None, None, None, T, N, out, None, part)
+    sync()
+    assert rel_l2(host(out), 2 * X.astype(np.float64).sum(0)) < 1e-5
+
+
+# ---------------------------------------------------------------------------
+# Rotary and attention
+# ---------------------------------------------------------------------------
+
+BATCHES = {
+    "ragged_causal": synth.Batch(np.array([0, 1, 6, 70, 135, 335], np.int32), np.array([0, 2, 5], np.int32)),
+    "ragged_prefix": synth.Batch(np.array([0, 1, 6, 70, 135, 335], np.int32), np.array([0, 2, 5], np.int32),
+                                 "prefix", np.array([0, 3, 16, 65, 150], np.int32)),
+}
+
+
+def _qkv(T, H, seed, dt):
+    return rnd((T, 3 * H), seed, dt=dt)
+
+
+@pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
+def test_rope_inplace(dt, heads):
+    code, tdt = DTYPES[dt]
+    nh, d = heads
+    H = nh * d
+    r = d // 2
+    b = BATCHES["ragged_causal"]
+    T = b.total_tokens
+    qkv = _qkv(T, H, 20, dt)
+    t = dev(qkv, dt)
+    pos = torch.empty(T, dtype=torch.int32, device="cuda")
+    ct = torch.empty(b.max_seqlen * r // 2, dtype=torch.float32, device="cuda")
+    st = torch.empty_like(ct)
+    F.fl_test_rope(code, t, dev_i32(b.cu_seqlens), b.num_seqs, T, b.max_seqlen, H, nh, r, 10000.0, pos, ct, st)
+    sync()
+    p = oracle.positions(b.cu_seqlens)
+    np.testing.assert_array_equal(pos.cpu().numpy(), p)
+    cos, sin = oracle.rope_tables(p, r, 10000.0)
+    out = host(t)
+    q = oracle.rope(qkv[:, :H].astype(np.float64).reshape(T, nh, d), cos, sin, r).reshape(T, H)
+    k = oracle.rope(qkv[:, H:2 * H].astype(np.float64).reshape(T, nh, d), cos, sin, r).reshape(T, H)
+    assert rel_l2(out[:, :H], q) < TOL[dt] / 4
+    assert rel_l2(out[:, H:2 * H], k) < TOL[dt] / 4
+    np.testing.assert_array_equal(out[:, 2 * H:], qkv[:, 2 * H:])
+
+
+def _lse_ref(q, k, b):
+    T, nh, d = q.shape
+    out = np.zeros((T, nh))
+    for s in range(b.num_seqs):
+        r0, r1 = int(b.cu_seqlens[s]), int(b.cu_seqlens[s + 1])
+        P = int(b.prefix_len[s]) if b.mask == "prefix" else None
+        allowed = oracle.allowed_mask(r1 - r0, P)
+        for h in range(nh):
+            S = q[r0:r1, h] @ k[r0:r1, h].T / math.sqrt(d)
+            S = np.where(allowed, S, -np.inf)
+            m = S.max(1, keepdims=True)
+            out[r0:r1, h] = (m + np.log(np.exp(S - m).sum(1, keepdims=True)))[:, 0]
+    return out
+
+
+@pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
+@pytest.mark.parametrize("bname", list(BATCHES))
+def test_attention_fwd_bwd(dt, heads, bname):
+    code, tdt = DTYPES[dt]
+    nh, d = heads
+    H = nh * d
+    b = BATCHES[bname]
+    T = b.total_tokens
+    qkv = _qkv(T, H, 21, dt)
+    q = qkv[:, :H].astype(np.float64).reshape(T, nh, d)
+    k = qkv[:, H:2 * H].astype(np.float64).reshape(T, nh, d)
+    v = qkv[:, 2 * H:].astype(np.float64).reshape(T, nh, d)
+    o_ref = oracle.attention_forward(q, k, v, b).reshape(T, H)
+    cu = dev_i32(b.cu_seqlens)
+    pre = dev_i32(b.prefix_len) if b.mask == "prefix" else None
+    t = dev(qkv, dt)
+    o = torch.full((T, H), float("nan"), dtype=tdt, device="cuda")
+    lse = torch.full((T, nh), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_fwd(code, t, o, lse, cu, pre, T, b.num_seqs, b.max_seqlen, H, nh)
+    sync()
+    assert rel_l2(host(o), o_ref) < TOL[dt] / 2
+    assert rel_l2(host(lse), _lse_ref(q, k, b)) < 1e-5
+
+    # backward, with and without the inverse rotation of dq, dk
+    do = rnd((T, H), 22, dt=dt)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b)
+    for r in (0, d // 2):
+        dqr, dkr = dq, dk
+        pos = ct = st = None
+        if r:
+            p = oracle.positions(b.cu_seqlens)
+            cos, sin = oracle.rope_tables(p, r, 10000.0)
+            dqr = oracle.rope(dq, cos, sin, r, inverse=True)
+            dkr = oracle.rope(dk, cos, sin, r, inverse=True)
+            pos = torch.empty(T, dtype=torch.int32, device="cuda")
+            ct = torch.empty(b.max_seqlen * r // 2, dtype=torch.float32, device="cuda")
+            st = torch.empty_like(ct)
+            scratch = torch.zeros((T, 3 * H), dtype=tdt, device="cuda")  # rope on a scratch copy fills the tables
+            F.fl_test_rope(code, scratch, cu, b.num_seqs, T, b.max_seqlen, H, nh, r, 10000.0, pos, ct, st)
+        dqkv = torch.full((T, 3 * H), float("nan"), dtype=tdt, device="cuda")
+        delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+        F.fl_test_attention_bwd(code, t, o, lse, dev(do, dt), dqkv, delta, cu, pre, pos, ct, st, r, T, b.num_seqs,
+                                b.max_seqlen, H, nh)
+        sync()
+        g = host(dqkv)
+        tol = TOL[dt] / 2
+        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
