@@ -166,6 +166,34 @@ int fl_pack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* con
 int fl_unpack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* packed, void* const* client_bufs,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Launch timing (off by default).  While enabled, every kernel launch the
+ * handle enqueues is bracketed by two HIP events on the call's stream and
+ * tagged with its class and its algorithmic work (flops of the contraction,
+ * minimal HBM bytes).  Enabling clears earlier records.  The overhead is two
+ * event records per launch. */
+#define FL_PROF_PLAN 0              /* positions + rotary table */
+#define FL_PROF_LAYERNORM_FWD 1
+#define FL_PROF_GEMM_NT_BIAS 2      /* QKV projection */
+#define FL_PROF_ROPE 3
+#define FL_PROF_ATTN_FWD 4
+#define FL_PROF_GEMM_NT_BIAS_RES 5  /* output projection, FFN2 (+ residual) */
+#define FL_PROF_GEMM_NT_BIAS_GELU 6 /* FFN1 + GeLU */
+#define FL_PROF_GEMM_TN_ACC 7       /* weight gradients (fp32 +=) */
+#define FL_PROF_GEMM_NN_GELU_BWD 8  /* FFN2 input gradient x GeLU' */
+#define FL_PROF_GEMM_NN 9           /* other input gradients */
+#define FL_PROF_LAYERNORM_BWD 10
+#define FL_PROF_COLSUM 11           /* bias and LayerNorm parameter gradients */
+#define FL_PROF_ATTN_BWD 12
+#define FL_PROF_NUM_CLASSES 13
+int fl_stack_profile(fl_stack* stack, int enable);
+/* Totals for one class over the records since profiling was enabled:
+ * launch count, summed event time (ms), algorithmic flops and bytes.
+ * Waits for the recorded events. */
+int fl_stack_profile_read(fl_stack* stack, int cls, int64_t* launches, double* milliseconds, double* flops,
+                          double* bytes);
+/* Name of a profiling class ("" when out of range). */
+const char* fl_profile_class_name(int cls);
+
 /* Thread-local description of the last error returned on this thread. */
 const char* fl_last_error(void);
 

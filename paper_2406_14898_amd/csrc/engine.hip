@@ -36,6 +36,11 @@ int fail(int code, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(FL_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
+// Enqueue one launch (an expression returning hipError_t) with its algorithmic
+// flops and bytes; timed when profiling is on.  Needs `st` and `s` in scope.
+#define LAUNCH(cls, flops, bytes, ...) \
+  HIP_OK(timed(st, s, (cls), (flops), (bytes), [&]() { return (__VA_ARGS__); }))
+
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -70,13 +75,57 @@ struct fl_stack {
   bool ev_made[kRing] = {};
   bool ev_used[kRing] = {};
   int next = 0;
+  // opt-in launch timing (fl_stack_profile)
+  struct Rec {
+    int cls;
+    hipEvent_t a, b;
+    double flops, bytes;
+  };
+  bool prof = false;
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
 };
+
+
+namespace {
+
+const char* const kProfNames[FL_PROF_NUM_CLASSES] = {
+    "plan",          "layernorm_fwd", "gemm_nt_bias", "rope_qk",  "attn_fwd",     "gemm_nt_bias_res", "gemm_nt_bias_gelu",
+    "gemm_tn_acc",   "gemm_nn_gelu_bwd", "gemm_nn",   "layernorm_bwd", "colsum", "attn_bwd"};
+
+hipError_t take_event(fl_stack* st, hipEvent_t* e) {
+  if (!st->pool.empty()) {
+    *e = st->pool.back();
+    st->pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+
+// Runs `launch` (returning hipError_t); when profiling is on, brackets it
+// with two events on stream s and records the launch's algorithmic work.
+template <class Fn>
+hipError_t timed(fl_stack* st, hipStream_t s, int cls, double flops, double bytes, Fn&& launch) {
+  if (!st->prof) return launch();
+  fl_stack::Rec r{cls, nullptr, nullptr, flops, bytes};
+  hipError_t e = take_event(st, &r.a);
+  if (e != hipSuccess) return e;
+  if ((e = take_event(st, &r.b)) != hipSuccess) return e;
+  if ((e = hipEventRecord(r.a, s)) != hipSuccess) return e;
+  e = launch();
+  hipError_t e2 = hipEventRecord(r.b, s);
+  st->recs.push_back(r);
+  return e != hipSuccess ? e : e2;
+}
+
+}  // namespace
 
 namespace {
 
 struct BatchInfo {
   int T, S, C, maxL;
   bool prefix;
+  double pairs;  // sum over sequences of visible (query, key) pairs
 };
 
 int validate_batch(const fl_batch_desc* b, BatchInfo* bi) {
@@ -121,6 +170,13 @@ int validate_batch(const fl_batch_desc* b, BatchInfo* bi) {
   bi->C = b->num_clients;
   bi->maxL = maxL;
   bi->prefix = b->mask_kind == FL_MASK_PREFIX;
+  bi->pairs = 0;
+  for (int s = 0; s < b->num_seqs; ++s) {
+    const double L = cu[s + 1] - cu[s];
+    const double P = bi->prefix ? b->prefix_len[s] : 0;
+    // causal pairs L(L+1)/2, plus the pairs a bidirectional prefix adds
+    bi->pairs += L * (L + 1) / 2 + (P > 1 ? P * (P - 1) / 2 : 0);
+  }
   return FL_OK;
 }
 
@@ -295,10 +351,17 @@ int upload_plan(fl_stack* st, const fl_batch_desc* b, const BatchInfo& bi, const
   HIP_OK(hipMemcpyAsync(p.prefix, h + ncu, sizeof(int32_t) * npre, hipMemcpyHostToDevice, stream));
   HIP_OK(hipEventRecord(st->ev[k], stream));
   st->ev_used[k] = true;
-  HIP_OK(seq_positions(p.cu, bi.S, p.pos, stream));
-  HIP_OK(rope_table(p.cos_t, p.sin_t, bi.maxL, st->d.rotary_dim, st->d.rope_base, stream));
+  hipStream_t s = stream;
+  LAUNCH(FL_PROF_PLAN, 0, 4.0 * bi.T, [&]() {
+    hipError_t e = seq_positions(p.cu, bi.S, p.pos, stream);
+    return e != hipSuccess ? e : rope_table(p.cos_t, p.sin_t, bi.maxL, st->d.rotary_dim, st->d.rope_base, stream);
+  }());
   return FL_OK;
 }
+
+// Algorithmic work of one launch, for the opt-in launch timing.
+double gemm_flops(double M, double N, double K) { return 2.0 * M * N * K; }
+double gemm_bytes(double M, double N, double K, double E, double Eout) { return (M * K + N * K) * E + M * N * Eout; }
 
 // ---------------------------------------------------------------------------
 // One block forward.  `out` may be NULL (recompute for the backward: the
@@ -308,39 +371,66 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
                   const Acts& a, void* out, hipStream_t s) {
   const DType dt = (DType)st->d.dtype;
   const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
-  HIP_OK(layernorm_fwd(dt, x, p.ln1_g, p.ln1_b, a.u, a.mean1, a.rstd1, T, H, st->d.ln_eps, s));
+  const double E = st->E, TH = (double)T * H;
+  LAUNCH(FL_PROF_LAYERNORM_FWD, 0, 2 * TH * E + 8.0 * T,
+         layernorm_fwd(dt, x, p.ln1_g, p.ln1_b, a.u, a.mean1, a.rstd1, T, H, st->d.ln_eps, s));
   GemmDesc g;
   g.A = a.u; g.B = p.w_qkv; g.C = a.qkv; g.M = T; g.N = 3 * H; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = 3 * H; g.bias = p.b_qkv;
-  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS, g, s));
-  HIP_OK(rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
+  LAUNCH(FL_PROF_GEMM_NT_BIAS, gemm_flops(T, 3 * H, H), gemm_bytes(T, 3 * H, H, E, E),
+         gemm(dt, GEMM_NT, EPI_BIAS, g, s));
+  LAUNCH(FL_PROF_ROPE, 0, 4 * TH * E,
+         rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
   ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;
   ad.num_seqs = bi.S; ad.max_seqlen = bi.maxL; ad.num_heads = st->d.num_heads; ad.head_dim = st->hd;
   ad.hidden = H; ad.total_tokens = T;
-  HIP_OK(attn_fwd(dt, ad, s));
+  LAUNCH(FL_PROF_ATTN_FWD, 4.0 * H * bi.pairs, 4 * TH * E + 4.0 * T * st->d.num_heads, attn_fwd(dt, ad, s));
   g = GemmDesc();
   g.A = a.o; g.B = p.w_o; g.C = a.h; g.M = T; g.N = H; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.R = x; g.ldr = H;
-  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
-  HIP_OK(layernorm_fwd(dt, a.h, p.ln2_g, p.ln2_b, a.w, a.mean2, a.rstd2, T, H, st->d.ln_eps, s));
+  LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E) + TH * E,
+         gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+  LAUNCH(FL_PROF_LAYERNORM_FWD, 0, 2 * TH * E + 8.0 * T,
+         layernorm_fwd(dt, a.h, p.ln2_g, p.ln2_b, a.w, a.mean2, a.rstd2, T, H, st->d.ln_eps, s));
   g = GemmDesc();
   g.A = a.w; g.B = p.w_1; g.C = a.z; g.C2 = a.g; g.M = T; g.N = F; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = F; g.ldc2 = F; g.bias = p.b_1;
-  HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_GELU, g, s));
+  LAUNCH(FL_PROF_GEMM_NT_BIAS_GELU, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
+         gemm(dt, GEMM_NT, EPI_BIAS_GELU, g, s));
   if (out) {
     g = GemmDesc();
     g.A = a.g; g.B = p.w_2; g.C = out; g.M = T; g.N = H; g.K = F;
     g.lda = F; g.ldb = F; g.ldc = H; g.bias = p.b_2; g.R = a.h; g.ldr = H;
-    HIP_OK(gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+    LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E) + TH * E,
+           gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
   }
   return FL_OK;
 }
 
-int colsum_into(DType dt, const void* X, long ldx, int T, int N, float* out, const Work& w, hipStream_t s) {
-  HIP_OK(colsum_partial(dt, 0, X, ldx, nullptr, nullptr, nullptr, T, N, w.part, nullptr, s));
-  HIP_OK(colsum_finish(w.part, colsum_blocks(T), N, out, s));
+// out[n] += sum_t X[t][n] (two-stage, deterministic).
+int colsum_into(fl_stack* st, DType dt, const void* X, long ldx, int T, int N, float* out, const Work& w,
+                hipStream_t s) {
+  LAUNCH(FL_PROF_COLSUM, 0, (double)T * N * st->E, [&]() {
+    hipError_t e = colsum_partial(dt, 0, X, ldx, nullptr, nullptr, nullptr, T, N, w.part, nullptr, s);
+    return e != hipSuccess ? e : colsum_finish(w.part, colsum_blocks(T), N, out, s);
+  }());
+  return FL_OK;
+}
+
+// LayerNorm backward: dx = dres + LN^T(dy); gain/shift gradients += column sums.
+int ln_backward(fl_stack* st, DType dt, const void* dy, const void* xin, const float* mean, const float* rstd,
+                const void* gamma, const void* dres, void* dx, float* dgamma, float* dbeta, int T, int H,
+                const Work& w, hipStream_t s) {
+  const double TH = (double)T * H, E = st->E;
+  LAUNCH(FL_PROF_LAYERNORM_BWD, 0, 4 * TH * E + 8.0 * T,
+         layernorm_bwd_dx(dt, dy, xin, mean, rstd, gamma, dres, dx, T, H, s));
+  LAUNCH(FL_PROF_COLSUM, 0, 2 * TH * E + 8.0 * T, [&]() {
+    hipError_t e = colsum_partial(dt, 1, dy, H, xin, mean, rstd, T, H, w.part, w.part2, s);
+    if (e == hipSuccess) e = colsum_finish(w.part, colsum_blocks(T), H, dgamma, s);
+    return e != hipSuccess ? e : colsum_finish(w.part2, colsum_blocks(T), H, dbeta, s);
+  }());
   return FL_OK;
 }
 
@@ -349,37 +439,37 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
                    const fl_layer_grads& gr, const void* x, const Acts& a, const void* dy, void* dx, hipStream_t s) {
   const DType dt = (DType)st->d.dtype;
   const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
+  const double E = st->E;
   int rc;
   // y = h + g W_2^T + b_2
-  if ((rc = colsum_into(dt, dy, H, T, H, gr.b_2, w, s))) return rc;
+  if ((rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
   GemmDesc g;
   g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
-  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
   g = GemmDesc();
   g.A = dy; g.B = p.w_2; g.C = w.dz; g.M = T; g.N = F; g.K = H; g.lda = H; g.ldb = F; g.ldc = F;
   g.Z = a.z; g.ldz = F;
-  HIP_OK(gemm(dt, GEMM_NN, EPI_GELU_BWD, g, s));
+  LAUNCH(FL_PROF_GEMM_NN_GELU_BWD, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
+         gemm(dt, GEMM_NN, EPI_GELU_BWD, g, s));
   // z = w W_1^T + b_1
-  if ((rc = colsum_into(dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
+  if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
   g = GemmDesc();
   g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
   g = GemmDesc();
   g.A = w.dz; g.B = p.w_1; g.C = w.tmp; g.M = T; g.N = H; g.K = F; g.lda = F; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E), gemm(dt, GEMM_NN, EPI_STORE, g, s));
   // w = LN2(h); h also feeds y directly
-  HIP_OK(layernorm_bwd_dx(dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, T, H, s));
-  HIP_OK(colsum_partial(dt, 1, w.tmp, H, a.h, a.mean2, a.rstd2, T, H, w.part, w.part2, s));
-  HIP_OK(colsum_finish(w.part, colsum_blocks(T), H, gr.ln2_g, s));
-  HIP_OK(colsum_finish(w.part2, colsum_blocks(T), H, gr.ln2_b, s));
+  if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, gr.ln2_g, gr.ln2_b, T, H, w, s)))
+    return rc;
   // h = x + o W_o^T + b_o
-  if ((rc = colsum_into(dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
+  if ((rc = colsum_into(st, dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
   g = GemmDesc();
   g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
   g = GemmDesc();
   g.A = w.dh; g.B = p.w_o; g.C = w.tmp; g.M = T; g.N = H; g.K = H; g.lda = H; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E), gemm(dt, GEMM_NN, EPI_STORE, g, s));
   // attention (dq, dk, dv with the inverse rotation applied)
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
@@ -388,21 +478,19 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.hidden = H; ad.total_tokens = T;
   ad.dout = w.tmp; ad.ld_dout = H; ad.delta = w.delta; ad.dqkv = w.dqkv; ad.ld_dqkv = 3 * H;
   ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t; ad.rotary_dim = st->d.rotary_dim;
-  HIP_OK(attn_bwd(dt, ad, s));
+  LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * bi.pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
   // qkv = u W_qkv^T + b_qkv
-  if ((rc = colsum_into(dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
+  if ((rc = colsum_into(st, dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
   g = GemmDesc();
   g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(3 * H, H, T), gemm_bytes(3 * H, H, T, E, 8),
+         gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
   g = GemmDesc();
   g.A = w.dqkv; g.B = p.w_qkv; g.C = w.tmp; g.M = T; g.N = H; g.K = 3 * H; g.lda = 3 * H; g.ldb = H; g.ldc = H;
-  HIP_OK(gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, 3 * H), gemm_bytes(T, H, 3 * H, E, E),
+         gemm(dt, GEMM_NN, EPI_STORE, g, s));
   // u = LN1(x); x also feeds h directly
-  HIP_OK(layernorm_bwd_dx(dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, w.dh, dx, T, H, s));
-  HIP_OK(colsum_partial(dt, 1, w.tmp, H, x, a.mean1, a.rstd1, T, H, w.part, w.part2, s));
-  HIP_OK(colsum_finish(w.part, colsum_blocks(T), H, gr.ln1_g, s));
-  HIP_OK(colsum_finish(w.part2, colsum_blocks(T), H, gr.ln1_b, s));
-  return FL_OK;
+  return ln_backward(st, dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, w.dh, dx, gr.ln1_g, gr.ln1_b, T, H, w, s);
 }
 
 }  // namespace
@@ -434,6 +522,12 @@ int fl_stack_create(const fl_stack_desc* desc, fl_stack** out) {
 int fl_stack_destroy(fl_stack* st) {
   if (!st) return FL_OK;
   int rc = FL_OK;
+  for (auto& r : st->recs) {
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+  }
+  for (hipEvent_t e : st->pool)
+    if (hipEventDestroy(e) != hipSuccess) rc = FL_ERR_HIP;
   for (int k = 0; k < fl_stack::kRing; ++k) {
     if (st->ev_used[k] && hipEventSynchronize(st->ev[k]) != hipSuccess) rc = FL_ERR_HIP;
     if (st->stage[k] && hipHostFree(st->stage[k]) != hipSuccess) rc = FL_ERR_HIP;
@@ -442,6 +536,41 @@ int fl_stack_destroy(fl_stack* st) {
   delete st;
   if (rc) return fail(rc, "HIP error while releasing the handle");
   return FL_OK;
+}
+
+int fl_stack_profile(fl_stack* st, int enable) {
+  if (!st) return fail(FL_ERR_NULL, "stack is NULL");
+  if (enable) {
+    for (auto& r : st->recs) {
+      st->pool.push_back(r.a);
+      st->pool.push_back(r.b);
+    }
+    st->recs.clear();
+  }
+  st->prof = enable != 0;
+  return FL_OK;
+}
+
+int fl_stack_profile_read(fl_stack* st, int cls, int64_t* launches, double* ms, double* flops, double* bytes) {
+  if (!st || !launches || !ms || !flops || !bytes) return fail(FL_ERR_NULL, "NULL argument");
+  if (cls < 0 || cls >= FL_PROF_NUM_CLASSES) return fail(FL_ERR_ARG, "profile class %d out of range", cls);
+  *launches = 0;
+  *ms = *flops = *bytes = 0.0;
+  for (auto& r : st->recs) {
+    if (r.cls != cls) continue;
+    HIP_OK(hipEventSynchronize(r.b));
+    float t = 0.f;
+    HIP_OK(hipEventElapsedTime(&t, r.a, r.b));
+    *launches += 1;
+    *ms += t;
+    *flops += r.flops;
+    *bytes += r.bytes;
+  }
+  return FL_OK;
+}
+
+const char* fl_profile_class_name(int cls) {
+  return (cls >= 0 && cls < FL_PROF_NUM_CLASSES) ? kProfNames[cls] : "";
 }
 
 int fl_stack_saved_bytes(const fl_stack* st, const fl_batch_desc* b, int recompute, size_t* bytes) {

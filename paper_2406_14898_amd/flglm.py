@@ -24,6 +24,7 @@ FL_BF16, FL_F32 = 0, 1
 FL_MASK_CAUSAL, FL_MASK_PREFIX = 0, 1
 FL_GEMM_NT, FL_GEMM_NN, FL_GEMM_TN = 0, 1, 2
 FL_EPI_STORE, FL_EPI_BIAS, FL_EPI_BIAS_RES, FL_EPI_BIAS_GELU, FL_EPI_GELU_BWD, FL_EPI_ACC_F32 = range(6)
+FL_PROF_NUM_CLASSES = 13
 
 PARAM_FIELDS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
                 "ln1_g", "ln1_b", "ln2_g", "ln2_b")
@@ -33,6 +34,7 @@ EXPORTS = (
     "fl_stack_create", "fl_stack_destroy", "fl_stack_saved_bytes", "fl_stack_workspace_bytes",
     "fl_server_stack_forward", "fl_server_stack_backward", "fl_client_token_range",
     "fl_pack_clients", "fl_unpack_clients", "fl_last_error",
+    "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_colsum",
     "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
 )
@@ -91,6 +93,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_client_token_range": [P(fl_batch_desc), i32, P(i64), P(i64)],
         "fl_pack_clients": [vp, P(fl_batch_desc), P(vp), vp, vp, sz, vp],
         "fl_unpack_clients": [vp, P(fl_batch_desc), vp, P(vp), vp, sz, vp],
+        "fl_stack_profile": [vp, ctypes.c_int],
+        "fl_stack_profile_read": [vp, ctypes.c_int, P(i64), P(ctypes.c_double), P(ctypes.c_double),
+                                  P(ctypes.c_double)],
         "fl_test_gemm": [ctypes.c_int] * 3 + [vp] * 3 + [ctypes.c_int] * 3 + [i64] * 3 + [vp, vp, i64, vp, i64, vp,
                                                                                           i64, vp],
         "fl_test_layernorm_fwd": [ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float,
@@ -107,6 +112,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         f.restype = ctypes.c_int
     lib.fl_last_error.argtypes = []
     lib.fl_last_error.restype = ctypes.c_char_p
+    lib.fl_profile_class_name.argtypes = [ctypes.c_int]
+    lib.fl_profile_class_name.restype = ctypes.c_char_p
     _lib = lib
     return lib
 
@@ -247,6 +254,32 @@ def fl_unpack_clients(handle: int, batch: BatchDesc, packed, client_bufs, worksp
     arr = (ctypes.c_void_p * len(client_bufs))(*[_ptr(c) for c in client_bufs])
     _check(load().fl_unpack_clients(handle, ctypes.byref(batch.desc), _ptr(packed), arr, _ptr(workspace),
                                     workspace_bytes, _stream(stream)))
+
+
+def fl_stack_profile(handle: int, enable: bool) -> None:
+    _check(load().fl_stack_profile(handle, int(enable)))
+
+
+def fl_profile_class_name(cls: int) -> str:
+    return load().fl_profile_class_name(cls).decode()
+
+
+def fl_stack_profile_read(handle: int, cls: int):
+    """(launches, milliseconds, flops, bytes) for one class; waits for the events."""
+    n, ms, fl, by = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(load().fl_stack_profile_read(handle, cls, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl),
+                                        ctypes.byref(by)))
+    return n.value, ms.value, fl.value, by.value
+
+
+def profile_table(handle: int):
+    """{class name: dict(launches, ms, flops, bytes)} for every class with launches."""
+    out = {}
+    for c in range(FL_PROF_NUM_CLASSES):
+        n, ms, fl, by = fl_stack_profile_read(handle, c)
+        if n:
+            out[fl_profile_class_name(c)] = dict(launches=n, ms=ms, flops=fl, bytes=by)
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -51,9 +51,9 @@ def bf16_bits(a: np.ndarray) -> np.ndarray:
     branch only keeps the encoding total.
     """
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    u = a.view(np.uint32)
+    # no overflow for any non-NaN pattern: the largest is 0xFF800000 (-inf)
+    r = ((u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) >> np.uint32(16)).astype(np.uint16)
     nan = np.isnan(a)
     if nan.any():
         r[nan] = 0x7FC0
