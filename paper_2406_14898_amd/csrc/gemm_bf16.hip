@@ -1,0 +1,358 @@
+// bf16 GEMM for gfx950: C[m, n] (op)= sum_k A(m, k) B(n, k), fp32 accumulate.
+//
+// Same contract and epilogues as gemm.hip, specialised for the throughput
+// path:
+//   * 256 x 256 output tile per workgroup, 8 waves (two per SIMD, so one
+//     wave's LDS waits are covered by the other's matrix-core work) of
+//     128 x 64, reduction stages of 64 double-buffered in LDS (128 KB): a
+//     DMA row segment is one full 128-byte line;
+//   * operands go from HBM/L2 straight into LDS with buffer loads in LDS-DMA
+//     mode (no VGPR staging).  Buffer resources bound each operand, so rows
+//     or reduction indices past the end read as zero (ragged token tails);
+//   * each operand stays in LDS in (blocks of) its global layout.
+//     K-contiguous tiles are [256 rows][64] and feed the matrix core with
+//     16-byte reads; MN-contiguous tiles are 4 column blocks of [64 k][64] and
+//     feed it with transpose reads (ds_read_b64_tr_b16: lane j of a 16-lane
+//     group receives four consecutive-k values of column j when lane s points
+//     at (k0 + s/4, c0 + 4 (s % 4)));
+//   * layouts are chosen so that every fragment address is one per-lane base
+//     plus a compile-time offset (the swizzle of K-contiguous rows depends on
+//     the lane only), which keeps the address arithmetic out of the VGPR
+//     budget;
+//   * an LDS-DMA lane always writes to base + 16 * lane, so swizzles are
+//     applied to the source addresses;
+//   * one barrier per stage, placed between the two 32-wide halves: the
+//     second half's fragments are already in registers when the barrier
+//     releases the slot, so the next stage's loads and fragment reads overlap
+//     matrix-core work.
+#include "common.h"
+#include "kernels.h"
+
+namespace flglm {
+namespace {
+
+constexpr int kBM = 256, kBN = 256, kBK = 64, kStages = 2, kThr = 512, kWaves = 8;
+// waves: 2 along M x 4 along N, each 128 x 64 (8 x 4 tiles of 16 x 16)
+constexpr int kWTM = 8, kWTN = 4;
+constexpr int kTileElems = 256 * kBK;  // one operand tile per stage (32 KB)
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+struct G2Args {
+  const bf16* A;
+  const bf16* B;
+  void* C;
+  int M, N, K;
+  long lda, ldb, ldc;
+  const bf16* bias;
+  const bf16* R;
+  long ldr;
+  bf16* C2;
+  long ldc2;
+  const bf16* Z;
+  long ldz;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
+// slot q ^ swz_k(r).  With this swizzle the fragment reads (16 consecutive
+// rows, one chunk each) are free of LDS bank conflicts on gfx950 (measured
+// with SQ_LDS_BANK_CONFLICT; (r ^ (r >> 3)) & 7, for instance, doubles the
+// read time).
+__device__ __forceinline__ int swz_k(int row) { return row & 7; }
+// MN-contiguous blocks: k-row k holds 8 chunks; chunk q sits at q ^ swz_m(k).
+// A transpose read serves 32 lanes per cycle: k-rows kb .. kb+3 and
+// kb+8 .. kb+11, 32 bytes each; k bits 1 and 3 move those eight segments
+// onto disjoint banks.
+__device__ __forceinline__ int swz_m(int k) { return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2); }
+
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, bf16* lds_inst_base, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LDS_AS void*)lds_inst_base, 16, voff, 0, 0, 0);
+}
+
+// K-contiguous tile [256 rows][64]: 2048 chunks, 4 DMA instructions per wave.
+__device__ __forceinline__ void load_k_tile(__amdgpu_buffer_rsrc_t rs, long ld, int k0, bf16* tile, int wave,
+                                            int lane) {
+#pragma unroll
+  for (int i = 0; i < 32 / kWaves; ++i) {
+    const int inst = i * kWaves + wave;
+    const int lin = inst * 64 + lane;
+    const int row = lin >> 3, q = (lin & 7) ^ swz_k(row);
+    dma16(rs, tile + inst * 512, (uint32_t)(row * ld + k0 + q * 8) * 2u);
+  }
+}
+
+// MN-contiguous tile: 4 column blocks of [64 k][64 columns] (8 KB each); a
+// DMA instruction fills 8 k-rows of 128 bytes; 4 per wave.
+__device__ __forceinline__ void load_m_tile(__amdgpu_buffer_rsrc_t rs, long ld, int k0, bf16* tile, int wave,
+                                            int lane) {
+#pragma unroll
+  for (int i = 0; i < 32 / kWaves; ++i) {
+    const int inst = i * kWaves + wave;  // 0..31: block inst/8, k-rows 8*(inst%8) ..
+    const int blk = inst >> 3, krow = (inst & 7) * 8 + (lane >> 3);
+    const int q = (lane & 7) ^ swz_m(krow);
+    dma16(rs, tile + inst * 512, (uint32_t)((long)(k0 + krow) * ld + blk * 64 + q * 8) * 2u);
+  }
+}
+
+// Per-lane fragment bases (element offsets inside one operand tile).
+// K-contiguous: fragment j of a wave (rows row0 + 16 j), reduction half c =
+// base(c) + 1024 j, base(1) = base(0) ^ 32.
+__device__ __forceinline__ int frag_k_base(int row0, int fr, int fg) {
+  const int row = row0 + fr;
+  return row * 64 + ((fg ^ swz_k(row)) * 8);
+}
+// MN-contiguous: fragment j (columns col0 + 16 j), reduction half c: the
+// 16-column group j % 4 of block col0/64 + j/4 sits at chunk pair
+// 2 (j % 4) ^ swz_m(k); k = 32 c + 8 g + s/4 (+ 4 for the second read).  The
+// per-lane base holds the swizzled pair for j % 4 == 0; other groups XOR it.
+__device__ __forceinline__ int frag_m_base(int col0, int fr, int fg) {
+  const int k = 8 * fg + (fr >> 2);
+  const int chunk = ((fr & 3) >> 1) ^ swz_m(k);
+  return (col0 >> 6) * 4096 + k * 64 + chunk * 8 + 4 * (fr & 1);
+}
+__device__ __forceinline__ bf16x8 frag_k(const bf16* tile, int base, int c, int j) {
+  return __builtin_bit_cast(bf16x8, ld16(tile + (base ^ (32 * c)) + 1024 * j));
+}
+__device__ __forceinline__ bf16x8 frag_m(const bf16* tile, int base, int c, int j) {
+  // column group j % 4 -> chunk-pair XOR 2 (j % 4) (16 elements per pair)
+  const bf16* p = tile + (base ^ (16 * (j & 3))) + 4096 * (j >> 2) + 2048 * c;
+  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p));
+  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 256));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// tanh-form GeLU via the logistic function: 0.5 (1 + tanh u) = sigma(2u), so
+//   gelu(z)  = z sigma(2u),  u = sqrt(2/pi) (z + 0.044715 z^3)
+//   gelu'(z) = sigma(2u) + 2 z sigma(2u) (1 - sigma(2u)) sqrt(2/pi) (1 + 3 * 0.044715 z^2)
+// with sigma(v) = 1 / (1 + 2^(-v log2 e)) from the hardware exp2 and reciprocal
+// (about 1 ulp each; exp2 saturates to 0 / inf, which gives sigma = 1 / 0).
+__device__ __forceinline__ float sigmoid2u(float z) {
+  const float c2 = 2.0f * 0.7978845608028654f * kLog2e, a = 0.044715f;
+  const float e = __builtin_amdgcn_exp2f(-c2 * (z + a * z * z * z));
+  return __builtin_amdgcn_rcpf(1.0f + e);
+}
+__device__ __forceinline__ float gelu2(float z) { return z * sigmoid2u(z); }
+__device__ __forceinline__ float gelu2_grad(float z) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  const float s = sigmoid2u(z);
+  return s + 2.0f * c * z * s * (1.0f - s) * (1.0f + 3.0f * a * z * z);
+}
+
+__device__ __forceinline__ void tile_coords2(int wg, int nwg, int tiles_m, int tiles_n, int& tm, int& tn) {
+  constexpr int kXcd = 8, kGroupM = 8;
+  const int q = nwg / kXcd, r = nwg % kXcd;
+  const int x = wg % kXcd, j = wg / kXcd;
+  const int id = (x < r) ? x * (q + 1) + j : r * (q + 1) + (x - r) * q + j;
+  const int per_group = kGroupM * tiles_n;
+  const int group = id / per_group;
+  const int first_m = group * kGroupM;
+  const int gsize = min(tiles_m - first_m, kGroupM);
+  const int in_group = id % per_group;
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
+
+template <bool AK, bool BKc, int EPI>
+__global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
+  __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kTileElems];  // [stage][A/B]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 1, wn = wave >> 1;  // wave tile: rows wm*128.., columns wn*64..
+  const int fr = lane & 15, fg = lane >> 4;
+  const int tiles_m = (p.M + kBM - 1) / kBM, tiles_n = p.N / kBN;
+  int tm, tn;
+  tile_coords2(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+
+  // Resources: K-contiguous -> base at the tile's first row, bound = its
+  // valid rows; MN-contiguous -> base at the tile's first column, bound = the
+  // rest of the buffer (reduction indices >= K read as zero).
+  __amdgpu_buffer_rsrc_t ra, rb;
+  if constexpr (AK) {
+    const int rows = min(kBM, p.M - m0);
+    ra = make_rsrc(p.A + (long)m0 * p.lda, (uint32_t)((long)rows * p.lda * 2));
+  } else {
+    ra = make_rsrc(p.A + m0, (uint32_t)(((long)p.K * p.lda - m0) * 2));
+  }
+  if constexpr (BKc) {
+    const int rows = min(kBN, p.N - n0);
+    rb = make_rsrc(p.B + (long)n0 * p.ldb, (uint32_t)((long)rows * p.ldb * 2));
+  } else {
+    rb = make_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
+  }
+  auto issue = [&](int kt) {
+    bf16* sa = smem[kt & (kStages - 1)][0];
+    bf16* sb = smem[kt & (kStages - 1)][1];
+    if constexpr (AK) load_k_tile(ra, p.lda, kt * kBK, sa, wave, lane);
+    else load_m_tile(ra, p.lda, kt * kBK, sa, wave, lane);
+    if constexpr (BKc) load_k_tile(rb, p.ldb, kt * kBK, sb, wave, lane);
+    else load_m_tile(rb, p.ldb, kt * kBK, sb, wave, lane);
+  };
+  const int abase = AK ? frag_k_base(wm * 128, fr, fg) : frag_m_base(wm * 128, fr, fg);
+  const int bbase = BKc ? frag_k_base(wn * 64, fr, fg) : frag_m_base(wn * 64, fr, fg);
+
+  f32x4 acc[kWTN][kWTM];
+#pragma unroll
+  for (int i = 0; i < kWTN; ++i)
+#pragma unroll
+    for (int j = 0; j < kWTM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (p.K + kBK - 1) / kBK;
+  // fragments of reduction half c of the stage in slot `slot`
+  auto load_frags = [&](int slot, int c, bf16x8 (&af)[kWTM], bf16x8 (&bf)[kWTN]) {
+    const bf16* as = smem[slot][0];
+    const bf16* bs = smem[slot][1];
+#pragma unroll
+    for (int i = 0; i < kWTN; ++i) bf[i] = BKc ? frag_k(bs, bbase, c, i) : frag_m(bs, bbase, c, i);
+#pragma unroll
+    for (int j = 0; j < kWTM; ++j) af[j] = AK ? frag_k(as, abase, c, j) : frag_m(as, abase, c, j);
+  };
+  auto mma_all = [&](const bf16x8 (&af)[kWTM], const bf16x8 (&bf)[kWTN]) {
+#pragma unroll
+    for (int j = 0; j < kWTM; ++j)
+#pragma unroll
+      for (int i = 0; i < kWTN; ++i) acc[i][j] = mma16(bf[i], af[j], acc[i][j]);
+  };
+  // bare barrier: a fence would also wait for the younger stage in flight
+  auto barrier = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // Stage kt lives in slot kt % 2.  Prologue: stages 0 and 1 in flight; once
+  // stage 0 is visible, read its first half.
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // 8 DMA instructions per stage per wave
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  barrier();
+  bf16x8 fa0[kWTM], fb0[kWTN], fa1[kWTM], fb1[kWTN];
+  load_frags(0, 0, fa0, fb0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int slot = kt & 1;
+    load_frags(slot, 1, fa1, fb1);
+    mma_all(fa0, fb0);
+    if (kt + 1 < nk) {
+      // stage kt+1 landed (own loads) and every wave has finished reading
+      // slot kt: refill it with stage kt+2, read stage kt+1's first half
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();
+      if (kt + 2 < nk) issue(kt + 2);
+      load_frags(slot ^ 1, 0, fa0, fb0);
+    }
+    mma_all(fa1, fb1);
+  }
+
+  // Epilogue: lane holds C[m][n .. n+3].
+#pragma unroll
+  for (int j = 0; j < kWTM; ++j) {
+    const int m = m0 + wm * 128 + 16 * j + fr;
+    if (m >= p.M) continue;
+#pragma unroll
+    for (int i = 0; i < kWTN; ++i) {
+      const int n = n0 + wn * 64 + 16 * i + 4 * fg;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      if constexpr (EPI == EPI_ACC_F32) {
+        float* C = static_cast<float*>(p.C) + (long)m * p.ldc + n;
+        Vec4<float> c;
+        c.load(C);
+        float o[4] = {c.get(0) + v[0], c.get(1) + v[1], c.get(2) + v[2], c.get(3) + v[3]};
+        c.set(o);
+        c.store(C);
+      } else {
+        if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
+          Vec4<bf16> b;
+          b.load(p.bias + n);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] += b.get(r);
+        }
+        if constexpr (EPI == EPI_BIAS_RES) {
+          Vec4<bf16> rr;
+          rr.load(p.R + (long)m * p.ldr + n);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] += rr.get(r);
+        }
+        if constexpr (EPI == EPI_GELU_BWD) {
+          Vec4<bf16> z;
+          z.load(p.Z + (long)m * p.ldz + n);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] *= gelu2_grad(z.get(r));
+        }
+        Vec4<bf16> o;
+        o.set(v);
+        o.store(static_cast<bf16*>(p.C) + (long)m * p.ldc + n);
+        if constexpr (EPI == EPI_BIAS_GELU) {
+          float g[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) g[r] = gelu2(v[r]);
+          Vec4<bf16> og;
+          og.set(g);
+          og.store(p.C2 + (long)m * p.ldc2 + n);
+        }
+      }
+    }
+  }
+}
+
+template <bool AK, bool BKc, int EPI>
+hipError_t launch2(const GemmDesc& d, hipStream_t st) {
+  G2Args a;
+  a.A = (const bf16*)d.A; a.B = (const bf16*)d.B; a.C = d.C;
+  a.M = d.M; a.N = d.N; a.K = d.K; a.lda = d.lda; a.ldb = d.ldb; a.ldc = d.ldc;
+  a.bias = (const bf16*)d.bias; a.R = (const bf16*)d.R; a.ldr = d.ldr;
+  a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
+  const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(tiles), dim3(kThr), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Shapes the DMA kernel takes: N a multiple of 256, K-contiguous operands
+// with K a multiple of 32, and every buffer offset below 2^31 bytes.
+bool gemm_bf16_dma_ok(GemmLayout layout, const GemmDesc& d) {
+  if (d.N % kBN != 0 || d.M <= 0) return false;
+  const bool ak = layout != GEMM_TN, bk = layout == GEMM_NT;
+  if ((ak || bk) && d.K % kBK != 0) return false;
+  const long lim = 1L << 31;
+  if (!ak && (long)d.K * d.lda * 2 >= lim) return false;
+  if (!bk && (long)d.K * d.ldb * 2 >= lim) return false;
+  if (ak && (long)kBM * d.lda * 2 >= lim) return false;
+  if (bk && (long)kBN * d.ldb * 2 >= lim) return false;
+  return true;
+}
+
+hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st) {
+  switch (layout) {
+    case GEMM_NT:
+      switch (epi) {
+        case EPI_STORE: return launch2<true, true, EPI_STORE>(d, st);
+        case EPI_BIAS: return launch2<true, true, EPI_BIAS>(d, st);
+        case EPI_BIAS_RES: return launch2<true, true, EPI_BIAS_RES>(d, st);
+        case EPI_BIAS_GELU: return launch2<true, true, EPI_BIAS_GELU>(d, st);
+      }
+      break;
+    case GEMM_NN:
+      switch (epi) {
+        case EPI_STORE: return launch2<true, false, EPI_STORE>(d, st);
+        case EPI_GELU_BWD: return launch2<true, false, EPI_GELU_BWD>(d, st);
+      }
+      break;
+    case GEMM_TN:
+      if (epi == EPI_ACC_F32) return launch2<false, false, EPI_ACC_F32>(d, st);
+      break;
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace flglm

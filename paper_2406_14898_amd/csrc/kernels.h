@@ -33,6 +33,9 @@ enum GemmEpi : int {
   EPI_ACC_F32 = 5,    // Cf += acc (fp32 output)
 };
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
+// bf16 LDS-DMA kernel (gemm_bf16.hip), used by gemm() for the shapes it takes.
+bool gemm_bf16_dma_ok(GemmLayout layout, const GemmDesc& d);
+hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
 
 // Batch bookkeeping: position of every packed row inside its own sequence.
 hipError_t seq_positions(const int32_t* cu_seqlens, int num_seqs, int32_t* pos, hipStream_t st);
