@@ -527,11 +527,23 @@ static hipError_t fwd_t(const AttnDesc& a, hipStream_t st) {
 }
 
 template <typename T, int D>
-static hipError_t bwd_t(const AttnDesc& a, hipStream_t st) {
+static hipError_t delta_t(const AttnDesc& a, hipStream_t st) {
   hipLaunchKernelGGL((attn_delta_kernel<T, D>), dim3((a.total_tokens + 3) / 4), dim3(256), 0, st,
                      (const T*)a.dout, a.ld_dout, (const T*)a.o, a.ld_o, a.delta, a.total_tokens, a.hidden,
                      a.num_heads);
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t attn_delta(DType dt, const AttnDesc& a, hipStream_t st) {
+  if (a.total_tokens <= 0) return hipSuccess;
+  if (a.head_dim == 128) return dt == DT_BF16 ? delta_t<bf16, 128>(a, st) : delta_t<float, 128>(a, st);
+  if (a.head_dim == 64) return dt == DT_BF16 ? delta_t<bf16, 64>(a, st) : delta_t<float, 64>(a, st);
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int D>
+static hipError_t bwd_t(const AttnDesc& a, hipStream_t st) {
+  hipError_t e = delta_t<T, D>(a, st);
   if (e != hipSuccess) return e;
   dim3 grid((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, D>), grid, dim3(kThreads), 0, st, a);
@@ -543,6 +555,7 @@ static hipError_t bwd_t(const AttnDesc& a, hipStream_t st) {
 
 hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;
+  if (dt == DT_BF16 && attn_bf16_ok(a)) return attn_fwd_bf16(a, st);
   if (a.head_dim == 128) return dt == DT_BF16 ? fwd_t<bf16, 128>(a, st) : fwd_t<float, 128>(a, st);
   if (a.head_dim == 64) return dt == DT_BF16 ? fwd_t<bf16, 64>(a, st) : fwd_t<float, 64>(a, st);
   return hipErrorInvalidValue;
@@ -550,6 +563,7 @@ hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st) {
 
 hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;
+  if (dt == DT_BF16 && attn_bf16_ok(a)) return attn_bwd_bf16(a, st);
   if (a.head_dim == 128) return dt == DT_BF16 ? bwd_t<bf16, 128>(a, st) : bwd_t<float, 128>(a, st);
   if (a.head_dim == 64) return dt == DT_BF16 ? bwd_t<bf16, 64>(a, st) : bwd_t<float, 64>(a, st);
   return hipErrorInvalidValue;

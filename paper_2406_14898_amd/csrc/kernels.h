@@ -90,6 +90,12 @@ struct AttnDesc {
 };
 hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st);
 hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st);
+// delta[t][h] = rowsum(dO * O), the backward pre-pass.
+hipError_t attn_delta(DType dt, const AttnDesc& a, hipStream_t st);
+// bf16 LDS-DMA kernels (attention_bf16.hip), used by attn_fwd / attn_bwd.
+bool attn_bf16_ok(const AttnDesc& a);
+hipError_t attn_fwd_bf16(const AttnDesc& a, hipStream_t st);
+hipError_t attn_bwd_bf16(const AttnDesc& a, hipStream_t st);
 
 // Client packing: client tensor [Lmax, nseq, H] (sequence-first) <-> packed
 // rows of sequences s0 .. s0+nseq-1.  Unpacking zero-fills padded positions.
