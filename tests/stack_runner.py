@@ -19,7 +19,12 @@ class GpuStack:
         self.shape, self.dt = shape, dt
         self.ss = ServerStack(shape.num_layers, shape.hidden, shape.num_heads, shape.ffn_hidden, shape.rotary_dim,
                               dt, shape.rope_base, shape.ln_eps)
-        self.params = [{k: dev(v, dt) for k, v in lp.items()} for lp in layers]
+        cache = {}  # layers given as the same dict share one device copy
+        self.params = []
+        for lp in layers:
+            if id(lp) not in cache:
+                cache[id(lp)] = {k: dev(v, dt) for k, v in lp.items()}
+            self.params.append(cache[id(lp)])
 
     def zero_grads(self):
         return [{k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()}

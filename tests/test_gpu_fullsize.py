@@ -1,0 +1,155 @@
+"""Parity at the full ChatGLM-6B block shape (hidden 4096, 32 heads of 128,
+FFN 16384), with the batch sizes and launch configuration the benchmark
+times.  The GPU runs the whole client batch; the oracle recomputes sampled
+sequences on their own, which equals their rows of the batched run because
+client batching mixes nothing across sequences (invariant I1, pinned in the
+oracle tests).  Weight gradients are checked in full on a small batch at the
+same shape.  26-block stacks alternate two generated layers to keep the
+parameter generation bounded; the kernels and launches are unchanged."""
+
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_helpers import rel_l2
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+from tests.stack_runner import GpuStack  # noqa: E402
+
+W2 = synth.WORKLOADS["chatglm6b_1blk_fwd_4x4x512"]
+W3 = synth.WORKLOADS["chatglm6b_1blk_ragged_8x4"]
+W4 = synth.WORKLOADS["chatglm6b_26blk_prefix_16x2x512"]
+W5 = synth.WORKLOADS["chatglm6b_26blk_ragged_32x1_recompute"]
+ONE = W2.shape
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def layers2():
+    t = time.time()
+    out = [synth.layer_params(ONE, l, seed=0) for l in range(2)]
+    print(f"[fullsize] generated 2 layers in {time.time() - t:.1f}s", flush=True)
+    return out
+
+
+def _seq_batch(b, s):
+    """The batch holding only sequence s, and its rows in the packed buffer."""
+    r0, r1 = int(b.cu_seqlens[s]), int(b.cu_seqlens[s + 1])
+    pre = None if b.prefix_len is None else np.array([int(b.prefix_len[s])], np.int32)
+    return synth.Batch(np.array([0, r1 - r0], np.int32), np.array([0, 1], np.int32), b.mask, pre), r0, r1
+
+
+def _shape(n):
+    return synth.StackShape(n, ONE.hidden, ONE.num_heads, ONE.ffn_hidden, ONE.rotary_dim)
+
+
+def test_cfg2_forward_sampled_sequences(layers2):
+    """1 block, forward, 4 clients x 4 x 512 tokens, causal."""
+    b = W2.batch()
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    g = GpuStack(ONE, [layers2[0]], "bf16")
+    y = g.to_host(g.run(b, x, None))["y"]
+    g.close()
+    for s in (0, b.num_seqs - 1):
+        sb, r0, r1 = _seq_batch(b, s)
+        yo, _ = oracle.stack_forward([layers2[0]], 1, x[r0:r1], sb, ONE, keep="none")
+        err = rel_l2(y[r0:r1], yo)
+        print(f"[fullsize] cfg2 seq {s}: rel-L2 {err:.2e}", flush=True)
+        assert err < TOL
+
+
+def test_cfg3_fwd_bwd_sampled_sequences(layers2):
+    """1 block, fwd+bwd, 8 clients x 4 ragged sequences U[128,1024]."""
+    b = W3.batch()
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W3.dy_std)
+    g = GpuStack(ONE, [layers2[0]], "bf16")
+    res = g.to_host(g.run(b, x, dy))
+    g.close()
+    lens = b.seqlens
+    for s in (int(np.argmin(lens)), int(np.argmax(lens))):
+        sb, r0, r1 = _seq_batch(b, s)
+        yo, xs = oracle.stack_forward([layers2[0]], 1, x[r0:r1], sb, ONE)
+        dxo, _ = oracle.stack_backward([layers2[0]], 1, xs, dy[r0:r1], sb, ONE)
+        ey, edx = rel_l2(res["y"][r0:r1], yo), rel_l2(res["dx"][r0:r1], dxo)
+        print(f"[fullsize] cfg3 seq {s} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e}", flush=True)
+        assert ey < TOL and edx < TOL
+
+
+def test_weight_grads_full_shape(layers2):
+    """Every weight gradient against the oracle at the full block shape, on a
+    small ragged two-client batch (reduction over 177 tokens, ragged tail)."""
+    b = synth.Batch(np.array([0, 100, 177], np.int32), np.array([0, 1, 2], np.int32))
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=2)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=2, std=1e-2)
+    g = GpuStack(ONE, [layers2[1]], "bf16")
+    res = g.to_host(g.run(b, x, dy))
+    g.close()
+    yo, xs = oracle.stack_forward([layers2[1]], 1, x, b, ONE)
+    dxo, go = oracle.stack_backward([layers2[1]], 1, xs, dy, b, ONE)
+    assert rel_l2(res["y"], yo) < TOL
+    assert rel_l2(res["dx"], dxo) < TOL
+    for k, v in go[0].items():
+        e = rel_l2(res["grads"][0][k], v)
+        print(f"[fullsize] grad {k}: rel-L2 {e:.2e}", flush=True)
+        assert e < TOL, k
+
+
+def _stack_sample(w, layers2, sample_seq, recompute):
+    b = w.batch()
+    n = w.shape.num_layers
+    layers = [layers2[l % 2] for l in range(n)]
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=w.dy_std)
+    g = GpuStack(w.shape, layers, "bf16")
+    t = time.time()
+    res = g.run(b, x, dy, recompute=recompute)
+    host = {"y": res["y"].float().cpu().numpy(), "dx": res["dx"].float().cpu().numpy()}
+    del res
+    g.close()
+    print(f"[fullsize] {w.name}: GPU run {time.time() - t:.1f}s", flush=True)
+    sb, r0, r1 = _seq_batch(b, sample_seq)
+    t = time.time()
+    # float32 oracle: 26 blocks on one sequence in well under a minute
+    yo, xs = oracle.stack_forward(layers, n, x[r0:r1], sb, w.shape, dtype=np.float32)
+    dxo, _ = oracle.stack_backward(layers, n, xs, dy[r0:r1], sb, w.shape, dtype=np.float32)
+    ey, edx = rel_l2(host["y"][r0:r1], yo), rel_l2(host["dx"][r0:r1], dxo)
+    print(f"[fullsize] {w.name} seq {sample_seq} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e} "
+          f"(oracle {time.time() - t:.1f}s)", flush=True)
+    assert ey < TOL and edx < TOL
+
+
+def test_cfg4_26_blocks_prefix_sampled(layers2):
+    """26 blocks, fwd+bwd, 16 clients x 2 x 512 tokens, prefix-LM (25%)."""
+    _stack_sample(W4, layers2, 0, recompute=False)
+
+
+def test_cfg5_26_blocks_ragged_recompute_sampled(layers2):
+    """26 blocks, fwd+bwd with per-block recompute, 32 clients x 1 sequence
+    U[512,2048]; the shortest sequence is recomputed by the oracle."""
+    _stack_sample(W5, layers2, int(np.argmin(W5.batch().seqlens)), recompute=True)
+
+
+def test_cfg4_recompute_is_bitwise_identical(layers2):
+    """Per-block recomputation changes no bit of y, dx or any weight gradient
+    at the full 26-block shape."""
+    b = W4.batch()
+    n = W4.shape.num_layers
+    layers = [layers2[l % 2] for l in range(n)]
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W4.dy_std)
+    g = GpuStack(W4.shape, layers, "bf16")
+    a = g.run(b, x, dy, recompute=False)
+    ya, dxa = a["y"].clone(), a["dx"].clone()
+    ga = [{k: v.clone() for k, v in gg.items()} for gg in a["grads"]]
+    del a
+    r = g.run(b, x, dy, recompute=True)
+    assert torch.equal(r["y"], ya) and torch.equal(r["dx"], dxa)
+    for l in (0, n // 2, n - 1):
+        for k in ga[l]:
+            assert torch.equal(r["grads"][l][k], ga[l][k]), (l, k)
+    g.close()
