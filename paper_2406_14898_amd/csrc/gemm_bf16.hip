@@ -319,7 +319,7 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
 }  // namespace
 
 // Shapes the DMA kernel takes: N a multiple of 256, K-contiguous operands
-// with K a multiple of 32, and every buffer offset below 2^31 bytes.
+// with K a multiple of 64, and every buffer offset below 2^31 bytes.
 bool gemm_bf16_dma_ok(GemmLayout layout, const GemmDesc& d) {
   if (d.N % kBN != 0 || d.M <= 0) return false;
   const bool ak = layout != GEMM_TN, bk = layout == GEMM_NT;
