@@ -38,6 +38,170 @@ METRIC = "server-stack fwd+bwd tokens/sec and MFMA util %, ChatGLM-6B shape"
 MFMA_CLASSES = ("gemm_nt_bias", "gemm_nt_bias_res", "gemm_nt_bias_gelu", "gemm_tn_acc", "gemm_nn_gelu_bwd",
                 "gemm_nn", "attn_fwd", "attn_bwd")
 GEMM_CLASSES = MFMA_CLASSES[:6]
+# Fragments of the kernel names rocprofv3 prints for each launch class of the
+# bf16 path (a class may launch several kernels), and the sources they are
+# built from (a stored counter reading is stale once these change).
+CLASS_KERNELS = {
+    "gemm_nt_bias": ("gemm_bf16_kernel<true, true, 1>",),
+    "gemm_nt_bias_res": ("gemm_bf16_kernel<true, true, 2>",),
+    "gemm_nt_bias_gelu": ("gemm_bf16_kernel<true, true, 3>",),
+    "gemm_nn_gelu_bwd": ("gemm_bf16_kernel<true, false, 4>",),
+    "gemm_nn": ("gemm_bf16_kernel<true, false, 0>",),
+    "gemm_tn_acc": ("gemm_bf16_kernel<false, false",),
+    "attn_fwd": ("::fwd_kernel<",),
+    "attn_bwd": ("attn_delta_kernel", "::dkdv_kernel<", "::dq_kernel<"),
+    "layernorm_fwd": ("ln_fwd_kernel",),
+    "layernorm_bwd": ("ln_bwd_dx_kernel",),
+    "rope_qk": ("rope_qk_kernel",),
+    "colsum": ("colsum_partial_kernel", "colsum_finish_kernel"),
+}
+CSRC = os.path.join(ROOT, "paper_2406_14898_amd", "csrc")
+CLASS_SOURCES = {"gemm": ("gemm_bf16.hip", "common.h", "kernels.h"),
+                 "attn": ("attention_bf16.hip", "attention.hip", "common.h", "kernels.h"),
+                 "": ("elementwise.hip", "common.h", "kernels.h")}
+COPY_KERNEL = "neg_kernel"   # calibration: y = -x over float32, reads and writes the same bytes
+
+
+def class_source_hash(cls: str) -> str:
+    import hashlib
+    files = next(v for k, v in CLASS_SOURCES.items() if cls.startswith(k))
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"server_stack_kernels_{workload}_hbm_traffic.txt")
+
+
+def committed_traffic(cls: str, workload: str):
+    """HBM bytes per launch of a class from the committed counter summary, or
+    None if there is none or the kernel sources changed since it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 4 and f[0] == "class" and f[1] == cls:
+            kv = dict(zip(f[2::2], f[3::2]))
+            if kv.get("src") != class_source_hash(cls):
+                return None
+            return int(float(kv["hbm_bytes_per_launch"]))
+    return None
+
+
+def _short_kernel(name: str) -> str:
+    name = name[5:] if name.startswith("void ") else name
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0 and i > 0 and name[i - 1] != ":":
+            return name[:i]
+    return name
+
+
+def _pmc_per_kernel(d: str, counter: str) -> dict:
+    """{kernel name: [dispatches, counter sum]} from a rocprofv3 --pmc CSV run."""
+    import csv
+    import glob
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            e = out.setdefault(r["Kernel_Name"], [0, 0.0])
+            e[0] += 1
+            e[1] += float(r["Counter_Value"])
+    return out
+
+
+def _class_totals(per_kernel: dict, cls: str):
+    pats = CLASS_KERNELS[cls]
+    launches, total = 0, 0.0
+    for name, (n, v) in per_kernel.items():
+        hit = [p for p in pats if p in name]
+        if hit:
+            total += v
+            if hit[0] == pats[0]:
+                launches += n
+    return launches, total
+
+
+def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
+    """Text summary of four rocprofv3 --pmc runs under root: fetch/ and write/
+    (FETCH_SIZE, WRITE_SIZE of the benchmark), copy_fetch/ and copy_write/ (the
+    same counters for --copy-calibration).  Counter KiB are scaled by the
+    ratio of the copy's known bytes to what the counter reads for it."""
+    copy_bytes = copy_mib << 20
+    lines = []
+    scale = {}
+    for c, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        pk = _pmc_per_kernel(os.path.join(root, "copy_" + sub), c)
+        hits = [(n, v) for k, (n, v) in pk.items() if COPY_KERNEL in k]
+        n, v = sum(h[0] for h in hits), sum(h[1] for h in hits)
+        per = v / max(n, 1) * 1024.0
+        scale[c] = copy_bytes / per
+        lines.append(f"calibration {c} copy_bytes {copy_bytes} dispatches {n} counter_bytes_per_dispatch "
+                     f"{per:.0f} factor {scale[c]:.4f}")
+    fetch = _pmc_per_kernel(os.path.join(root, "fetch"), "FETCH_SIZE")
+    write = _pmc_per_kernel(os.path.join(root, "write"), "WRITE_SIZE")
+    for cls in CLASS_KERNELS:
+        n, fv = _class_totals(fetch, cls)
+        n2, wv = _class_totals(write, cls)
+        if n == 0:
+            continue
+        fb = fv / n * 1024.0 * scale["FETCH_SIZE"]
+        wb = wv / max(n2, 1) * 1024.0 * scale["WRITE_SIZE"]
+        lines.append(f"class {cls} launches {n} fetch_bytes_per_launch {fb:.0f} write_bytes_per_launch {wb:.0f} "
+                     f"hbm_bytes_per_launch {fb + wb:.0f} src {class_source_hash(cls)}")
+    return "\n".join(lines)
+
+
+def summarize_trace(root: str) -> str:
+    """Per-kernel table from a rocprofv3 --kernel-trace --stats CSV run."""
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    out = [f"{'kernel':<72} {'calls':>6} {'avg_us':>10} {'total_ms':>10} {'pct':>6}"]
+    for r in rows:
+        out.append(f"{_short_kernel(r['Name'])[:72]:<72} {int(r['Calls']):>6} {float(r['AverageNs']) / 1e3:>10.1f} "
+                   f"{float(r['TotalDurationNs']) / 1e6:>10.2f} {float(r['Percentage']):>6.2f}")
+    by_cls = {}
+    for r in rows:
+        for cls, pats in CLASS_KERNELS.items():
+            hit = [p for p in pats if p in r["Name"]]
+            if hit:
+                e = by_cls.setdefault(cls, [0, 0.0])
+                e[1] += float(r["TotalDurationNs"])
+                if hit[0] == pats[0]:
+                    e[0] += int(r["Calls"])
+                break
+    out.append("")
+    out.append(f"{'class':<20} {'launches':>8} {'avg_us_per_launch':>18}")
+    for cls, (n, t) in sorted(by_cls.items(), key=lambda kv: -kv[1][1]):
+        out.append(f"{cls:<20} {n:>8} {t / max(n, 1) / 1e3:>18.1f}")
+    return "\n".join(out)
+
+
+def copy_calibration(mib: int) -> None:
+    """A plain streaming kernel of known size for scaling the HBM counters:
+    y = -x over mib MiB of float32 (reads and writes mib MiB each), 3 times."""
+    import torch
+    n = (mib << 20) // 4
+    x = torch.ones(n, device="cuda", dtype=torch.float32)
+    y = torch.empty_like(x)
+    for _ in range(3):
+        torch.neg(x, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": mib << 20, "dispatches": 3}))
 
 
 def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
@@ -139,7 +303,23 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of CPU oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
+    ap.add_argument("--copy-calibration", type=int, metavar="MIB",
+                    help="only run the counter-calibration copy kernel over MIB MiB")
+    ap.add_argument("--summarize-traffic", metavar="DIR",
+                    help="print the HBM traffic summary of rocprofv3 --pmc runs under DIR (no GPU)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print the per-kernel table of a rocprofv3 --kernel-trace --stats run (no GPU)")
+    ap.add_argument("--copy-mib", type=int, default=1024, help="size the calibration run used")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        print(summarize_traffic(args.summarize_traffic, args.copy_mib, args.workload))
+        return 0
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return 0
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this build runs the server stack on one GPU only; "
@@ -212,11 +392,13 @@ def main() -> int:
         if dom in MFMA_CLASSES:
             ach = r["flops"] / r["launches"] / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak, "unit": "TFLOP/s",
-                        "frac": round(ach / peak, 4), "traffic": None}
+                        "frac": round(ach / peak, 4),
+                        "traffic": committed_traffic(dom, w.name)}
         else:
             ach = r["bytes"] / r["launches"] / avg_s / 1e9
             roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                        "traffic": committed_traffic(dom, w.name)}
 
     out = {
         "metric": METRIC,

@@ -379,7 +379,8 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   g.lda = H; g.ldb = H; g.ldc = 3 * H; g.bias = p.b_qkv;
   LAUNCH(FL_PROF_GEMM_NT_BIAS, gemm_flops(T, 3 * H, H), gemm_bytes(T, 3 * H, H, E, E),
          gemm(dt, GEMM_NT, EPI_BIAS, g, s));
-  LAUNCH(FL_PROF_ROPE, 0, 4 * TH * E,
+  // q and k: the first rotary_dim features of every head, read and written
+  LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
          rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
