@@ -236,69 +236,114 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   barrier();
   bf16x8 fa0[kWTM], fb0[kWTN], fa1[kWTM], fb1[kWTN];
   load_frags(0, 0, fa0, fb0);
-  for (int kt = 0; kt < nk; ++kt) {
+  // The last stage is peeled so that every path through the loop body passes
+  // the barrier: the compiler then knows the second-half fragments are
+  // complete there and lets the next stage's first-half reads overlap the
+  // second half's matrix-core work instead of waiting for them.
+  for (int kt = 0; kt < nk - 1; ++kt) {
     const int slot = kt & 1;
     load_frags(slot, 1, fa1, fb1);
     mma_all(fa0, fb0);
-    if (kt + 1 < nk) {
-      // stage kt+1 landed (own loads) and every wave has finished reading
-      // slot kt: refill it with stage kt+2, read stage kt+1's first half
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();
-      if (kt + 2 < nk) issue(kt + 2);
-      load_frags(slot ^ 1, 0, fa0, fb0);
-    }
+    // stage kt+1 landed (own loads) and every wave has finished reading
+    // slot kt: refill it with stage kt+2, read stage kt+1's first half
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();
+    if (kt + 2 < nk) issue(kt + 2);
+    load_frags(slot ^ 1, 0, fa0, fb0);
     mma_all(fa1, fb1);
   }
+  load_frags((nk - 1) & 1, 1, fa1, fb1);
+  mma_all(fa0, fb0);
+  mma_all(fa1, fb1);
 
-  // Epilogue: lane holds C[m][n .. n+3].
+  // Epilogue, staged through LDS so that every global access is a full row
+  // segment: the accumulators of one 128-row half of the tile go to LDS as
+  // fp32 ([128][256], 16-byte chunk c of row r at c ^ (r & 15)); then each
+  // wave owns whole rows, a lane four consecutive columns, and bias,
+  // residual, GeLU input and output rows are read and written contiguously
+  // (a lane of the matrix core holds 4 columns of 16 different rows, which
+  // as direct stores cost more than the reduction for K = 4096).
+  float* stg = reinterpret_cast<float*>(&smem[0][0][0]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  barrier();  // every wave is done with the operand tiles
+  const int n = n0 + 4 * lane;
+  float bias[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
+    Vec4<bf16> b;
+    b.load(p.bias + n);
 #pragma unroll
-  for (int j = 0; j < kWTM; ++j) {
-    const int m = m0 + wm * 128 + 16 * j + fr;
-    if (m >= p.M) continue;
+    for (int e = 0; e < 4; ++e) bias[e] = b.get(e);
+  }
 #pragma unroll
-    for (int i = 0; i < kWTN; ++i) {
-      const int n = n0 + wn * 64 + 16 * i + 4 * fg;
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      if constexpr (EPI == EPI_ACC_F32) {
-        float* C = static_cast<float*>(p.C) + (long)m * p.ldc + n;
-        Vec4<float> c;
-        c.load(C);
-        float o[4] = {c.get(0) + v[0], c.get(1) + v[1], c.get(2) + v[2], c.get(3) + v[3]};
-        c.set(o);
-        c.store(C);
-      } else {
-        if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
-          Vec4<bf16> b;
-          b.load(p.bias + n);
+  for (int half = 0; half < 2; ++half) {
+    // Rows wave, wave + 8, ... of this half: issue every row's global loads
+    // (residual, GeLU input, fp32 accumulator) before the first use so they
+    // are in flight together.
+    constexpr int kRows = 128 / kWaves;
+    const int mbase = m0 + half * 128 + wave;
+    Vec4<bf16> ext[kRows];
+    Vec4<float> cacc[kRows];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] += b.get(r);
+    for (int q = 0; q < kRows; ++q) {
+      const long m = mbase + q * kWaves;
+      if (m < p.M) {
+        if constexpr (EPI == EPI_BIAS_RES) ext[q].load(p.R + m * p.ldr + n);
+        if constexpr (EPI == EPI_GELU_BWD) ext[q].load(p.Z + m * p.ldz + n);
+        if constexpr (EPI == EPI_ACC_F32) cacc[q].load(static_cast<float*>(p.C) + m * p.ldc + n);
+      }
+    }
+    if (wm == half) {
+#pragma unroll
+      for (int j = 0; j < kWTM; ++j) {
+        const int r = 16 * j + fr;
+#pragma unroll
+        for (int i = 0; i < kWTN; ++i) {
+          const int c = (wn * 64 + 16 * i + 4 * fg) >> 2;
+          st16(stg + r * 256 + ((c ^ (r & 15)) << 2), __builtin_bit_cast(u32x4, acc[i][j]));
         }
-        if constexpr (EPI == EPI_BIAS_RES) {
-          Vec4<bf16> rr;
-          rr.load(p.R + (long)m * p.ldr + n);
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] += rr.get(r);
+    for (int q = 0; q < kRows; ++q) {
+      const int r = wave + q * kWaves;
+      const long m = mbase + q * kWaves;
+      if (m >= p.M) break;
+      const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
+      if constexpr (EPI == EPI_ACC_F32) {
+        float o[4] = {cacc[q].get(0) + v[0], cacc[q].get(1) + v[1], cacc[q].get(2) + v[2], cacc[q].get(3) + v[3]};
+        cacc[q].set(o);
+        cacc[q].store(static_cast<float*>(p.C) + m * p.ldc + n);
+      } else {
+        if constexpr (EPI == EPI_BIAS_RES) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += ext[q].get(e);
         }
         if constexpr (EPI == EPI_GELU_BWD) {
-          Vec4<bf16> z;
-          z.load(p.Z + (long)m * p.ldz + n);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] *= gelu2_grad(z.get(r));
+          for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[q].get(e));
         }
         Vec4<bf16> o;
         o.set(v);
-        o.store(static_cast<bf16*>(p.C) + (long)m * p.ldc + n);
+        o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
         if constexpr (EPI == EPI_BIAS_GELU) {
           float g[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) g[r] = gelu2(v[r]);
+          for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
           Vec4<bf16> og;
           og.set(g);
-          og.store(p.C2 + (long)m * p.ldc2 + n);
+          og.store(p.C2 + m * p.ldc2 + n);
         }
       }
+    }
+    if (half == 0) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();  // the second half overwrites the staging buffer
     }
   }
 }

@@ -30,9 +30,12 @@ def _gelu(z):
 @pytest.mark.parametrize("dt", DT)
 @pytest.mark.parametrize("epi", [F.FL_EPI_STORE, F.FL_EPI_BIAS, F.FL_EPI_BIAS_RES, F.FL_EPI_BIAS_GELU])
 @pytest.mark.parametrize("N", [512, 384])
-def test_gemm_nt(dt, epi, N):
+@pytest.mark.parametrize("M", [300, 400])
+def test_gemm_nt(dt, epi, N, M):
+    """M = 300 / 400: the last 256-row tile ends inside its first / second
+    128-row epilogue half."""
     code, tdt = DTYPES[dt]
-    M, K = 300, 320
+    K = 320
     A, B = rnd((M, K), 1, dt=dt), rnd((N, K), 2, 0.1, dt=dt)
     bias, R = rnd((N,), 3, dt=dt), rnd((M, N), 4, dt=dt)
     ref = A.astype(np.float64) @ B.astype(np.float64).T
@@ -52,9 +55,10 @@ def test_gemm_nt(dt, epi, N):
 
 @pytest.mark.parametrize("dt", DT)
 @pytest.mark.parametrize("epi", [F.FL_EPI_STORE, F.FL_EPI_GELU_BWD])
-def test_gemm_nn(dt, epi):
+@pytest.mark.parametrize("N", [384, 512])
+def test_gemm_nn(dt, epi, N):
     code, tdt = DTYPES[dt]
-    M, N, K = 200, 384, 448
+    M, K = 420, 448
     A, B, Z = rnd((M, K), 5, dt=dt), rnd((K, N), 6, 0.1, dt=dt), rnd((M, N), 7, dt=dt)
     ref = A.astype(np.float64) @ B.astype(np.float64)
     if epi == F.FL_EPI_GELU_BWD:
