@@ -53,8 +53,12 @@ struct G2Args {
   long ldz;
 };
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+// Buffer resource: base address, no stride, num_records = bytes, raw
+// (untyped) access; reads past num_records return zero.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffff), (int)bytes, 0x00020000};
 }
 
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
@@ -69,32 +73,44 @@ __device__ __forceinline__ int swz_k(int row) { return row & 7; }
 // onto disjoint banks.
 __device__ __forceinline__ int swz_m(int k) { return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2); }
 
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, bf16* lds_inst_base, uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LDS_AS void*)lds_inst_base, 16, voff, 0, 0, 0);
+// One LDS-DMA instruction: 64 lanes x 16 bytes from rs + voff into LDS at
+// LDS byte address lds_inst_base + 16 * lane.  Written as inline assembly so that the
+// compiler does not see an LDS write whose completion it would have to wait
+// for (vmcnt) before every later LDS read: the pipeline waits for the stage
+// explicitly, one stage later, before the barrier that publishes it.
+__device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_inst_base, uint32_t voff) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_inst_base);
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(lds), "v"(voff), "s"(rs)
+      : "memory", "m0");
 }
 
 // K-contiguous tile [256 rows][64]: 2048 chunks, 4 DMA instructions per wave.
-__device__ __forceinline__ void load_k_tile(__amdgpu_buffer_rsrc_t rs, long ld, int k0, bf16* tile, int wave,
+__device__ __forceinline__ void load_k_tile(i32x4 rs, long ld, int k0, uint32_t tile, int wave,
                                             int lane) {
 #pragma unroll
   for (int i = 0; i < 32 / kWaves; ++i) {
     const int inst = i * kWaves + wave;
     const int lin = inst * 64 + lane;
     const int row = lin >> 3, q = (lin & 7) ^ swz_k(row);
-    dma16(rs, tile + inst * 512, (uint32_t)(row * ld + k0 + q * 8) * 2u);
+    dma16(rs, tile + inst * 1024, (uint32_t)(row * ld + k0 + q * 8) * 2u);
   }
 }
 
 // MN-contiguous tile: 4 column blocks of [64 k][64 columns] (8 KB each); a
 // DMA instruction fills 8 k-rows of 128 bytes; 4 per wave.
-__device__ __forceinline__ void load_m_tile(__amdgpu_buffer_rsrc_t rs, long ld, int k0, bf16* tile, int wave,
+__device__ __forceinline__ void load_m_tile(i32x4 rs, long ld, int k0, uint32_t tile, int wave,
                                             int lane) {
 #pragma unroll
   for (int i = 0; i < 32 / kWaves; ++i) {
     const int inst = i * kWaves + wave;  // 0..31: block inst/8, k-rows 8*(inst%8) ..
     const int blk = inst >> 3, krow = (inst & 7) * 8 + (lane >> 3);
     const int q = (lane & 7) ^ swz_m(krow);
-    dma16(rs, tile + inst * 512, (uint32_t)((long)(k0 + krow) * ld + blk * 64 + q * 8) * 2u);
+    dma16(rs, tile + inst * 1024, (uint32_t)((long)(k0 + krow) * ld + blk * 64 + q * 8) * 2u);
   }
 }
 
@@ -171,7 +187,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   // Resources: K-contiguous -> base at the tile's first row, bound = its
   // valid rows; MN-contiguous -> base at the tile's first column, bound = the
   // rest of the buffer (reduction indices >= K read as zero).
-  __amdgpu_buffer_rsrc_t ra, rb;
+  i32x4 ra, rb;
   if constexpr (AK) {
     const int rows = min(kBM, p.M - m0);
     ra = make_rsrc(p.A + (long)m0 * p.lda, (uint32_t)((long)rows * p.lda * 2));
@@ -184,9 +200,11 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   } else {
     rb = make_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
   }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(LDS_AS void*)&smem[0][0][0];
   auto issue = [&](int kt) {
-    bf16* sa = smem[kt & (kStages - 1)][0];
-    bf16* sb = smem[kt & (kStages - 1)][1];
+    // byte addresses of this stage's A and B tiles
+    const uint32_t sa = lds0 + (uint32_t)(kt & (kStages - 1)) * (2 * kTileElems * 2);
+    const uint32_t sb = sa + kTileElems * 2;
     if constexpr (AK) load_k_tile(ra, p.lda, kt * kBK, sa, wave, lane);
     else load_m_tile(ra, p.lda, kt * kBK, sa, wave, lane);
     if constexpr (BKc) load_k_tile(rb, p.ldb, kt * kBK, sb, wave, lane);
