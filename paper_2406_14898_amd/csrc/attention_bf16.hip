@@ -45,20 +45,16 @@ __device__ __forceinline__ SeqB seqb(const int32_t* cu, const int32_t* prefix, i
 }
 __device__ __forceinline__ bool vis(int i, int j, int L, int P) { return j < L && (j <= i || j < P); }
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
 template <int D>
 __device__ __forceinline__ int swz(int row) {
   return D == 128 ? 2 * (row & 7) : (row & 7);
 }
 
 // DMA a [64 rows][D] tile: rows row0 .. of the resource (row stride ld
-// elements); D/8 instructions per tile, spread over the 4 waves.
+// elements) into LDS at byte address tile; D/8 instructions per tile,
+// spread over the 4 waves.
 template <int D>
-__device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, long ld, int row0, bf16* tile, int wave,
-                                         int lane) {
+__device__ __forceinline__ void dma_tile(i32x4 rs, long ld, int row0, uint32_t tile, int wave, int lane) {
   constexpr int CH = D / 8;          // chunks per row
   constexpr int RPI = 64 / CH;       // rows per instruction
 #pragma unroll
@@ -67,7 +63,7 @@ __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, long ld, int
     const int row = inst * RPI + lane / CH;
     const int q = (lane % CH) ^ swz<D>(row);
     const uint32_t voff = (uint32_t)((long)(row0 + row) * ld + q * 8) * 2u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LDS_AS void*)(tile + inst * 512), 16, voff, 0, 0, 0);
+    dma_lds<16>(rs, tile + inst * 1024, voff);
   }
 }
 
@@ -143,13 +139,14 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
   const float sl2 = kLog2e / sqrtf((float)D);
 
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
-  const auto rk = rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
-  const auto rv = rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
+  const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
   const int nkt = (kv_end + kRows - 1) / kRows;
+  const uint32_t lds_k = FL_LDS_ADDR(&Ks[0][0]), lds_v = FL_LDS_ADDR(&Vs[0][0]);
   auto issue = [&](int kt) {
-    dma_tile<D>(rk, ld, kt * kRows, Ks[kt & 1], w, lane);
-    dma_tile<D>(rv, ld, kt * kRows, Vs[kt & 1], w, lane);
+    dma_tile<D>(rk, ld, kt * kRows, lds_k + (kt & 1) * (kRows * D * 2), w, lane);
+    dma_tile<D>(rv, ld, kt * kRows, lds_v + (kt & 1) * (kRows * D * 2), w, lane);
   };
   issue(0);
 
@@ -162,6 +159,10 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
       qf[qs][c] = qi < si.L ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + qi) * ld + h * D + 32 * c + 8 * fg))
                             : bf16x8{};
   }
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) settle(qf[qs][c]);
   f32x4 acc[D / 16][QS];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt)
@@ -282,13 +283,14 @@ __global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
   const float sl2 = kLog2e / sqrtf((float)D);
 
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
-  const auto rk = rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
-  const auto rv = rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
+  const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
   const int nkt = (kv_end + kRows - 1) / kRows;
+  const uint32_t lds_k = FL_LDS_ADDR(&Ks[0][0]), lds_v = FL_LDS_ADDR(&Vs[0][0]);
   auto issue = [&](int kt) {
-    dma_tile<D>(rk, ld, kt * kRows, Ks[kt & 1], w, lane);
-    dma_tile<D>(rv, ld, kt * kRows, Vs[kt & 1], w, lane);
+    dma_tile<D>(rk, ld, kt * kRows, lds_k + (kt & 1) * (kRows * D * 2), w, lane);
+    dma_tile<D>(rv, ld, kt * kRows, lds_v + (kt & 1) * (kRows * D * 2), w, lane);
   };
   issue(0);
 
@@ -304,7 +306,12 @@ __global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
                     : bf16x8{};
   }
   const float lse2 = qvalid ? a.lse[(long)(si.r0 + qi) * a.num_heads + h] * kLog2e : 0.f;
-  const float dlt = qvalid ? a.delta[(long)(si.r0 + qi) * a.num_heads + h] : 0.f;
+  float dlt = qvalid ? a.delta[(long)(si.r0 + qi) * a.num_heads + h] : 0.f;
+  float lse2s = lse2;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) { settle(qf[c]); settle(dof[c]); }
+  settle(dlt);
+  settle(lse2s);
   f32x4 acc[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -333,7 +340,7 @@ __global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int j = j0 + 16 * at + 4 * fg + i;
-        const float pr = (qvalid && vis(qi, j, si.L, si.P)) ? exp2f(st[at][i] * sl2 - lse2) : 0.f;
+        const float pr = (qvalid && vis(qi, j, si.L, si.P)) ? exp2f(st[at][i] * sl2 - lse2s) : 0.f;
         ds[at][i] = pr * (dp[at][i] - dlt);
       }
 #pragma unroll
@@ -382,20 +389,22 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
   const int H = a.hidden, nh = a.num_heads;
   const float sl2 = kLog2e / sqrtf((float)D);
 
-  const auto rq = rsrc(qkv + (long)si.r0 * ld + h * D, (uint32_t)((long)si.L * ld * 2));
-  const auto ro = rsrc(dout + (long)si.r0 * a.ld_dout + h * D, (uint32_t)((long)si.L * a.ld_dout * 2));
-  const auto rl = rsrc(a.lse + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
-  const auto rd = rsrc(a.delta + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
+  const auto rq = buf_rsrc(qkv + (long)si.r0 * ld + h * D, (uint32_t)((long)si.L * ld * 2));
+  const auto ro = buf_rsrc(dout + (long)si.r0 * a.ld_dout + h * D, (uint32_t)((long)si.L * a.ld_dout * 2));
+  const auto rl = buf_rsrc(a.lse + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
+  const auto rd = buf_rsrc(a.delta + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
   const int qstart = ((k0 < si.P) ? 0 : k0) / kRows;
   const int nqt = (si.L + kRows - 1) / kRows;
+  const uint32_t lds_q = FL_LDS_ADDR(&Qs[0][0]), lds_o = FL_LDS_ADDR(&Os[0][0]);
+  const uint32_t lds_l = FL_LDS_ADDR(&Ls[0][0]), lds_d = FL_LDS_ADDR(&Ds[0][0]);
   auto issue = [&](int qt) {
     const int slot = qt & 1;
-    dma_tile<D>(rq, ld, qt * kRows, Qs[slot], w, lane);
-    dma_tile<D>(ro, a.ld_dout, qt * kRows, Os[slot], w, lane);
+    dma_tile<D>(rq, ld, qt * kRows, lds_q + slot * (kRows * D * 2), w, lane);
+    dma_tile<D>(ro, a.ld_dout, qt * kRows, lds_o + slot * (kRows * D * 2), w, lane);
     // LSE (scaled on use) and delta rows: 64 x 4 bytes each
     const uint32_t voff = (uint32_t)((qt * kRows + lane) * nh) * 4u;
-    if (w == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (LDS_AS void*)Ls[slot], 4, voff, 0, 0, 0);
-    if (w == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (LDS_AS void*)Ds[slot], 4, voff, 0, 0, 0);
+    if (w == 0) dma_lds<4>(rl, lds_l + slot * (kRows * 4), voff);
+    if (w == 1) dma_lds<4>(rd, lds_d + slot * (kRows * 4), voff);
   };
   issue(qstart);
 
@@ -410,6 +419,8 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
                 ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + kj) * ld + 2 * H + h * D + 32 * c + 8 * fg))
                 : bf16x8{};
   }
+#pragma unroll
+  for (int c = 0; c < NC; ++c) { settle(kf[c]); settle(vf[c]); }
   f32x4 dk[D / 16], dv[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) { dk[dt] = f32x4{0.f, 0.f, 0.f, 0.f}; dv[dt] = dk[dt]; }

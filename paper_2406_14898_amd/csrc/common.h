@@ -169,6 +169,49 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// ---------------------------------------------------------------------------
+// Global -> LDS transfers with buffer loads in LDS-DMA mode.
+// ---------------------------------------------------------------------------
+// Buffer resource: base address, no stride, num_records = bytes, raw
+// (untyped) access; reads at or past num_records return zero.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 buf_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffff), (int)bytes, 0x00020000};
+}
+// LDS byte address of a __shared__ object (take it once per array and add
+// integer offsets; casting derived generic pointers costs a null check).
+#define FL_LDS_ADDR(obj) ((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)(obj))
+// One instruction: 64 lanes x BYTES (16 or 4) from rs + voff into LDS at
+// lds + BYTES * lane (the LDS side ignores per-lane addresses).  Issued as
+// inline assembly so that the compiler does not see an LDS write it would
+// have to wait for (vmcnt) before every later LDS read: callers wait for a
+// stage explicitly, when they publish it with a barrier.
+template <int BYTES>
+__device__ __forceinline__ void dma_lds(i32x4 rs, uint32_t lds, uint32_t voff) {
+  static_assert(BYTES == 16 || BYTES == 4, "dwordx4 or dword");
+  const uint32_t m = __builtin_amdgcn_readfirstlane(lds);
+  if constexpr (BYTES == 16)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(m), "v"(voff), "s"(rs)
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(m), "v"(voff), "s"(rs)
+                 : "memory", "m0");
+}
+
+// Marks a register value as used here.  Values loaded from global memory
+// before a loop whose body issues dma_lds() must be settled before the loop:
+// otherwise the compiler places its wait for them (vmcnt) inside the body,
+// where it would also wait for the in-flight DMA it does not know about.
+template <typename T>
+__device__ __forceinline__ void settle(T& v) {
+  asm volatile("" : "+v"(v));
+}
+
 // XOR swizzle of the 8-element chunk index inside an LDS row holding 8
 // chunks; spreads both row-wise (fragment reads) and strided (transposed
 // writes) access patterns over distinct banks.

@@ -53,14 +53,6 @@ struct G2Args {
   long ldz;
 };
 
-// Buffer resource: base address, no stride, num_records = bytes, raw
-// (untyped) access; reads past num_records return zero.
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
-  const uint64_t a = reinterpret_cast<uint64_t>(base);
-  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffff), (int)bytes, 0x00020000};
-}
-
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
 // slot q ^ swz_k(r).  With this swizzle the fragment reads (16 consecutive
 // rows, one chunk each) are free of LDS bank conflicts on gfx950 (measured
@@ -73,20 +65,8 @@ __device__ __forceinline__ int swz_k(int row) { return row & 7; }
 // onto disjoint banks.
 __device__ __forceinline__ int swz_m(int k) { return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2); }
 
-// One LDS-DMA instruction: 64 lanes x 16 bytes from rs + voff into LDS at
-// LDS byte address lds_inst_base + 16 * lane.  Written as inline assembly so that the
-// compiler does not see an LDS write whose completion it would have to wait
-// for (vmcnt) before every later LDS read: the pipeline waits for the stage
-// explicitly, one stage later, before the barrier that publishes it.
 __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_inst_base, uint32_t voff) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_inst_base);
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0\n\t"
-      "buffer_load_dwordx4 %1, %2, 0 offen lds"
-      :
-      : "s"(lds), "v"(voff), "s"(rs)
-      : "memory", "m0");
+  dma_lds<16>(rs, lds_inst_base, voff);
 }
 
 // K-contiguous tile [256 rows][64]: 2048 chunks, 4 DMA instructions per wave.
@@ -190,17 +170,17 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   i32x4 ra, rb;
   if constexpr (AK) {
     const int rows = min(kBM, p.M - m0);
-    ra = make_rsrc(p.A + (long)m0 * p.lda, (uint32_t)((long)rows * p.lda * 2));
+    ra = buf_rsrc(p.A + (long)m0 * p.lda, (uint32_t)((long)rows * p.lda * 2));
   } else {
-    ra = make_rsrc(p.A + m0, (uint32_t)(((long)p.K * p.lda - m0) * 2));
+    ra = buf_rsrc(p.A + m0, (uint32_t)(((long)p.K * p.lda - m0) * 2));
   }
   if constexpr (BKc) {
     const int rows = min(kBN, p.N - n0);
-    rb = make_rsrc(p.B + (long)n0 * p.ldb, (uint32_t)((long)rows * p.ldb * 2));
+    rb = buf_rsrc(p.B + (long)n0 * p.ldb, (uint32_t)((long)rows * p.ldb * 2));
   } else {
-    rb = make_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
+    rb = buf_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
   }
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(LDS_AS void*)&smem[0][0][0];
+  const uint32_t lds0 = FL_LDS_ADDR(&smem[0][0][0]);
   auto issue = [&](int kt) {
     // byte addresses of this stage's A and B tiles
     const uint32_t sa = lds0 + (uint32_t)(kt & (kStages - 1)) * (2 * kTileElems * 2);
