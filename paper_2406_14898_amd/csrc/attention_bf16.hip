@@ -23,6 +23,12 @@
 // Kernels: forward (S^T = K Q^T, online softmax, O^T += V^T P^T); dq
 // (S^T, dP^T = V dO^T, dQ^T += K^T dS^T); dk/dv (S = Q K^T, dP = dO V^T,
 // dV^T += dO^T P, dK^T += Q^T dS).  Every output element has one writer.
+// Loops are unrolled over the two LDS slots so tile addresses are
+// compile-time; per-lane fragment offsets are computed once; a wave skips
+// key tiles it cannot see and masks only tiles that straddle the diagonal
+// or the sequence end.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -43,7 +49,8 @@ __device__ __forceinline__ SeqB seqb(const int32_t* cu, const int32_t* prefix, i
   si.P = prefix ? prefix[s] : 0;
   return si;
 }
-__device__ __forceinline__ bool vis(int i, int j, int L, int P) { return j < L && (j <= i || j < P); }
+// Branch-free (bitwise) so that masking stays a select per element.
+__device__ __forceinline__ bool vis(int i, int j, int L, int P) { return (j < L) & ((j <= i) | (j < P)); }
 
 template <int D>
 __device__ __forceinline__ int swz(int row) {
@@ -67,41 +74,53 @@ __device__ __forceinline__ void dma_tile(i32x4 rs, long ld, int row0, uint32_t t
   }
 }
 
-// 16 rows (r0 + fr) x reduction slots 32c + 8g .. +7 (16-byte read).
+// Per-lane element offsets of the fragment reads inside a [64][D] tile, so
+// that every read in the loops is one base plus a compile-time offset:
+//   row[c]: rows fr (+ 16 at), reduction slots 32c + 8g .. +7 (16-byte read);
+//   tr[dt]: columns 16 dt + lane (two transpose reads over rows
+//           {kb + 4g + e, kb + 16 + 4g + e}, e < 4; + kb D, + 16 D).
+// Row offsets that are multiples of 8 leave the swizzle unchanged.
 template <int D>
-__device__ __forceinline__ bf16x8 frag_row(const bf16* tile, int r0, int c, int fr, int fg) {
-  const int row = r0 + fr;
-  return __builtin_bit_cast(bf16x8, ld16(tile + row * D + (((4 * c + fg) ^ swz<D>(row)) * 8)));
-}
-// Columns d0 + j (lane j of the group) x reduction rows
-// {kb + 4g + e, kb + 16 + 4g + e}, e < 4 (two transpose reads).
+struct FragBase {
+  int row[D / 32];
+  int tr[D / 16];
+  __device__ __forceinline__ void init(int fr, int fg) {
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) row[c] = fr * D + (((4 * c + fg) ^ swz<D>(fr)) << 3);
+    const int r1 = 4 * fg + (fr >> 2);
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const int col = 16 * dt + 4 * (fr & 3);
+      tr[dt] = r1 * D + (((col >> 3) ^ swz<D>(r1)) << 3) + (col & 7);
+    }
+  }
+};
+__device__ __forceinline__ bf16x8 rd_row(const bf16* p) { return __builtin_bit_cast(bf16x8, ld16(p)); }
 template <int D>
-__device__ __forceinline__ bf16x8 frag_tr(const bf16* tile, int kb, int d0, int fr, int fg) {
-  const int col = d0 + 4 * (fr & 3);
-  const int r1 = kb + 4 * fg + (fr >> 2), r2 = r1 + 16;
-  const bf16* p1 = tile + r1 * D + (((col >> 3) ^ swz<D>(r1)) * 8) + (col & 7);
-  const bf16* p2 = tile + r2 * D + (((col >> 3) ^ swz<D>(r2)) * 8) + (col & 7);
-  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)p1);
-  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)p2);
+__device__ __forceinline__ bf16x8 rd_tr(const bf16* p) {
+  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)p);
+  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 16 * D));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-__device__ __forceinline__ bf16x8 pack_p(const float (&x)[4], const float (&y)[4]) {
+__device__ __forceinline__ bf16x8 pack_p(const f32x4& x, const f32x4& y) {
   return bf16x8{from_f32<bf16>(x[0]), from_f32<bf16>(x[1]), from_f32<bf16>(x[2]), from_f32<bf16>(x[3]),
                 from_f32<bf16>(y[0]), from_f32<bf16>(y[1]), from_f32<bf16>(y[2]), from_f32<bf16>(y[3])};
 }
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
 
 __device__ __forceinline__ void bar() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
+template <int V>
+using Slot = std::integral_constant<int, V>;
 
 // Inverse rotation of a gradient held as lane tiles acc[dt] (rows d = 16dt +
 // 4g + i): pairs (d, d + r/2) for d < r/2, angle -p*theta.
-template <int D>
-__device__ __forceinline__ void rope_back(f32x4 (&acc)[D / 16], int p, int r, int fg, const float* ct,
-                                          const float* stb) {
+template <int D, typename Acc>
+__device__ __forceinline__ void rope_back(Acc& acc, int p, int r, int fg, const float* ct, const float* stb) {
   const int half = r / 2, ht = half / 16;
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
@@ -118,12 +137,20 @@ __device__ __forceinline__ void rope_back(f32x4 (&acc)[D / 16], int p, int r, in
   }
 }
 
+// Key tile [j0, j0 + 64) against queries [qlo, qlo + nq): none visible / all
+// visible (keys inside the sequence, each at or before every query or in the
+// prefix).  Wave-uniform, so only diagonal and ragged tiles pay for masking.
+__device__ __forceinline__ bool tile_dark(int j0, int qlo, int nq, int P) { return j0 > qlo + nq - 1 && j0 >= P; }
+__device__ __forceinline__ bool tile_full(int j0, int qlo, int L, int P) {
+  return j0 + kRows <= L && (j0 + kRows - 1 <= qlo || j0 + kRows <= P);
+}
+
 // ---------------------------------------------------------------------------
 // Forward: 128 queries per workgroup (4 waves x 32), key tiles of 64.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
-  constexpr int NC = D / 32, QS = 2, BM = 128;
+__global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
+  constexpr int NC = D / 32, ND = D / 16, QS = 2, BM = 128;
   __shared__ __attribute__((aligned(1024))) bf16 Ks[2][kRows * D];
   __shared__ __attribute__((aligned(1024))) bf16 Vs[2][kRows * D];
 
@@ -137,6 +164,8 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
   const long ld = a.ld_qkv;
   const int H = a.hidden;
   const float sl2 = kLog2e / sqrtf((float)D);
+  FragBase<D> fb;
+  fb.init(fr, fg);
 
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
   const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
@@ -150,10 +179,11 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
   };
   issue(0);
 
+  const int qlo = q0 + 32 * w;  // this wave's queries: qlo + 16 qs + fr
   bf16x8 qf[QS][NC];
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
-    const int qi = q0 + 32 * w + 16 * qs + fr;
+    const int qi = qlo + 16 * qs + fr;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
       qf[qs][c] = qi < si.L ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + qi) * ld + h * D + 32 * c + 8 * fg))
@@ -163,23 +193,27 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
   for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
     for (int c = 0; c < NC; ++c) settle(qf[qs][c]);
-  f32x4 acc[D / 16][QS];
+  f32x4 acc[ND][QS];
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt)
+  for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // running maximum (log2 units of the scaled scores) and sum; key 0 is
+  // visible to every query, so the maximum is finite after the first tile
   float m[QS], l[QS];
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) { m[qs] = -INFINITY; l[qs] = 0.f; }
 
-  for (int kt = 0; kt < nkt; ++kt) {
+  auto step = [&](auto slot, int kt) {
+    constexpr int SL = decltype(slot)::value;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    bar();  // tile kt landed for every wave; slot (kt+1)&1 is free
+    bar();  // tile kt landed for every wave; the other slot is free
     if (kt + 1 < nkt) issue(kt + 1);
-    const bf16* ks = Ks[kt & 1];
-    const bf16* vs = Vs[kt & 1];
     const int j0 = kt * kRows;
-
+    if (tile_dark(j0, qlo, 32, si.P)) return;
+    const bool full = tile_full(j0, qlo, si.L, si.P);
+    const bf16* ks = Ks[SL];
+    const bf16* vs = Vs[SL];
     f32x4 st[QS][4];
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs)
@@ -189,56 +223,63 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
     for (int c = 0; c < NC; ++c) {
       bf16x8 kf[4];
 #pragma unroll
-      for (int at = 0; at < 4; ++at) kf[at] = frag_row<D>(ks, 16 * at, c, fr, fg);
+      for (int at = 0; at < 4; ++at) kf[at] = rd_row(ks + 16 * at * D + fb.row[c]);
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
         for (int at = 0; at < 4; ++at) st[qs][at] = mma16(kf[at], qf[qs][c], st[qs][at]);
     }
-    float p[QS][4][4];
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
-      const int qi = q0 + 32 * w + 16 * qs + fr;
-      float mx = -INFINITY;
+      if (!full) {
+        const int qi = qlo + 16 * qs + fr;
+#pragma unroll
+        for (int at = 0; at < 4; ++at)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            st[qs][at][i] = vis(qi, j0 + 16 * at + 4 * fg + i, si.L, si.P) ? st[qs][at][i] : -INFINITY;
+      }
+      float mx = st[qs][0][0];
 #pragma unroll
       for (int at = 0; at < 4; ++at)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = j0 + 16 * at + 4 * fg + i;
-          const float v = vis(qi, j, si.L, si.P) ? st[qs][at][i] * sl2 : -INFINITY;
-          p[qs][at][i] = v;
-          mx = fmaxf(mx, v);
-        }
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[qs][at][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(m[qs], mx);
-      const float alpha = (mnew == -INFINITY) ? 1.f : exp2f(m[qs] - mnew);
+      const float mnew = fmaxf(m[qs], mx * sl2);
+      const float alpha = ex2(m[qs] - mnew);
       m[qs] = mnew;
       float ls = 0.f;
 #pragma unroll
       for (int at = 0; at < 4; ++at)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float e = (p[qs][at][i] == -INFINITY) ? 0.f : exp2f(p[qs][at][i] - mnew);
-          p[qs][at][i] = e;
+          const float e = ex2(fmaf(st[qs][at][i], sl2, -mnew));
+          st[qs][at][i] = e;
           ls += e;
         }
       l[qs] = l[qs] * alpha + ls;
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) acc[dt][qs] *= alpha;
+        for (int dt = 0; dt < ND; ++dt) acc[dt][qs] *= alpha;
+      }
     }
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
       bf16x8 pf[QS];
 #pragma unroll
-      for (int qs = 0; qs < QS; ++qs) pf[qs] = pack_p(p[qs][2 * c2], p[qs][2 * c2 + 1]);
+      for (int qs = 0; qs < QS; ++qs) pf[qs] = pack_p(st[qs][2 * c2], st[qs][2 * c2 + 1]);
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16x8 vf = frag_tr<D>(vs, 32 * c2, 16 * dt, fr, fg);
+      for (int dt = 0; dt < ND; ++dt) {
+        const bf16x8 vf = rd_tr<D>(vs + 32 * c2 * D + fb.tr[dt]);
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = mma16(vf, pf[qs], acc[dt][qs]);
       }
     }
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(Slot<0>{}, kt);
+    if (kt + 1 < nkt) step(Slot<1>{}, kt + 1);
   }
 
   bf16* o = static_cast<bf16*>(a.o);
@@ -247,11 +288,11 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
     float lt = l[qs];
     lt += __shfl_xor(lt, 16, 64);
     lt += __shfl_xor(lt, 32, 64);
-    const int qi = q0 + 32 * w + 16 * qs + fr;
+    const int qi = qlo + 16 * qs + fr;
     if (qi >= si.L) continue;
     const float inv = 1.f / lt;
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
+    for (int dt = 0; dt < ND; ++dt) {
       const float v[4] = {acc[dt][qs][0] * inv, acc[dt][qs][1] * inv, acc[dt][qs][2] * inv, acc[dt][qs][3] * inv};
       Vec4<bf16> ov;
       ov.set(v);
@@ -262,11 +303,13 @@ __global__ void __launch_bounds__(256) fwd_kernel(AttnDesc a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward, dq: 64 queries per workgroup (4 waves x 16), key tiles of 64.
+// Backward, dq: 128 queries per workgroup (4 waves x 32), key tiles of 64.
+// Rows past the sequence end read as zero, so they add nothing to dq; only
+// the causal / prefix mask needs applying, on diagonal tiles.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
-  constexpr int NC = D / 32, BM = 64;
+__global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
+  constexpr int NC = D / 32, ND = D / 16, QS = 2, BM = 128;
   __shared__ __attribute__((aligned(1024))) bf16 Ks[2][kRows * D];
   __shared__ __attribute__((aligned(1024))) bf16 Vs[2][kRows * D];
 
@@ -281,6 +324,8 @@ __global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
   const long ld = a.ld_qkv;
   const int H = a.hidden;
   const float sl2 = kLog2e / sqrtf((float)D);
+  FragBase<D> fb;
+  fb.init(fr, fg);
 
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
   const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
@@ -294,84 +339,124 @@ __global__ void __launch_bounds__(256) dq_kernel(AttnDesc a) {
   };
   issue(0);
 
-  const int qi = q0 + 16 * w + fr;
-  const bool qvalid = qi < si.L;
-  bf16x8 qf[NC], dof[NC];
+  const int qlo = q0 + 32 * w;
+  bf16x8 qf[QS][NC], dof[QS][NC];
+  float lse2[QS], dlt[QS];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    qf[c] = qvalid ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + qi) * ld + h * D + 32 * c + 8 * fg))
-                   : bf16x8{};
-    dof[c] = qvalid ? __builtin_bit_cast(bf16x8,
-                                         ld16(dout + (long)(si.r0 + qi) * a.ld_dout + h * D + 32 * c + 8 * fg))
-                    : bf16x8{};
+  for (int qs = 0; qs < QS; ++qs) {
+    const int qi = qlo + 16 * qs + fr;
+    const bool ok = qi < si.L;
+    const long r = si.r0 + qi;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      qf[qs][c] = ok ? __builtin_bit_cast(bf16x8, ld16(qkv + r * ld + h * D + 32 * c + 8 * fg)) : bf16x8{};
+      dof[qs][c] = ok ? __builtin_bit_cast(bf16x8, ld16(dout + r * a.ld_dout + h * D + 32 * c + 8 * fg)) : bf16x8{};
+    }
+    lse2[qs] = ok ? a.lse[r * a.num_heads + h] * kLog2e : 0.f;
+    dlt[qs] = ok ? a.delta[r * a.num_heads + h] : 0.f;
   }
-  const float lse2 = qvalid ? a.lse[(long)(si.r0 + qi) * a.num_heads + h] * kLog2e : 0.f;
-  float dlt = qvalid ? a.delta[(long)(si.r0 + qi) * a.num_heads + h] : 0.f;
-  float lse2s = lse2;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) { settle(qf[c]); settle(dof[c]); }
-  settle(dlt);
-  settle(lse2s);
-  f32x4 acc[D / 16];
+  for (int qs = 0; qs < QS; ++qs) {
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < NC; ++c) { settle(qf[qs][c]); settle(dof[qs][c]); }
+    settle(lse2[qs]);
+    settle(dlt[qs]);
+  }
+  f32x4 acc[ND][QS];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kt = 0; kt < nkt; ++kt) {
+  auto step = [&](auto slot, int kt) {
+    constexpr int SL = decltype(slot)::value;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     bar();
     if (kt + 1 < nkt) issue(kt + 1);
-    const bf16* ks = Ks[kt & 1];
-    const bf16* vs = Vs[kt & 1];
     const int j0 = kt * kRows;
-    f32x4 st[4], dp[4];
-#pragma unroll
-    for (int at = 0; at < 4; ++at) { st[at] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[at] = st[at]; }
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-#pragma unroll
-      for (int at = 0; at < 4; ++at) {
-        st[at] = mma16(frag_row<D>(ks, 16 * at, c, fr, fg), qf[c], st[at]);
-        dp[at] = mma16(frag_row<D>(vs, 16 * at, c, fr, fg), dof[c], dp[at]);
-      }
-    }
-    float ds[4][4];
-#pragma unroll
-    for (int at = 0; at < 4; ++at)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = j0 + 16 * at + 4 * fg + i;
-        const float pr = (qvalid && vis(qi, j, si.L, si.P)) ? exp2f(st[at][i] * sl2 - lse2s) : 0.f;
-        ds[at][i] = pr * (dp[at][i] - dlt);
-      }
+    if (tile_dark(j0, qlo, 32, si.P)) return;
+    const bool full = tile_full(j0, qlo, si.L, si.P);
+    const bf16* ks = Ks[SL];
+    const bf16* vs = Vs[SL];
+    // keys in two halves of 32 (reduction half c2 of the dq product), which
+    // keeps half of the score and dP tiles live at a time
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
-      const bf16x8 df = pack_p(ds[2 * c2], ds[2 * c2 + 1]);
+      f32x4 st[QS][2], dp[QS][2];
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) acc[dt] = mma16(frag_tr<D>(ks, 32 * c2, 16 * dt, fr, fg), df, acc[dt]);
+      for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) { st[qs][u] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[qs][u] = st[qs][u]; }
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int at = 2 * c2 + u;
+          const bf16x8 kf = rd_row(ks + 16 * at * D + fb.row[c]);
+          const bf16x8 vf = rd_row(vs + 16 * at * D + fb.row[c]);
+#pragma unroll
+          for (int qs = 0; qs < QS; ++qs) {
+            st[qs][u] = mma16(kf, qf[qs][c], st[qs][u]);
+            dp[qs][u] = mma16(vf, dof[qs][c], dp[qs][u]);
+          }
+        }
+      }
+      bf16x8 df[QS];
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) {
+        const int qi = qlo + 16 * qs + fr;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float pr = ex2(fmaf(st[qs][u][i], sl2, -lse2[qs]));
+            pr = (full | vis(qi, j0 + 16 * (2 * c2 + u) + 4 * fg + i, si.L, si.P)) ? pr : 0.f;
+            st[qs][u][i] = pr * (dp[qs][u][i] - dlt[qs]);
+          }
+        df[qs] = pack_p(st[qs][0], st[qs][1]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) {
+        const bf16x8 kt_ = rd_tr<D>(ks + 32 * c2 * D + fb.tr[dt]);
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = mma16(kt_, df[qs], acc[dt][qs]);
+      }
     }
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(Slot<0>{}, kt);
+    if (kt + 1 < nkt) step(Slot<1>{}, kt + 1);
   }
-  if (!qvalid) return;
+
   const float sc = 1.f / sqrtf((float)D);
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) acc[dt] *= sc;
-  rope_back<D>(acc, qi, a.rotary_dim, fg, a.cos_t, a.sin_t);
-  bf16* dq = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + qi) * a.ld_dqkv + h * D;
+  for (int qs = 0; qs < QS; ++qs) {
+    const int qi = qlo + 16 * qs + fr;
+    if (qi >= si.L) continue;
+    f32x4 g[ND];
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const float v[4] = {acc[dt][0], acc[dt][1], acc[dt][2], acc[dt][3]};
-    Vec4<bf16> ov;
-    ov.set(v);
-    ov.store(dq + 16 * dt + 4 * fg);
+    for (int dt = 0; dt < ND; ++dt) g[dt] = acc[dt][qs] * sc;
+    rope_back<D>(g, qi, a.rotary_dim, fg, a.cos_t, a.sin_t);
+    bf16* dq = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + qi) * a.ld_dqkv + h * D;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      const float v[4] = {g[dt][0], g[dt][1], g[dt][2], g[dt][3]};
+      Vec4<bf16> ov;
+      ov.set(v);
+      ov.store(dq + 16 * dt + 4 * fg);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // Backward, dk and dv: 64 keys per workgroup (4 waves x 16), query tiles of
-// 64 with their LSE and delta rows.
+// 64 with their LSE and delta rows.  Query rows past the sequence end read
+// as zero (and their LSE and delta as zero), which makes their dS and their
+// dO rows zero: they add nothing, so again only diagonal tiles are masked.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
-  constexpr int NC = D / 32, BK = 64;
+__global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
+  constexpr int NC = D / 32, ND = D / 16, BK = 64;
   __shared__ __attribute__((aligned(1024))) bf16 Qs[2][kRows * D];
   __shared__ __attribute__((aligned(1024))) bf16 Os[2][kRows * D];
   __shared__ __attribute__((aligned(256))) float Ls[2][kRows];
@@ -388,6 +473,8 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
   const long ld = a.ld_qkv;
   const int H = a.hidden, nh = a.num_heads;
   const float sl2 = kLog2e / sqrtf((float)D);
+  FragBase<D> fb;
+  fb.init(fr, fg);
 
   const auto rq = buf_rsrc(qkv + (long)si.r0 * ld + h * D, (uint32_t)((long)si.L * ld * 2));
   const auto ro = buf_rsrc(dout + (long)si.r0 * a.ld_dout + h * D, (uint32_t)((long)si.L * a.ld_dout * 2));
@@ -397,8 +484,9 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
   const int nqt = (si.L + kRows - 1) / kRows;
   const uint32_t lds_q = FL_LDS_ADDR(&Qs[0][0]), lds_o = FL_LDS_ADDR(&Os[0][0]);
   const uint32_t lds_l = FL_LDS_ADDR(&Ls[0][0]), lds_d = FL_LDS_ADDR(&Ds[0][0]);
+  // query tile qt lives in slot (qt - qstart) & 1
   auto issue = [&](int qt) {
-    const int slot = qt & 1;
+    const int slot = (qt - qstart) & 1;
     dma_tile<D>(rq, ld, qt * kRows, lds_q + slot * (kRows * D * 2), w, lane);
     dma_tile<D>(ro, a.ld_dout, qt * kRows, lds_o + slot * (kRows * D * 2), w, lane);
     // LSE (scaled on use) and delta rows: 64 x 4 bytes each
@@ -408,7 +496,8 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
   };
   issue(qstart);
 
-  const int kj = k0 + 16 * w + fr;
+  const int klo = k0 + 16 * w;  // this wave's keys: klo + fr
+  const int kj = klo + fr;
   const bool kvalid = kj < si.L;
   bf16x8 kf[NC], vf[NC];
 #pragma unroll
@@ -421,35 +510,41 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
   }
 #pragma unroll
   for (int c = 0; c < NC; ++c) { settle(kf[c]); settle(vf[c]); }
-  f32x4 dk[D / 16], dv[D / 16];
+  f32x4 dk[ND], dv[ND];
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) { dk[dt] = f32x4{0.f, 0.f, 0.f, 0.f}; dv[dt] = dk[dt]; }
+  for (int dt = 0; dt < ND; ++dt) { dk[dt] = f32x4{0.f, 0.f, 0.f, 0.f}; dv[dt] = dk[dt]; }
 
-  for (int qt = qstart; qt < nqt; ++qt) {
+  auto step = [&](auto slot, int qt) {
+    constexpr int SL = decltype(slot)::value;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     bar();
     if (qt + 1 < nqt) issue(qt + 1);
-    const bf16* qs_ = Qs[qt & 1];
-    const bf16* os_ = Os[qt & 1];
-    const float* ls_ = Ls[qt & 1];
-    const float* dls = Ds[qt & 1];
     const int qb = qt * kRows;
-    float pr[4][4], ds[4][4];
+    // queries [qb, qb + 64) against keys [klo, klo + 16)
+    if (qb + kRows - 1 < klo && klo >= si.P) return;
+    const bool full = qb >= klo + 15 || klo + 15 < si.P;
+    const bf16* qs_ = Qs[SL];
+    const bf16* os_ = Os[SL];
+    const float* ls_ = Ls[SL];
+    const float* dls = Ds[SL];
+    f32x4 pr[4], ds[4];
 #pragma unroll
     for (int qs = 0; qs < 4; ++qs) {
       f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f}, dp = st;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        st = mma16(frag_row<D>(qs_, 16 * qs, c, fr, fg), kf[c], st);
-        dp = mma16(frag_row<D>(os_, 16 * qs, c, fr, fg), vf[c], dp);
+        st = mma16(rd_row(qs_ + 16 * qs * D + fb.row[c]), kf[c], st);
+        dp = mma16(rd_row(os_ + 16 * qs * D + fb.row[c]), vf[c], dp);
       }
+      // rows q = qb + 16 qs + 4 g + i of this lane's column kj
+      const f32x4 lq = __builtin_bit_cast(f32x4, ld16(ls_ + 16 * qs + 4 * fg));
+      const f32x4 dq = __builtin_bit_cast(f32x4, ld16(dls + 16 * qs + 4 * fg));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int ql = 16 * qs + 4 * fg + i;
-        const int q = qb + ql;
-        const float p = (kvalid && vis(q, kj, si.L, si.P)) ? exp2f(st[i] * sl2 - ls_[ql] * kLog2e) : 0.f;
+        float p = ex2(fmaf(st[i], sl2, -lq[i] * kLog2e));
+        p = (full | vis(qb + 16 * qs + 4 * fg + i, kj, si.L, si.P)) ? p : 0.f;
         pr[qs][i] = p;
-        ds[qs][i] = p * (dp[i] - dls[ql]);
+        ds[qs][i] = p * (dp[i] - dq[i]);
       }
     }
 #pragma unroll
@@ -457,20 +552,24 @@ __global__ void __launch_bounds__(256) dkdv_kernel(AttnDesc a) {
       const bf16x8 pf = pack_p(pr[2 * c2], pr[2 * c2 + 1]);
       const bf16x8 df = pack_p(ds[2 * c2], ds[2 * c2 + 1]);
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        dv[dt] = mma16(frag_tr<D>(os_, 32 * c2, 16 * dt, fr, fg), pf, dv[dt]);
-        dk[dt] = mma16(frag_tr<D>(qs_, 32 * c2, 16 * dt, fr, fg), df, dk[dt]);
+      for (int dt = 0; dt < ND; ++dt) {
+        dv[dt] = mma16(rd_tr<D>(os_ + 32 * c2 * D + fb.tr[dt]), pf, dv[dt]);
+        dk[dt] = mma16(rd_tr<D>(qs_ + 32 * c2 * D + fb.tr[dt]), df, dk[dt]);
       }
     }
+  };
+  for (int qt = qstart; qt < nqt; qt += 2) {
+    step(Slot<0>{}, qt);
+    if (qt + 1 < nqt) step(Slot<1>{}, qt + 1);
   }
   if (!kvalid) return;
   const float sc = 1.f / sqrtf((float)D);
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) dk[dt] *= sc;
+  for (int dt = 0; dt < ND; ++dt) dk[dt] *= sc;
   rope_back<D>(dk, kj, a.rotary_dim, fg, a.cos_t, a.sin_t);
   bf16* row = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + kj) * a.ld_dqkv + h * D;
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
+  for (int dt = 0; dt < ND; ++dt) {
     const float vk[4] = {dk[dt][0], dk[dt][1], dk[dt][2], dk[dt][3]};
     const float vv[4] = {dv[dt][0], dv[dt][1], dv[dt][2], dv[dt][3]};
     Vec4<bf16> ok, ov;
@@ -492,10 +591,11 @@ template <int D>
 hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
   hipError_t e = attn_delta(DT_BF16, a, st);
   if (e != hipSuccess) return e;
-  dim3 grid((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
-  hipLaunchKernelGGL((dkdv_kernel<D>), grid, dim3(256), 0, st, a);
+  const dim3 gkv((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
+  hipLaunchKernelGGL((dkdv_kernel<D>), gkv, dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((dq_kernel<D>), grid, dim3(256), 0, st, a);
+  const dim3 gq((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
+  hipLaunchKernelGGL((dq_kernel<D>), gq, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
