@@ -69,29 +69,21 @@ __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_inst_base, uint32_t
   dma_lds<16>(rs, lds_inst_base, voff);
 }
 
-// K-contiguous tile [256 rows][64]: 2048 chunks, 4 DMA instructions per wave.
-__device__ __forceinline__ void load_k_tile(i32x4 rs, long ld, int k0, uint32_t tile, int wave,
-                                            int lane) {
-#pragma unroll
-  for (int i = 0; i < 32 / kWaves; ++i) {
-    const int inst = i * kWaves + wave;
-    const int lin = inst * 64 + lane;
-    const int row = lin >> 3, q = (lin & 7) ^ swz_k(row);
-    dma16(rs, tile + inst * 1024, (uint32_t)(row * ld + k0 + q * 8) * 2u);
-  }
+// Per-lane source byte offsets (reduction index 0) of DMA instruction inst
+// (0..31) of an operand tile.
+// K-contiguous tile [256 rows][64]: instruction inst fills rows 8 inst ..
+// 8 inst + 7, 128 bytes each.
+__device__ __forceinline__ uint32_t k_src(long ld, int inst, int lane) {
+  const int lin = inst * 64 + lane;
+  const int row = lin >> 3, q = (lin & 7) ^ swz_k(row);
+  return (uint32_t)(row * ld + q * 8) * 2u;
 }
-
-// MN-contiguous tile: 4 column blocks of [64 k][64 columns] (8 KB each); a
-// DMA instruction fills 8 k-rows of 128 bytes; 4 per wave.
-__device__ __forceinline__ void load_m_tile(i32x4 rs, long ld, int k0, uint32_t tile, int wave,
-                                            int lane) {
-#pragma unroll
-  for (int i = 0; i < 32 / kWaves; ++i) {
-    const int inst = i * kWaves + wave;  // 0..31: block inst/8, k-rows 8*(inst%8) ..
-    const int blk = inst >> 3, krow = (inst & 7) * 8 + (lane >> 3);
-    const int q = (lane & 7) ^ swz_m(krow);
-    dma16(rs, tile + inst * 1024, (uint32_t)((long)(k0 + krow) * ld + blk * 64 + q * 8) * 2u);
-  }
+// MN-contiguous tile: 4 column blocks of [64 k][64 columns] (8 KB each);
+// instruction inst fills k-rows 8 (inst % 8) .. + 7 of block inst / 8.
+__device__ __forceinline__ uint32_t m_src(long ld, int inst, int lane) {
+  const int blk = inst >> 3, krow = (inst & 7) * 8 + (lane >> 3);
+  const int q = (lane & 7) ^ swz_m(krow);
+  return (uint32_t)((long)krow * ld + blk * 64 + q * 8) * 2u;
 }
 
 // Per-lane fragment bases (element offsets inside one operand tile).
@@ -180,15 +172,31 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   } else {
     rb = buf_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
   }
+  // DMA bookkeeping.  Instruction i (0..3) of this wave fills 1 KB of an
+  // operand tile at byte (8 i + wave) * 1024; its per-lane source offset is
+  // fixed up to the stage's reduction offset, added per stage.
   const uint32_t lds0 = FL_LDS_ADDR(&smem[0][0][0]);
+  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + wave * 1024);
+  uint32_t voa[4], vob[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    voa[i] = AK ? k_src(p.lda, i * kWaves + wave, lane) : m_src(p.lda, i * kWaves + wave, lane);
+    vob[i] = BKc ? k_src(p.ldb, i * kWaves + wave, lane) : m_src(p.ldb, i * kWaves + wave, lane);
+  }
+  // byte offset of reduction index k0 along each operand
+  auto kstep_a = [&](int k0) { return AK ? (uint32_t)k0 * 2u : (uint32_t)((long)k0 * p.lda * 2); };
+  auto kstep_b = [&](int k0) { return BKc ? (uint32_t)k0 * 2u : (uint32_t)((long)k0 * p.ldb * 2); };
+  // DMA instruction g (0..7: A 0..3, B 0..3) of stage kt
+  auto dma_one = [&](int kt, int g) {
+    const uint32_t slot_off = (uint32_t)(kt & (kStages - 1)) * (2 * kTileElems * 2);
+    if (g < 4)
+      dma16(ra, lds_wave + slot_off + g * 8192, voa[g] + kstep_a(kt * kBK));
+    else
+      dma16(rb, lds_wave + slot_off + kTileElems * 2 + (g - 4) * 8192, vob[g - 4] + kstep_b(kt * kBK));
+  };
   auto issue = [&](int kt) {
-    // byte addresses of this stage's A and B tiles
-    const uint32_t sa = lds0 + (uint32_t)(kt & (kStages - 1)) * (2 * kTileElems * 2);
-    const uint32_t sb = sa + kTileElems * 2;
-    if constexpr (AK) load_k_tile(ra, p.lda, kt * kBK, sa, wave, lane);
-    else load_m_tile(ra, p.lda, kt * kBK, sa, wave, lane);
-    if constexpr (BKc) load_k_tile(rb, p.ldb, kt * kBK, sb, wave, lane);
-    else load_m_tile(rb, p.ldb, kt * kBK, sb, wave, lane);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) dma_one(kt, g);
   };
   const int abase = AK ? frag_k_base(wm * 128, fr, fg) : frag_m_base(wm * 128, fr, fg);
   const int bbase = BKc ? frag_k_base(wn * 64, fr, fg) : frag_m_base(wn * 64, fr, fg);
@@ -200,14 +208,20 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     for (int j = 0; j < kWTM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = (p.K + kBK - 1) / kBK;
+  auto rd_a = [&](int slot, int c, int j) {
+    const bf16* as = smem[slot][0];
+    return AK ? frag_k(as, abase, c, j) : frag_m(as, abase, c, j);
+  };
+  auto rd_b = [&](int slot, int c, int i) {
+    const bf16* bs = smem[slot][1];
+    return BKc ? frag_k(bs, bbase, c, i) : frag_m(bs, bbase, c, i);
+  };
   // fragments of reduction half c of the stage in slot `slot`
   auto load_frags = [&](int slot, int c, bf16x8 (&af)[kWTM], bf16x8 (&bf)[kWTN]) {
-    const bf16* as = smem[slot][0];
-    const bf16* bs = smem[slot][1];
 #pragma unroll
-    for (int i = 0; i < kWTN; ++i) bf[i] = BKc ? frag_k(bs, bbase, c, i) : frag_m(bs, bbase, c, i);
+    for (int i = 0; i < kWTN; ++i) bf[i] = rd_b(slot, c, i);
 #pragma unroll
-    for (int j = 0; j < kWTM; ++j) af[j] = AK ? frag_k(as, abase, c, j) : frag_m(as, abase, c, j);
+    for (int j = 0; j < kWTM; ++j) af[j] = rd_a(slot, c, j);
   };
   auto mma_all = [&](const bf16x8 (&af)[kWTM], const bf16x8 (&bf)[kWTN]) {
 #pragma unroll
@@ -234,22 +248,41 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   barrier();
   bf16x8 fa0[kWTM], fb0[kWTN], fa1[kWTM], fb1[kWTN];
   load_frags(0, 0, fa0, fb0);
-  // The last stage is peeled so that every path through the loop body passes
-  // the barrier: the compiler then knows the second-half fragments are
-  // complete there and lets the next stage's first-half reads overlap the
-  // second half's matrix-core work instead of waiting for them.
+  // Main loop, one stage per iteration, in two halves of 32 reductions.  The
+  // issue order is fixed by scheduling barriers: each group of four matrix
+  // instructions (one A fragment against the four B fragments) is preceded
+  // by one or two fragment reads for the next half and, in the second half,
+  // by one of the wave's eight DMA instructions for stage kt + 2, so the
+  // memory pipes are fed steadily instead of in bursts that stall issue.
+  // The last stage is peeled so that every path through the body passes the
+  // barrier (the compiler then never waits for next-half reads early).
   for (int kt = 0; kt < nk - 1; ++kt) {
     const int slot = kt & 1;
-    load_frags(slot, 1, fa1, fb1);
-    mma_all(fa0, fb0);
+#pragma unroll
+    for (int j = 0; j < kWTM; ++j) {
+      fa1[j] = rd_a(slot, 1, j);
+      if (j < kWTN) fb1[j] = rd_b(slot, 1, j);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < kWTN; ++i) acc[i][j] = mma16(fb0[i], fa0[j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     // stage kt+1 landed (own loads) and every wave has finished reading
     // slot kt: refill it with stage kt+2, read stage kt+1's first half
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     barrier();
-    if (kt + 2 < nk) issue(kt + 2);
-    load_frags(slot ^ 1, 0, fa0, fb0);
-    mma_all(fa1, fb1);
+    const bool more = kt + 2 < nk;
+#pragma unroll
+    for (int j = 0; j < kWTM; ++j) {
+      if (more) dma_one(kt + 2, j);
+      fa0[j] = rd_a(slot ^ 1, 0, j);
+      if (j < kWTN) fb0[j] = rd_b(slot ^ 1, 0, j);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < kWTN; ++i) acc[i][j] = mma16(fb1[i], fa1[j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
   load_frags((nk - 1) & 1, 1, fa1, fb1);
   mma_all(fa0, fb0);
