@@ -148,12 +148,21 @@ template <bool AK, bool BKc, int EPI>
 __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kTileElems];  // [stage][A/B]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tiles_m = (p.M + kBM - 1) / kBM, tiles_n = p.N / kBN;
+  const int ntiles = tiles_m * tiles_n;
+  // Persistent: one workgroup per CU walks the tiles; a tile's epilogue
+  // stores drain while the next tile's first stages load.
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  // Per-lane values are rederived in every tile (the opaque copy keeps the
+  // compiler from hoisting them out of the tile loop, where they would stay
+  // live across the whole body and spill).
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;  // wave tile: rows wm*128.., columns wn*64..
   const int fr = lane & 15, fg = lane >> 4;
-  const int tiles_m = (p.M + kBM - 1) / kBM, tiles_n = p.N / kBN;
   int tm, tn;
-  tile_coords2(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_coords2(t, ntiles, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
 
   // Resources: K-contiguous -> base at the tile's first row, bound = its
@@ -308,22 +317,8 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   }
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
-    // Rows wave, wave + 8, ... of this half: issue every row's global loads
-    // (residual, GeLU input, fp32 accumulator) before the first use so they
-    // are in flight together.
     constexpr int kRows = 128 / kWaves;
     const int mbase = m0 + half * 128 + wave;
-    Vec4<bf16> ext[kRows];
-    Vec4<float> cacc[kRows];
-#pragma unroll
-    for (int q = 0; q < kRows; ++q) {
-      const long m = mbase + q * kWaves;
-      if (m < p.M) {
-        if constexpr (EPI == EPI_BIAS_RES) ext[q].load(p.R + m * p.ldr + n);
-        if constexpr (EPI == EPI_GELU_BWD) ext[q].load(p.Z + m * p.ldz + n);
-        if constexpr (EPI == EPI_ACC_F32) cacc[q].load(static_cast<float*>(p.C) + m * p.ldc + n);
-      }
-    }
     if (wm == half) {
 #pragma unroll
       for (int j = 0; j < kWTM; ++j) {
@@ -337,46 +332,77 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     barrier();
+    // Rows wave + 8 q, in batches whose global loads (residual, GeLU input,
+    // fp32 accumulator) are issued together before their first use.
+    constexpr int kBatch = EPI == EPI_ACC_F32 ? 4 : 8;
 #pragma unroll
-    for (int q = 0; q < kRows; ++q) {
-      const int r = wave + q * kWaves;
-      const long m = mbase + q * kWaves;
-      if (m >= p.M) break;
-      const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
-      float v[4];
+    for (int q0 = 0; q0 < kRows; q0 += kBatch) {
+      Vec4<bf16> ext[kBatch];
+      Vec4<float> cacc[kBatch];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
-      if constexpr (EPI == EPI_ACC_F32) {
-        float o[4] = {cacc[q].get(0) + v[0], cacc[q].get(1) + v[1], cacc[q].get(2) + v[2], cacc[q].get(3) + v[3]};
-        cacc[q].set(o);
-        cacc[q].store(static_cast<float*>(p.C) + m * p.ldc + n);
-      } else {
-        if constexpr (EPI == EPI_BIAS_RES) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += ext[q].get(e);
+      for (int u = 0; u < kBatch; ++u) {
+        const long m = mbase + (q0 + u) * kWaves;
+        if (m < p.M) {
+          if constexpr (EPI == EPI_BIAS_RES) ext[u].load(p.R + m * p.ldr + n);
+          if constexpr (EPI == EPI_GELU_BWD) ext[u].load(p.Z + m * p.ldz + n);
+          if constexpr (EPI == EPI_ACC_F32) cacc[u].load(static_cast<float*>(p.C) + m * p.ldc + n);
         }
-        if constexpr (EPI == EPI_GELU_BWD) {
+      }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[q].get(e));
-        }
-        Vec4<bf16> o;
-        o.set(v);
-        o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
-        if constexpr (EPI == EPI_BIAS_GELU) {
-          float g[4];
+      for (int u = 0; u < kBatch; ++u) {
+        const int r = wave + (q0 + u) * kWaves;
+        const long m = mbase + (q0 + u) * kWaves;
+        if (m >= p.M) break;
+        const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
+        float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
-          Vec4<bf16> og;
-          og.set(g);
-          og.store(p.C2 + m * p.ldc2 + n);
+        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
+        if constexpr (EPI == EPI_ACC_F32) {
+          float o[4] = {cacc[u].get(0) + v[0], cacc[u].get(1) + v[1], cacc[u].get(2) + v[2], cacc[u].get(3) + v[3]};
+          cacc[u].set(o);
+          cacc[u].store(static_cast<float*>(p.C) + m * p.ldc + n);
+        } else {
+          if constexpr (EPI == EPI_BIAS_RES) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] += ext[u].get(e);
+          }
+          if constexpr (EPI == EPI_GELU_BWD) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[u].get(e));
+          }
+          Vec4<bf16> o;
+          o.set(v);
+          o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
+          if constexpr (EPI == EPI_BIAS_GELU) {
+            float g[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
+            Vec4<bf16> og;
+            og.set(g);
+            og.store(p.C2 + m * p.ldc2 + n);
+          }
         }
       }
     }
-    if (half == 0) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();  // the second half overwrites the staging buffer
-    }
+    // the second half, or the next tile's loads, overwrite the staging area
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();
   }
+  }
+}
+
+// Compute units of the current device (one persistent workgroup each; a
+// multiple of the 8 XCDs on MI355X, which the tile order relies on).
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n - n % 8 > 0 ? n - n % 8 : n;
+  }
+  return cached[dev];
 }
 
 template <bool AK, bool BKc, int EPI>
@@ -388,7 +414,8 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(tiles), dim3(kThr), 0, st, a);
+  const int cus = num_cus();
+  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(tiles < cus ? tiles : cus), dim3(kThr), 0, st, a);
   return hipGetLastError();
 }
 
