@@ -137,6 +137,31 @@ __device__ __forceinline__ void rope_back(Acc& acc, int p, int r, int fg, const 
   }
 }
 
+// Workgroup -> (row tile, head, sequence), XCD-aware.  Workgroup i runs on
+// XCD i % 8.  (sequence, head) groups are dealt round-robin to the XCDs
+// (every XCD gets every eighth head of every sequence, which balances
+// ragged lengths), and each group's row tiles run back to back on its XCD,
+// so the tiles that stream the same K/V (or Q/dO) rows share one L2.  The
+// tile order inside a group is reversed: the longest-running tiles start
+// first.  Groups past the real count exit.
+struct WgCoord {
+  int tile, h, s;
+};
+__device__ __forceinline__ WgCoord wg_coord(int ntiles, int nh) {
+  const int i = blockIdx.x, x = i % 8, j = i / 8;
+  const int gi = j / ntiles;
+  WgCoord c;
+  c.tile = ntiles - 1 - (j - gi * ntiles);
+  const int g = gi * 8 + x;
+  c.h = g % nh;
+  c.s = g / nh;
+  return c;
+}
+__host__ __forceinline__ dim3 wg_grid(int ntiles, int nh, int nseq) {
+  const long groups = ((long)nh * nseq + 7) / 8 * 8;
+  return dim3((unsigned)(groups * ntiles));
+}
+
 // Key tile [j0, j0 + 64) against queries [qlo, qlo + nq): none visible / all
 // visible (keys inside the sequence, each at or before every query or in the
 // prefix).  Wave-uniform, so only diagonal and ragged tiles pay for masking.
@@ -154,8 +179,9 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
   __shared__ __attribute__((aligned(1024))) bf16 Ks[2][kRows * D];
   __shared__ __attribute__((aligned(1024))) bf16 Vs[2][kRows * D];
 
-  const int s = blockIdx.z, h = blockIdx.y;
-  const int q0 = (gridDim.x - 1 - blockIdx.x) * BM;  // longest-running query tiles first
+  const WgCoord wc = wg_coord((a.max_seqlen + BM - 1) / BM, a.num_heads);
+  if (wc.s >= a.num_seqs) return;
+  const int s = wc.s, h = wc.h, q0 = wc.tile * BM;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
   if (q0 >= si.L) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -313,8 +339,9 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
   __shared__ __attribute__((aligned(1024))) bf16 Ks[2][kRows * D];
   __shared__ __attribute__((aligned(1024))) bf16 Vs[2][kRows * D];
 
-  const int s = blockIdx.z, h = blockIdx.y;
-  const int q0 = (gridDim.x - 1 - blockIdx.x) * BM;
+  const WgCoord wc = wg_coord((a.max_seqlen + BM - 1) / BM, a.num_heads);
+  if (wc.s >= a.num_seqs) return;
+  const int s = wc.s, h = wc.h, q0 = wc.tile * BM;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
   if (q0 >= si.L) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -462,8 +489,9 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   __shared__ __attribute__((aligned(256))) float Ls[2][kRows];
   __shared__ __attribute__((aligned(256))) float Ds[2][kRows];
 
-  const int s = blockIdx.z, h = blockIdx.y;
-  const int k0 = (gridDim.x - 1 - blockIdx.x) * BK;
+  const WgCoord wc = wg_coord((a.max_seqlen + BK - 1) / BK, a.num_heads);
+  if (wc.s >= a.num_seqs) return;
+  const int s = wc.s, h = wc.h, k0 = wc.tile * BK;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
   if (k0 >= si.L) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -527,35 +555,71 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
     const bf16* os_ = Os[SL];
     const float* ls_ = Ls[SL];
     const float* dls = Ds[SL];
-    f32x4 pr[4], ds[4];
+    // Software pipeline with a fixed issue order (scheduling barriers):
+    //   phase 1, steps n = (qs, c): S^T and dP^T tiles, fragment reads two
+    //   steps ahead; the softmax-gradient arithmetic of query group qs - 1
+    //   runs between the matrix instructions of group qs;
+    //   phase 3, steps n = (c2, dt): dV^T and dK^T, transpose reads two steps
+    //   ahead.
+    constexpr int N1 = 4 * NC, N3 = 2 * ND;
+    f32x4 st[4], dp[4], pr[4], dsv[4];
 #pragma unroll
-    for (int qs = 0; qs < 4; ++qs) {
-      f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f}, dp = st;
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        st = mma16(rd_row(qs_ + 16 * qs * D + fb.row[c]), kf[c], st);
-        dp = mma16(rd_row(os_ + 16 * qs * D + fb.row[c]), vf[c], dp);
-      }
-      // rows q = qb + 16 qs + 4 g + i of this lane's column kj
-      const f32x4 lq = __builtin_bit_cast(f32x4, ld16(ls_ + 16 * qs + 4 * fg));
-      const f32x4 dq = __builtin_bit_cast(f32x4, ld16(dls + 16 * qs + 4 * fg));
+    for (int q = 0; q < 4; ++q) { st[q] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[q] = st[q]; }
+    f32x4 lq[2], dq[2];
+    bf16x8 pf[2], df[2];
+    auto rd1 = [&](int n, bf16x8& x, bf16x8& y) {
+      const int q = n / NC, c = n % NC;
+      x = rd_row(qs_ + 16 * q * D + fb.row[c]);
+      y = rd_row(os_ + 16 * q * D + fb.row[c]);
+    };
+    auto elem = [&](int q) {
+      // rows qb + 16 q + 4 g + i of this lane's column kj
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float p = ex2(fmaf(st[i], sl2, -lq[i] * kLog2e));
-        p = (full | vis(qb + 16 * qs + 4 * fg + i, kj, si.L, si.P)) ? p : 0.f;
-        pr[qs][i] = p;
-        ds[qs][i] = p * (dp[i] - dq[i]);
+        float pv = ex2(fmaf(st[q][i], sl2, -lq[q & 1][i] * kLog2e));
+        pv = (full | vis(qb + 16 * q + 4 * fg + i, kj, si.L, si.P)) ? pv : 0.f;
+        pr[q][i] = pv;
+        dsv[q][i] = pv * (dp[q][i] - dq[q & 1][i]);
       }
+      if (q & 1) {
+        pf[q >> 1] = pack_p(pr[q - 1], pr[q]);
+        df[q >> 1] = pack_p(dsv[q - 1], dsv[q]);
+      }
+    };
+    bf16x8 fq[3], fo[3];
+    rd1(0, fq[0], fo[0]);
+    rd1(1, fq[1], fo[1]);
+#pragma unroll
+    for (int n = 0; n < N1; ++n) {
+      const int q = n / NC, c = n % NC;
+      if (n + 2 < N1) rd1(n + 2, fq[(n + 2) % 3], fo[(n + 2) % 3]);
+      if (c == 0) {
+        lq[q & 1] = __builtin_bit_cast(f32x4, ld16(ls_ + 16 * q + 4 * fg));
+        dq[q & 1] = __builtin_bit_cast(f32x4, ld16(dls + 16 * q + 4 * fg));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      st[q] = mma16(fq[n % 3], kf[c], st[q]);
+      dp[q] = mma16(fo[n % 3], vf[c], dp[q]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (c == 1 && q >= 1) elem(q - 1);
     }
+    auto rd3 = [&](int n, bf16x8& x, bf16x8& y) {
+      const int c2 = n / ND, dt = n % ND;
+      x = rd_tr<D>(os_ + 32 * c2 * D + fb.tr[dt]);
+      y = rd_tr<D>(qs_ + 32 * c2 * D + fb.tr[dt]);
+    };
+    bf16x8 to[3], tq[3];
+    rd3(0, to[0], tq[0]);
+    elem(3);
+    rd3(1, to[1], tq[1]);
 #pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
-      const bf16x8 pf = pack_p(pr[2 * c2], pr[2 * c2 + 1]);
-      const bf16x8 df = pack_p(ds[2 * c2], ds[2 * c2 + 1]);
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt) {
-        dv[dt] = mma16(rd_tr<D>(os_ + 32 * c2 * D + fb.tr[dt]), pf, dv[dt]);
-        dk[dt] = mma16(rd_tr<D>(qs_ + 32 * c2 * D + fb.tr[dt]), df, dk[dt]);
-      }
+    for (int n = 0; n < N3; ++n) {
+      const int c2 = n / ND, dt = n % ND;
+      if (n + 2 < N3) rd3(n + 2, to[(n + 2) % 3], tq[(n + 2) % 3]);
+      __builtin_amdgcn_sched_barrier(0);
+      dv[dt] = mma16(to[n % 3], pf[c2], dv[dt]);
+      dk[dt] = mma16(tq[n % 3], df[c2], dk[dt]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   for (int qt = qstart; qt < nqt; qt += 2) {
@@ -582,7 +646,7 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
 
 template <int D>
 hipError_t fwd_launch(const AttnDesc& a, hipStream_t st) {
-  dim3 grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
+  const dim3 grid = wg_grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((fwd_kernel<D>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
@@ -591,10 +655,10 @@ template <int D>
 hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
   hipError_t e = attn_delta(DT_BF16, a, st);
   if (e != hipSuccess) return e;
-  const dim3 gkv((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
+  const dim3 gkv = wg_grid((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((dkdv_kernel<D>), gkv, dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const dim3 gq((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
+  const dim3 gq = wg_grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((dq_kernel<D>), gq, dim3(256), 0, st, a);
   return hipGetLastError();
 }
