@@ -254,12 +254,21 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
     forward + recompute + backward over whole sequences of the workload,
     shortest first, until the budget is used; scaled to the full stack depth."""
     import oracle
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
-                      default=1)
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max((i.get("num_threads", 1) for i in info), default=1)
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
     except Exception:  # pragma: no cover
         threads = len(os.sched_getaffinity(0))
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "unknown")
+    except OSError:  # pragma: no cover
+        pass
     one = synth.StackShape(1, w.shape.hidden, w.shape.num_heads, w.shape.ffn_hidden, w.shape.rotary_dim,
                            w.shape.rope_base, w.shape.ln_eps)
     layer = synth.layer_params(w.shape, 0, seed=0, bf16=w.dtype == "bf16")
@@ -289,7 +298,8 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
         "kind": "oracle",
         "sample": (f"1 of {w.shape.num_layers} blocks, {'fwd+recompute+bwd' if w.backward else 'fwd'}, float64, "
                    f"{len(seqs)} whole sequence(s) of lengths {seqs} ({done_tokens} tokens) in {spent:.1f} s; "
-                   f"tokens/s divided by {w.shape.num_layers} blocks"),
+                   f"tokens/s divided by {w.shape.num_layers} blocks; host {cpu}, BLAS {blas}, "
+                   f"{len(os.sched_getaffinity(0))} cores visible"),
     }
 
 
@@ -357,14 +367,15 @@ def main() -> int:
         torch.cuda.synchronize()
         print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     F.fl_stack_profile(ss.handle, not args.no_profile)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    start.record(stream)
+    marks[0].record(stream)
     for i in range(args.steps):
         step()
-    end.record(stream)
+        marks[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
+    ms = marks[0].elapsed_time(marks[-1]) / args.steps
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     prof = F.profile_table(ss.handle)
     F.fl_stack_profile(ss.handle, False)
     print(f"[bench] timed {args.steps} steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
@@ -382,6 +393,10 @@ def main() -> int:
         if r["bytes"] > 0 and name not in MFMA_CLASSES:
             ent["gbs"] = round(r["bytes"] / (r["ms"] / 1e3) / 1e9, 1)
         kernels[name] = ent
+    # hardware flops: every launch's own count (forward recompute launches
+    # included); the attention backward also recomputes S and dP twice (dk/dv
+    # and dq kernels): 14 H per pair against the 8 H counted as algorithmic
+    hw_flops = sum(r["flops"] * (14.0 / 8.0 if k == "attn_bwd" else 1.0) for k, r in prof.items()) / args.steps
     gemm_ms = sum(prof[k]["ms"] for k in GEMM_CLASSES if k in prof)
     gemm_fl = sum(prof[k]["flops"] for k in GEMM_CLASSES if k in prof)
     roofline = None
@@ -417,7 +432,11 @@ def main() -> int:
                    "max_seqlen": b.max_seqlen, "blocks": w.shape.num_layers, "hidden": w.shape.hidden,
                    "heads": w.shape.num_heads, "ffn": w.shape.ffn_hidden, "mask": w.mask,
                    "backward": w.backward, "recompute": w.recompute, "parallelism": "single GPU"},
+        "ms_per_step_median": round(per_step[len(per_step) // 2], 3),
+        "ms_per_step_min": round(per_step[0], 3),
         "mfma_util": round(flops["total"] / (ms / 1e3) / (peak * 1e12), 4),
+        "hfu": round(hw_flops / (ms / 1e3) / (peak * 1e12), 4) if hw_flops else None,
+        "hardware_tflop_per_step": round(hw_flops / 1e12, 3) if hw_flops else None,
         "gemm_mfma_util": round(gemm_fl / (gemm_ms / 1e3) / (peak * 1e12), 4) if gemm_ms else None,
         "algorithmic_tflop_per_step": round(flops["total"] / 1e12, 3),
         "roofline": roofline,
