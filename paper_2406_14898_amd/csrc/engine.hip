@@ -207,6 +207,8 @@ struct Plan {
   int32_t* pos;
   float* cos_t;
   float* sin_t;
+  float* gemm_part;  // split-reduction scratch of the bf16 GEMMs (null for fp32)
+  size_t gemm_part_bytes;
 };
 
 void carve_plan(Carver& cv, const BatchInfo& bi, int rotary_dim, Plan* p) {
@@ -259,6 +261,8 @@ struct Work {
 void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, T = bi.T;
   carve_plan(cv, bi, st->d.rotary_dim, &w->plan);
+  w->plan.gemm_part_bytes = st->d.dtype == FL_BF16 ? gemm_part_bytes() : 0;
+  w->plan.gemm_part = w->plan.gemm_part_bytes ? (float*)cv.take(w->plan.gemm_part_bytes) : nullptr;
   carve_acts(cv, st, bi.T, &w->acts);
   w->ping[0] = cv.take(E * T * H);
   w->ping[1] = cv.take(E * T * H);
@@ -367,6 +371,13 @@ double gemm_bytes(double M, double N, double K, double E, double Eout) { return 
 // One block forward.  `out` may be NULL (recompute for the backward: the
 // final projection is not needed).
 // ---------------------------------------------------------------------------
+// Hands the GEMM the workspace's split-reduction scratch.
+GemmDesc& with_part(GemmDesc& g, const Plan& plan) {
+  g.part = plan.gemm_part;
+  g.part_bytes = plan.gemm_part_bytes;
+  return g;
+}
+
 int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_layer_params& p, const void* x,
                   const Acts& a, void* out, hipStream_t s) {
   const DType dt = (DType)st->d.dtype;
@@ -382,7 +393,7 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   g.rot_half = st->d.rotary_dim / 2; g.head_dim = st->hd; g.rot_cols = 2 * H;
   const bool fuse_rope = dt == DT_BF16 && st->d.rotary_dim > 0 && gemm_bf16_dma_ok(GEMM_NT, g);
   LAUNCH(FL_PROF_GEMM_NT_BIAS, gemm_flops(T, 3 * H, H), gemm_bytes(T, 3 * H, H, E, E),
-         gemm(dt, GEMM_NT, fuse_rope ? EPI_BIAS_ROPE : EPI_BIAS, g, s));
+         gemm(dt, GEMM_NT, fuse_rope ? EPI_BIAS_ROPE : EPI_BIAS, with_part(g, plan), s));
   if (!fuse_rope) {
     // q and k: the first rotary_dim features of every head, read and written
     LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
@@ -398,20 +409,20 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   g.A = a.o; g.B = p.w_o; g.C = a.h; g.M = T; g.N = H; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.R = x; g.ldr = H;
   LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E) + TH * E,
-         gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+         gemm(dt, GEMM_NT, EPI_BIAS_RES, with_part(g, plan), s));
   LAUNCH(FL_PROF_LAYERNORM_FWD, 0, 2 * TH * E + 8.0 * T,
          layernorm_fwd(dt, a.h, p.ln2_g, p.ln2_b, a.w, a.mean2, a.rstd2, T, H, st->d.ln_eps, s));
   g = GemmDesc();
   g.A = a.w; g.B = p.w_1; g.C = a.z; g.C2 = a.g; g.M = T; g.N = F; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = F; g.ldc2 = F; g.bias = p.b_1;
   LAUNCH(FL_PROF_GEMM_NT_BIAS_GELU, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
-         gemm(dt, GEMM_NT, EPI_BIAS_GELU, g, s));
+         gemm(dt, GEMM_NT, EPI_BIAS_GELU, with_part(g, plan), s));
   if (out) {
     g = GemmDesc();
     g.A = a.g; g.B = p.w_2; g.C = out; g.M = T; g.N = H; g.K = F;
     g.lda = F; g.ldb = F; g.ldc = H; g.bias = p.b_2; g.R = a.h; g.ldr = H;
     LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E) + TH * E,
-           gemm(dt, GEMM_NT, EPI_BIAS_RES, g, s));
+           gemm(dt, GEMM_NT, EPI_BIAS_RES, with_part(g, plan), s));
   }
   return FL_OK;
 }
@@ -452,20 +463,20 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   if ((rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
   GemmDesc g;
   g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
   g = GemmDesc();
   g.A = dy; g.B = p.w_2; g.C = w.dz; g.M = T; g.N = F; g.K = H; g.lda = H; g.ldb = F; g.ldc = F;
   g.Z = a.z; g.ldz = F;
   LAUNCH(FL_PROF_GEMM_NN_GELU_BWD, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
-         gemm(dt, GEMM_NN, EPI_GELU_BWD, g, s));
+         gemm(dt, GEMM_NN, EPI_GELU_BWD, with_part(g, plan), s));
   // z = w W_1^T + b_1
   if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
   g = GemmDesc();
   g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
   g = GemmDesc();
   g.A = w.dz; g.B = p.w_1; g.C = w.tmp; g.M = T; g.N = H; g.K = F; g.lda = F; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E), gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E), gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
   // w = LN2(h); h also feeds y directly
   if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, gr.ln2_g, gr.ln2_b, T, H, w, s)))
     return rc;
@@ -473,10 +484,10 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   if ((rc = colsum_into(st, dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
   g = GemmDesc();
   g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
   g = GemmDesc();
   g.A = w.dh; g.B = p.w_o; g.C = w.tmp; g.M = T; g.N = H; g.K = H; g.lda = H; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E), gemm(dt, GEMM_NN, EPI_STORE, g, s));
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E), gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
   // attention (dq, dk, dv with the inverse rotation applied)
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
@@ -491,11 +502,11 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   g = GemmDesc();
   g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
   LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(3 * H, H, T), gemm_bytes(3 * H, H, T, E, 8),
-         gemm(dt, GEMM_TN, EPI_ACC_F32, g, s));
+         gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
   g = GemmDesc();
   g.A = w.dqkv; g.B = p.w_qkv; g.C = w.tmp; g.M = T; g.N = H; g.K = 3 * H; g.lda = 3 * H; g.ldb = H; g.ldc = H;
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, 3 * H), gemm_bytes(T, H, 3 * H, E, E),
-         gemm(dt, GEMM_NN, EPI_STORE, g, s));
+         gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
   // u = LN1(x); x also feeds h directly
   return ln_backward(st, dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, w.dh, dx, gr.ln1_g, gr.ln1_b, T, H, w, s);
 }

@@ -25,6 +25,8 @@
 //     second half's fragments are already in registers when the barrier
 //     releases the slot, so the next stage's loads and fragment reads overlap
 //     matrix-core work.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -55,6 +57,12 @@ struct G2Args {
   const float* cos_t;
   const float* sin_t;
   int rot_half, head_dim, rot_cols;
+  // Split reduction for the last, partial round of tiles: the final `tail`
+  // tiles are cut into `splits` reduction slices whose fp32 partial
+  // accumulators go to `part`; a second launch (fixup = 1) sums them in a
+  // fixed order and runs the epilogue.
+  float* part;
+  int tail, splits, fixup;
 };
 
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
@@ -154,9 +162,25 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
 
   const int tiles_m = (p.M + kBM - 1) / kBM, tiles_n = p.N / kBN;
   const int ntiles = tiles_m * tiles_n;
-  // Persistent: one workgroup per CU walks the tiles; a tile's epilogue
-  // stores drain while the next tile's first stages load.
-  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  const int nk = (p.K + kBK - 1) / kBK;
+  const int full = ntiles - p.tail;
+  const int nwork = p.fixup ? p.tail : full + p.tail * p.splits;
+  // Persistent: one workgroup per CU walks the work items (whole tiles, then
+  // the reduction slices of the tail tiles); a tile's epilogue stores drain
+  // while the next item's first stages load.
+  for (int wi = blockIdx.x; wi < nwork; wi += gridDim.x) {
+  int t, kt0 = 0, kt1 = nk, slice = -1;
+  if (p.fixup) {
+    t = full + wi;
+  } else if (wi < full) {
+    t = wi;
+  } else {
+    slice = wi - full;
+    t = full + slice / p.splits;
+    const int per = (nk + p.splits - 1) / p.splits;
+    kt0 = min(nk, (slice % p.splits) * per);
+    kt1 = min(nk, kt0 + per);
+  }
   // Per-lane values are rederived in every tile (the opaque copy keeps the
   // compiler from hoisting them out of the tile loop, where they would stay
   // live across the whole body and spill).
@@ -220,7 +244,6 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
 #pragma unroll
     for (int j = 0; j < kWTM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = (p.K + kBK - 1) / kBK;
   auto rd_a = [&](int slot, int c, int j) {
     const bf16* as = smem[slot][0];
     return AK ? frag_k(as, abase, c, j) : frag_m(as, abase, c, j);
@@ -249,18 +272,29 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     asm volatile("" ::: "memory");
   };
 
+  if (p.fixup) {
+    // sum the tile's reduction slices in slice order (deterministic)
+    const float* src = p.part + (long)(t - full) * p.splits * (kWTN * kWTM * kThr * 4);
+    for (int c = 0; c < p.splits; ++c) {
+#pragma unroll
+      for (int i = 0; i < kWTN; ++i)
+#pragma unroll
+        for (int j = 0; j < kWTM; ++j)
+          acc[i][j] += __builtin_bit_cast(f32x4, ld16(src + ((long)(c * kWTN * kWTM + i * kWTM + j) * kThr + tid) * 4));
+    }
+  } else if (kt1 > kt0) {
   // Stage kt lives in slot kt % 2.  Prologue: stages 0 and 1 in flight; once
   // stage 0 is visible, read its first half.
-  issue(0);
-  if (nk > 1) {
-    issue(1);
+  issue(kt0);
+  if (kt1 - kt0 > 1) {
+    issue(kt0 + 1);
     asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // 8 DMA instructions per stage per wave
   } else {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
   barrier();
   bf16x8 fa0[kWTM], fb0[kWTN], fa1[kWTM], fb1[kWTN];
-  load_frags(0, 0, fa0, fb0);
+  load_frags(kt0 & 1, 0, fa0, fb0);
   // Main loop, one stage per iteration, in two halves of 32 reductions.  The
   // issue order is fixed by scheduling barriers: each group of four matrix
   // instructions (one A fragment against the four B fragments) is preceded
@@ -269,7 +303,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   // memory pipes are fed steadily instead of in bursts that stall issue.
   // The last stage is peeled so that every path through the body passes the
   // barrier (the compiler then never waits for next-half reads early).
-  for (int kt = 0; kt < nk - 1; ++kt) {
+  for (int kt = kt0; kt < kt1 - 1; ++kt) {
     const int slot = kt & 1;
 #pragma unroll
     for (int j = 0; j < kWTM; ++j) {
@@ -285,7 +319,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     barrier();
-    const bool more = kt + 2 < nk;
+    const bool more = kt + 2 < kt1;
 #pragma unroll
     for (int j = 0; j < kWTM; ++j) {
       if (more) dma_one(kt + 2, j);
@@ -297,9 +331,23 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  load_frags((nk - 1) & 1, 1, fa1, fb1);
+  load_frags((kt1 - 1) & 1, 1, fa1, fb1);
   mma_all(fa0, fb0);
   mma_all(fa1, fb1);
+  }
+  if (slice >= 0) {
+    // a reduction slice of a tail tile: store the partial accumulators
+    // ([slice][i][j][thread][4], coalesced) and move on
+    float* dst = p.part + (long)slice * (kWTN * kWTM * kThr * 4);
+#pragma unroll
+    for (int i = 0; i < kWTN; ++i)
+#pragma unroll
+      for (int j = 0; j < kWTM; ++j)
+        st16(dst + ((long)(i * kWTM + j) * kThr + tid) * 4, __builtin_bit_cast(u32x4, acc[i][j]));
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();  // every wave is done with the operand tiles before the next item's loads
+    continue;
+  }
 
   // Epilogue, staged through LDS so that every global access is a full row
   // segment: the accumulators of one 128-row half of the tile go to LDS as
@@ -424,6 +472,9 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   }
 }
 
+// fp32 partial accumulators of one 256 x 256 tile slice
+constexpr size_t kSliceBytes = (size_t)kBM * kBN * 4;
+
 // Compute units of the current device (one persistent workgroup each; a
 // multiple of the 8 XCDs on MI355X, which the tile order relies on).
 int num_cus() {
@@ -447,14 +498,35 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
   a.pos = d.pos; a.cos_t = d.cos_t; a.sin_t = d.sin_t;
   a.rot_half = d.rot_half; a.head_dim = d.head_dim; a.rot_cols = d.rot_cols;
+  a.part = d.part; a.tail = 0; a.splits = 1; a.fixup = 0;
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
   const int cus = num_cus();
-  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(tiles < cus ? tiles : cus), dim3(kThr), 0, st, a);
+  // A last round that would leave three quarters of the CUs idle is cut
+  // into reduction slices (at least 4 stages each) spread over all CUs.
+  const int rem = tiles % cus, nk = (d.K + kBK - 1) / kBK;
+  if (d.part && rem > 0 && 4 * rem <= cus && nk >= 8) {
+    int splits = std::min(std::min(cus / rem, nk / 4), 16);
+    while (splits > 1 && (size_t)rem * splits * kSliceBytes > d.part_bytes) --splits;
+    if (splits > 1) {
+      a.tail = rem;
+      a.splits = splits;
+    }
+  }
+  const int items = tiles - a.tail + a.tail * a.splits;
+  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(items < cus ? items : cus), dim3(kThr), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.tail == 0) return e;
+  a.fixup = 1;
+  hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKc, EPI>), dim3(a.tail), dim3(kThr), 0, st, a);
   return hipGetLastError();
 }
 
 }  // namespace
+
+// One slice per compute unit of an MI355X (256); launches split only as far
+// as the scratch they are given allows.
+size_t gemm_part_bytes() { return (size_t)256 * kSliceBytes; }
 
 // Shapes the DMA kernel takes: N a multiple of 256, K-contiguous operands
 // with K a multiple of 64, and every buffer offset below 2^31 bytes.

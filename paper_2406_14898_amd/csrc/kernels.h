@@ -30,7 +30,14 @@ struct GemmDesc {
   const float* cos_t = nullptr;
   const float* sin_t = nullptr;
   int rot_half = 0, head_dim = 0, rot_cols = 0;
+  // Optional fp32 scratch for splitting the reduction of a partial last
+  // round of tiles (bf16 LDS-DMA kernel); null = never split.
+  float* part = nullptr;
+  size_t part_bytes = 0;
 };
+// Scratch that lets gemm() split the partial last round of tiles (one
+// 256 KB slice per compute unit).
+size_t gemm_part_bytes();
 enum GemmEpi : int {
   EPI_STORE = 0,      // C = acc
   EPI_BIAS = 1,       // C = acc + bias

@@ -82,6 +82,60 @@ def test_gemm_tn_accumulates(dt):
     assert rel_l2(host(C), ref) < (1e-5 if dt == "f32" else 5e-3)
 
 
+SPLIT_CASES = [  # (layout, epi, M, N, K): 2-4 tiles, K of 16+ stages, so the launch splits the reduction
+    (F.FL_GEMM_NT, F.FL_EPI_BIAS_RES, 300, 512, 1024),
+    (F.FL_GEMM_NT, F.FL_EPI_BIAS_GELU, 200, 256, 1536),
+    (F.FL_GEMM_NN, F.FL_EPI_STORE, 420, 256, 1024),
+    (F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, 300, 512, 1024),
+    (F.FL_GEMM_TN, F.FL_EPI_ACC_F32, 272, 512, 1100),
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: f"L{c[0]}E{c[1]}M{c[2]}N{c[3]}K{c[4]}")
+def test_gemm_split_reduction(case):
+    """bf16: the partial last round of tiles split into reduction slices (fp32
+    partials in scratch, fixed-order fixup) against fp64 and the unsplit run."""
+    lay, epi, M, N, K = case
+    rng = 40 + epi
+    if lay == F.FL_GEMM_NT:
+        A, B, lda, ldb = rnd((M, K), rng), rnd((N, K), rng + 1, 0.05), K, K
+        ref = A.astype(np.float64) @ B.astype(np.float64).T
+    elif lay == F.FL_GEMM_NN:
+        A, B, lda, ldb = rnd((M, K), rng), rnd((K, N), rng + 1, 0.05), K, N
+        ref = A.astype(np.float64) @ B.astype(np.float64)
+    else:
+        A, B, lda, ldb = rnd((K, M), rng), rnd((K, N), rng + 1), M, N
+        ref = A.astype(np.float64).T @ B.astype(np.float64)
+    bias, R, Z = rnd((N,), rng + 2), rnd((M, N), rng + 3), rnd((M, N), rng + 4)
+    C0 = rnd((M, N), rng + 5, dt="f32")
+    if epi in (F.FL_EPI_BIAS_RES, F.FL_EPI_BIAS_GELU):
+        ref = ref + bias
+    if epi == F.FL_EPI_BIAS_RES:
+        ref = ref + R
+    if epi == F.FL_EPI_GELU_BWD:
+        ref = ref * oracle.gelu_grad(Z.astype(np.float64))
+    if epi == F.FL_EPI_ACC_F32:
+        ref = ref + C0
+    outs = []
+    for part in (None, torch.zeros(64 << 20 >> 2, dtype=torch.float32, device="cuda")):
+        if epi == F.FL_EPI_ACC_F32:
+            C = torch.from_numpy(C0.copy()).cuda()
+        else:
+            C = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+        C2 = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+        F.fl_test_gemm(F.FL_BF16, lay, epi, dev(A, "bf16"), dev(B, "bf16"), C, M, N, K, lda, ldb, N,
+                       bias=dev(bias, "bf16"), R=dev(R, "bf16"), ldr=N, C2=C2, ldc2=N, Z=dev(Z, "bf16"), ldz=N,
+                       part=part)
+        sync()
+        outs.append((host(C), host(C2)))
+        tol = 5e-3 if epi == F.FL_EPI_ACC_F32 else TOL["bf16"] / 4
+        assert rel_l2(outs[-1][0], ref) < tol
+        if epi == F.FL_EPI_BIAS_GELU:
+            assert rel_l2(outs[-1][1], _gelu(ref)) < TOL["bf16"] / 4
+    # the split run differs from the unsplit one only by fp32 summation order
+    assert rel_l2(outs[1][0], outs[0][0]) < 1e-2
+
+
 def test_gemm_rejects_bad_shapes():
     A = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(F.FlglmError):
