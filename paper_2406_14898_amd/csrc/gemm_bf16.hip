@@ -504,8 +504,10 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   const int cus = num_cus();
   // A last round that would leave three quarters of the CUs idle is cut
   // into reduction slices (at least 4 stages each) spread over all CUs.
+  // Measured on MI355X: worth it from 128 stages (K = 8192) on; below that
+  // the partial stores and the fixup launch cost more than the idle CUs.
   const int rem = tiles % cus, nk = (d.K + kBK - 1) / kBK;
-  if (d.part && rem > 0 && 4 * rem <= cus && nk >= 8) {
+  if (d.part && rem > 0 && 4 * rem <= cus && nk >= 128) {
     int splits = std::min(std::min(cus / rem, nk / 4), 16);
     while (splits > 1 && (size_t)rem * splits * kSliceBytes > d.part_bytes) --splits;
     if (splits > 1) {

@@ -82,12 +82,12 @@ def test_gemm_tn_accumulates(dt):
     assert rel_l2(host(C), ref) < (1e-5 if dt == "f32" else 5e-3)
 
 
-SPLIT_CASES = [  # (layout, epi, M, N, K): 2-4 tiles, K of 16+ stages, so the launch splits the reduction
-    (F.FL_GEMM_NT, F.FL_EPI_BIAS_RES, 300, 512, 1024),
-    (F.FL_GEMM_NT, F.FL_EPI_BIAS_GELU, 200, 256, 1536),
-    (F.FL_GEMM_NN, F.FL_EPI_STORE, 420, 256, 1024),
-    (F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, 300, 512, 1024),
-    (F.FL_GEMM_TN, F.FL_EPI_ACC_F32, 272, 512, 1100),
+SPLIT_CASES = [  # (layout, epi, M, N, K): 1-4 tiles, K of 128+ stages, so the launch splits the reduction
+    (F.FL_GEMM_NT, F.FL_EPI_BIAS_RES, 300, 512, 8192),
+    (F.FL_GEMM_NT, F.FL_EPI_BIAS_GELU, 200, 256, 8256),
+    (F.FL_GEMM_NN, F.FL_EPI_STORE, 420, 256, 8192),
+    (F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, 300, 512, 8192),
+    (F.FL_GEMM_TN, F.FL_EPI_ACC_F32, 272, 512, 8300),
 ]
 
 
