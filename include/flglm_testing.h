@@ -52,14 +52,6 @@ int fl_test_layernorm_bwd(int dtype, const void* dy, const void* x, const float*
  * partial: device fp32 scratch of at least ceil(T/256) * N * 2 floats. */
 int fl_test_colsum(int dtype, int mode, const void* X, const void* Y, const float* mean, const float* rstd, int T,
                    int N, float* out, float* out2, float* partial, void* stream);
-/* bf16 only: qkv [T, 3H] = u [T, K] w^T + bias with the rotary encoding of
- * the q and k heads fused into the GEMM epilogue (rows rotate by their
- * position inside their sequence, from device cu_seqlens [S+1]); w is
- * [3H, K]; scratch as for fl_test_rope.  3H % 256 == 0, K % 64 == 0, head
- * dim 64 or 128, rotary_dim a multiple of 32. */
-int fl_test_gemm_qkv_rope(const void* u, const void* w, const void* bias, void* qkv, const int32_t* cu_dev, int S,
-                          int T, int max_seqlen, int H, int num_heads, int K, int rotary_dim, float base, int32_t* pos,
-                          float* cos_t, float* sin_t, void* stream);
 /* Rotary encoding in place on the q and k parts of qkv [T, 3H]; positions
  * from device cu_seqlens [S+1]; table scratch cos/sin: device fp32
  * [max_seqlen * rotary_dim / 2] each; pos scratch: device int32 [T]. */

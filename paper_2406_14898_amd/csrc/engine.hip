@@ -388,17 +388,14 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   GemmDesc g;
   g.A = a.u; g.B = p.w_qkv; g.C = a.qkv; g.M = T; g.N = 3 * H; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = 3 * H; g.bias = p.b_qkv;
-  // rotary on q and k fused into the QKV epilogue where the bf16 kernel runs
-  g.pos = plan.pos; g.cos_t = plan.cos_t; g.sin_t = plan.sin_t;
-  g.rot_half = st->d.rotary_dim / 2; g.head_dim = st->hd; g.rot_cols = 2 * H;
-  const bool fuse_rope = dt == DT_BF16 && st->d.rotary_dim > 0 && gemm_bf16_dma_ok(GEMM_NT, g);
   LAUNCH(FL_PROF_GEMM_NT_BIAS, gemm_flops(T, 3 * H, H), gemm_bytes(T, 3 * H, H, E, E),
-         gemm(dt, GEMM_NT, fuse_rope ? EPI_BIAS_ROPE : EPI_BIAS, with_part(g, plan), s));
-  if (!fuse_rope) {
-    // q and k: the first rotary_dim features of every head, read and written
-    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
-           rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
-  }
+         gemm(dt, GEMM_NT, EPI_BIAS, with_part(g, plan), s));
+  // q and k: the first rotary_dim features of every head, read and written.
+  // A separate pass on purpose: folded into the QKV epilogue (a lane-pair
+  // exchange plus table loads per row) it measured 0.5 ms slower per call
+  // at T = 41447 than this 0.14 ms kernel, the epilogue being latency-bound.
+  LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
+         rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
   ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;

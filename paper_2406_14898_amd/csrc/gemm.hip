@@ -315,7 +315,6 @@ static hipError_t dispatch_layout(int epi, const GemmArgs& a, hipStream_t st) {
 
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st) {
   if (dt == DT_BF16 && gemm_bf16_dma_ok(layout, d)) return gemm_bf16_dma(layout, epi, d, st);
-  if (epi == EPI_BIAS_ROPE) return hipErrorInvalidValue;  // fused rotary: LDS-DMA kernel only
   GemmArgs a;
   a.A = d.A; a.B = d.B; a.C = d.C;
   a.M = d.M; a.N = d.N; a.K = d.K;

@@ -53,10 +53,6 @@ struct G2Args {
   long ldc2;
   const bf16* Z;
   long ldz;
-  const int32_t* pos;
-  const float* cos_t;
-  const float* sin_t;
-  int rot_half, head_dim, rot_cols;
   // Split reduction for the last, partial round of tiles: the final `tail`
   // tiles are cut into `splits` reduction slices whose fp32 partial
   // accumulators go to `part`; a second launch (fixup = 1) sums them in a
@@ -361,19 +357,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   barrier();  // every wave is done with the operand tiles
   const int n = n0 + 4 * lane;
   float bias[4] = {0.f, 0.f, 0.f, 0.f};
-  // Rotary (q and k columns): this lane's four columns sit at offset c of
-  // their head; pairs (c, c + r/2) for c < r/2 live in lanes r/8 apart.
-  bool rope = false, rope_first = false, rope_lane = false;
-  int rope_partner = lane, rope_i = 0;
-  if constexpr (EPI == EPI_BIAS_ROPE) {
-    const int c = (4 * lane) % p.head_dim, hf = p.rot_half;
-    rope = n0 < p.rot_cols;
-    rope_lane = c < 2 * hf;
-    rope_first = c < hf;
-    rope_partner = rope_first ? lane + hf / 4 : lane - hf / 4;
-    rope_i = rope_first ? c : c - hf;
-  }
-  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU || EPI == EPI_BIAS_ROPE) {
+  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
     Vec4<bf16> b;
     b.load(p.bias + n);
 #pragma unroll
@@ -434,24 +418,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[u].get(e));
           }
-          if constexpr (EPI == EPI_BIAS_ROPE) {
-            if (rope) {  // uniform per tile; every lane takes part in the exchange
-              float pv[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) pv[e] = __shfl(v[e], rope_partner, 64);
-              if (rope_lane) {
-                const long o = (long)p.pos[m] * p.rot_half + rope_i;
-                const u32x4 cr = ld16(p.cos_t + o), sr = ld16(p.sin_t + o);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  const float cs = __uint_as_float(cr[e]), sn = __uint_as_float(sr[e]);
-                  // (x1, x2) -> (x1 cos - x2 sin, x2 cos + x1 sin)
-                  v[e] = rope_first ? v[e] * cs - pv[e] * sn : v[e] * cs + pv[e] * sn;
-                }
-              }
-            }
-          }
-          Vec4<bf16> o;
+        Vec4<bf16> o;
           o.set(v);
           o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
           if constexpr (EPI == EPI_BIAS_GELU) {
@@ -496,8 +463,6 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.M = d.M; a.N = d.N; a.K = d.K; a.lda = d.lda; a.ldb = d.ldb; a.ldc = d.ldc;
   a.bias = (const bf16*)d.bias; a.R = (const bf16*)d.R; a.ldr = d.ldr;
   a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
-  a.pos = d.pos; a.cos_t = d.cos_t; a.sin_t = d.sin_t;
-  a.rot_half = d.rot_half; a.head_dim = d.head_dim; a.rot_cols = d.rot_cols;
   a.part = d.part; a.tail = 0; a.splits = 1; a.fixup = 0;
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
@@ -550,7 +515,6 @@ hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStrea
       switch (epi) {
         case EPI_STORE: return launch2<true, true, EPI_STORE>(d, st);
         case EPI_BIAS: return launch2<true, true, EPI_BIAS>(d, st);
-        case EPI_BIAS_ROPE: return launch2<true, true, EPI_BIAS_ROPE>(d, st);
         case EPI_BIAS_RES: return launch2<true, true, EPI_BIAS_RES>(d, st);
         case EPI_BIAS_GELU: return launch2<true, true, EPI_BIAS_GELU>(d, st);
       }

@@ -23,13 +23,6 @@ struct GemmDesc {
   long ldc2 = 0;
   const void* Z = nullptr;
   long ldz = 0;
-  // EPI_BIAS_ROPE: columns [0, rot_cols) hold heads of head_dim; the first
-  // 2 * rot_half of each head rotate by the row's position pos[m] with the
-  // cos / sin tables [max_pos][rot_half].
-  const int32_t* pos = nullptr;
-  const float* cos_t = nullptr;
-  const float* sin_t = nullptr;
-  int rot_half = 0, head_dim = 0, rot_cols = 0;
   // Optional fp32 scratch for splitting the reduction of a partial last
   // round of tiles (bf16 LDS-DMA kernel); null = never split.
   float* part = nullptr;
@@ -45,7 +38,6 @@ enum GemmEpi : int {
   EPI_BIAS_GELU = 3,  // C = z = acc + bias; C2 = gelu(z)
   EPI_GELU_BWD = 4,   // C = acc * gelu'(Z)
   EPI_ACC_F32 = 5,    // Cf += acc (fp32 output)
-  EPI_BIAS_ROPE = 6,  // C = rotate(acc + bias) (bf16 LDS-DMA kernel only)
 };
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
 // bf16 LDS-DMA kernel (gemm_bf16.hip), used by gemm() for the shapes it takes.

@@ -111,29 +111,6 @@ int fl_test_rope(int dtype, void* qkv, const int32_t* cu_dev, int S, int T, int 
   return herr(rope_qk((DType)dtype, qkv, 3L * H, pos, cos_t, sin_t, T, H, d, rotary_dim, s));
 }
 
-int fl_test_gemm_qkv_rope(const void* u, const void* w, const void* bias, void* qkv, const int32_t* cu_dev, int S,
-                          int T, int max_seqlen, int H, int num_heads, int K, int rotary_dim, float base, int32_t* pos,
-                          float* cos_t, float* sin_t, void* stream) {
-  if (!u || !w || !bias || !qkv || !cu_dev || !pos || !cos_t || !sin_t) return set_error(FL_ERR_NULL, "NULL argument");
-  if (!al16(u) || !al16(w) || !al16(bias) || !al16(qkv) || !al16(cos_t) || !al16(sin_t))
-    return set_error(FL_ERR_ALIGN, "operands must be 16-byte aligned");
-  if (num_heads <= 0 || H % num_heads) return set_error(FL_ERR_ARG, "bad heads");
-  const int d = H / num_heads;
-  if (d != 64 && d != 128) return set_error(FL_ERR_ARG, "head dim must be 64 or 128");
-  if (rotary_dim <= 0 || rotary_dim > d || rotary_dim % 32) return set_error(FL_ERR_ARG, "bad rotary_dim");
-  if (T <= 0 || K <= 0 || K % 64 || (3 * H) % 256) return set_error(FL_ERR_ARG, "bad T / K / H");
-  GemmDesc g;
-  g.A = u; g.B = w; g.C = qkv; g.M = T; g.N = 3 * H; g.K = K;
-  g.lda = K; g.ldb = K; g.ldc = 3L * H; g.bias = bias;
-  g.pos = pos; g.cos_t = cos_t; g.sin_t = sin_t; g.rot_half = rotary_dim / 2; g.head_dim = d; g.rot_cols = 2 * H;
-  if (!gemm_bf16_dma_ok(GEMM_NT, g)) return set_error(FL_ERR_ARG, "shape not taken by the fused kernel");
-  hipStream_t s = (hipStream_t)stream;
-  int rc = herr(seq_positions(cu_dev, S, pos, s));
-  if (rc) return rc;
-  if ((rc = herr(rope_table(cos_t, sin_t, max_seqlen, rotary_dim, base, s)))) return rc;
-  return herr(gemm(DT_BF16, GEMM_NT, EPI_BIAS_ROPE, g, s));
-}
-
 int fl_test_attention_fwd(int dtype, const void* qkv, void* o, float* lse, const int32_t* cu_dev,
                           const int32_t* prefix_dev, int T, int S, int max_seqlen, int H, int num_heads,
                           void* stream) {

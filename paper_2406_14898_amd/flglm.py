@@ -36,7 +36,7 @@ EXPORTS = (
     "fl_pack_clients", "fl_unpack_clients", "fl_last_error",
     "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_colsum",
-    "fl_test_rope", "fl_test_gemm_qkv_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
+    "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
 )
 
 
@@ -103,7 +103,6 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
         "fl_test_colsum": [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp],
         "fl_test_rope": [ctypes.c_int, vp, vp] + [ctypes.c_int] * 6 + [ctypes.c_float, vp, vp, vp, vp],
-        "fl_test_gemm_qkv_rope": [vp] * 5 + [ctypes.c_int] * 7 + [ctypes.c_float, vp, vp, vp, vp],
         "fl_test_attention_fwd": [ctypes.c_int, vp, vp, vp, vp, vp] + [ctypes.c_int] * 5 + [vp],
         "fl_test_attention_bwd": [ctypes.c_int] + [vp] * 11 + [ctypes.c_int] * 6 + [vp],
     }
@@ -308,13 +307,6 @@ def fl_test_layernorm_bwd(dtype, dy, x, mean, rstd, g, dres, dx, T, H, stream=No
 def fl_test_colsum(dtype, mode, X, Y, mean, rstd, T, N, out, out2, partial, stream=None) -> None:
     _check(load().fl_test_colsum(dtype, mode, _ptr(X), _ptr(Y), _ptr(mean), _ptr(rstd), T, N, _ptr(out), _ptr(out2),
                                  _ptr(partial), _stream(stream)))
-
-
-def fl_test_gemm_qkv_rope(u, w, bias, qkv, cu_dev, S, T, max_seqlen, H, num_heads, K, rotary_dim, base, pos, cos_t,
-                          sin_t, stream=None) -> None:
-    _check(load().fl_test_gemm_qkv_rope(_ptr(u), _ptr(w), _ptr(bias), _ptr(qkv), _ptr(cu_dev), S, T, max_seqlen, H,
-                                        num_heads, K, rotary_dim, base, _ptr(pos), _ptr(cos_t), _ptr(sin_t),
-                                        _stream(stream)))
 
 
 def fl_test_rope(dtype, qkv, cu_dev, S, T, max_seqlen, H, num_heads, rotary_dim, base, pos, cos_t, sin_t,

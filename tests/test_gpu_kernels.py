@@ -257,36 +257,6 @@ def _lse_ref(q, k, b):
     return out
 
 
-@pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
-@pytest.mark.parametrize("rdiv", [2, 1])
-def test_gemm_qkv_rope_fused(heads, rdiv):
-    """QKV projection with the rotary encoding fused into the bf16 GEMM
-    epilogue: (u w^T + b), then q and k heads rotated by in-sequence position
-    (oracle), v untouched.  335 rows: two 256-row tiles, ragged sequences."""
-    nh, d = heads
-    H, K, r = nh * d, 320, d // rdiv
-    b = BATCHES["ragged_causal"]
-    T = b.total_tokens
-    u, w, bias = rnd((T, K), 31), rnd((3 * H, K), 32, 0.1), rnd((3 * H,), 33)
-    ref = u.astype(np.float64) @ w.astype(np.float64).T + bias
-    pos = oracle.positions(b.cu_seqlens)
-    cos, sin = oracle.rope_tables(pos, r, 10000.0)
-    for part in (0, 1):
-        blk = ref[:, part * H:(part + 1) * H].reshape(T, nh, d)
-        ref[:, part * H:(part + 1) * H] = oracle.rope(blk, cos, sin, r).reshape(T, H)
-    qkv = torch.full((T, 3 * H), float("nan"), dtype=torch.bfloat16, device="cuda")
-    tpos = torch.empty(T, dtype=torch.int32, device="cuda")
-    ct = torch.empty(b.max_seqlen * r // 2, dtype=torch.float32, device="cuda")
-    st = torch.empty_like(ct)
-    F.fl_test_gemm_qkv_rope(dev(u, "bf16"), dev(w, "bf16"), dev(bias, "bf16"), qkv, dev_i32(b.cu_seqlens),
-                            b.num_seqs, T, b.max_seqlen, H, nh, K, r, 10000.0, tpos, ct, st)
-    sync()
-    got = host(qkv)
-    for part in range(3):
-        sl = slice(part * H, (part + 1) * H)
-        assert rel_l2(got[:, sl], ref[:, sl]) < TOL["bf16"] / 4, part
-
-
 @pytest.mark.parametrize("dt", DT)
 @pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
 @pytest.mark.parametrize("bname", list(BATCHES))
