@@ -198,43 +198,73 @@ def _scores_probs(qs: np.ndarray, ks: np.ndarray, allowed: np.ndarray, scale: fl
     return P
 
 
-def attention_forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, batch) -> np.ndarray:
-    """o = softmax_mask(q k^T / sqrt(d)) v for every sequence and head
-    (Appendix A gives the softmax(Q K^T / sqrt(d_h)) form).  q, k, v, o: [T, n_h, d]."""
+def _prefix_head(pk: Optional[np.ndarray], h: int, d: int, dtype) -> np.ndarray:
+    """Prefix rows of head h ([L_p, d]); an empty array when there is none."""
+    if pk is None:
+        return np.zeros((0, d), dtype)
+    return pk[:, h]
+
+
+def attention_forward(q: np.ndarray, k: np.ndarray, v: np.ndarray, batch,
+                      pk: Optional[np.ndarray] = None, pv: Optional[np.ndarray] = None) -> np.ndarray:
+    """o = softmax_mask(q k'^T / sqrt(d)) v' for every sequence and head
+    (Appendix A gives the softmax(Q K^T / sqrt(d_h)) form).  q, k, v, o:
+    [T, n_h, d].  With P-tuning v2 (Appendix A, P-tuning v2 section) the
+    block's prefix keys and values pk, pv [L_p, n_h, d] are spliced in front:
+    K' = [pk; k], V' = [pv; v], the prefix visible to every query of every
+    sequence; the sequence's own keys keep their causal / prefix-LM mask."""
     T, nh, d = q.shape
     scale = 1.0 / math.sqrt(d)
     o = np.zeros_like(q)
     cu = batch.cu_seqlens
     for s in range(len(cu) - 1):
         r0, r1 = int(cu[s]), int(cu[s + 1])
-        allowed = allowed_mask(r1 - r0, _seq_prefix(batch, s))
+        L = r1 - r0
         for h in range(nh):
-            P = _scores_probs(q[r0:r1, h], k[r0:r1, h], allowed, scale)
-            o[r0:r1, h] = P @ v[r0:r1, h]
+            pkh = _prefix_head(pk, h, d, q.dtype)
+            pvh = _prefix_head(pv, h, d, q.dtype)
+            allowed = np.concatenate([np.ones((L, len(pkh)), bool), allowed_mask(L, _seq_prefix(batch, s))], axis=1)
+            P = _scores_probs(q[r0:r1, h], np.concatenate([pkh, k[r0:r1, h]]), allowed, scale)
+            o[r0:r1, h] = P @ np.concatenate([pvh, v[r0:r1, h]])
     return o
 
 
-def attention_backward(q: np.ndarray, k: np.ndarray, v: np.ndarray, do: np.ndarray, batch):
+def attention_backward(q: np.ndarray, k: np.ndarray, v: np.ndarray, do: np.ndarray, batch,
+                       pk: Optional[np.ndarray] = None, pv: Optional[np.ndarray] = None):
     """Gradient of ``attention_forward`` given do; P is recomputed.
-        dV = P^T dO,  dP = dO V^T,  D_i = sum_j P_ij dP_ij,
-        dS = P (dP - D),  dQ = dS K / sqrt(d),  dK = dS^T Q / sqrt(d)."""
+        dV' = P^T dO,  dP = dO V'^T,  D_i = sum_j P_ij dP_ij,
+        dS = P (dP - D),  dQ = dS K' / sqrt(d),  dK' = dS^T Q / sqrt(d).
+    Returns (dq, dk, dv), plus (dpk, dpv) summed over all sequences when a
+    prefix is given."""
     T, nh, d = q.shape
     scale = 1.0 / math.sqrt(d)
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    Lp = 0 if pk is None else pk.shape[0]
+    dpk = np.zeros((Lp, nh, d), q.dtype)
+    dpv = np.zeros((Lp, nh, d), q.dtype)
     cu = batch.cu_seqlens
     for s in range(len(cu) - 1):
         r0, r1 = int(cu[s]), int(cu[s + 1])
-        allowed = allowed_mask(r1 - r0, _seq_prefix(batch, s))
+        L = r1 - r0
+        allowed = np.concatenate([np.ones((L, Lp), bool), allowed_mask(L, _seq_prefix(batch, s))], axis=1)
         for h in range(nh):
-            qs, ks, vs, dos = q[r0:r1, h], k[r0:r1, h], v[r0:r1, h], do[r0:r1, h]
-            P = _scores_probs(qs, ks, allowed, scale)
-            dv[r0:r1, h] = P.T @ dos
-            dP = dos @ vs.T
+            kk = np.concatenate([_prefix_head(pk, h, d, q.dtype), k[r0:r1, h]])
+            vv = np.concatenate([_prefix_head(pv, h, d, q.dtype), v[r0:r1, h]])
+            qs, dos = q[r0:r1, h], do[r0:r1, h]
+            P = _scores_probs(qs, kk, allowed, scale)
+            dvv = P.T @ dos
+            dP = dos @ vv.T
             D = (P * dP).sum(axis=1, keepdims=True)
             dS = P * (dP - D)
-            dq[r0:r1, h] = (dS @ ks) * scale
-            dk[r0:r1, h] = (dS.T @ qs) * scale
-    return dq, dk, dv
+            dq[r0:r1, h] = (dS @ kk) * scale
+            dkk = (dS.T @ qs) * scale
+            dk[r0:r1, h] = dkk[Lp:]
+            dv[r0:r1, h] = dvv[Lp:]
+            dpk[:, h] += dkk[:Lp]
+            dpv[:, h] += dvv[:Lp]
+    if pk is None:
+        return dq, dk, dv
+    return dq, dk, dv, dpk, dpv
 
 
 # ----------------------------------------------------------------------------
@@ -268,15 +298,30 @@ def block_forward(p: Dict[str, np.ndarray], x: np.ndarray, batch, shape, dtype=n
     v = qkv[:, 2 * H:3 * H].reshape(T, nh, d)
     qr = rope(q, cos, sin, shape.rotary_dim)
     kr = rope(k, cos, sin, shape.rotary_dim)
-    o = attention_forward(qr, kr, v, batch).reshape(T, H)
+    # P-tuning v2 prefix (Appendix A): learned keys / values [L_p, H] spliced
+    # in front of every sequence's own; they carry no position, so they are
+    # not rotated
+    pk, pv = _prefix_kv(p, nh, d)
+    o = attention_forward(qr, kr, v, batch, pk, pv).reshape(T, H)
     h = x + o @ p["w_o"].T + p["b_o"]
     w, xhat2, rstd2 = layer_norm(h, p["ln2_g"], p["ln2_b"], eps)
     z = w @ p["w_1"].T + p["b_1"]
     g = gelu(z)
     y = h + g @ p["w_2"].T + p["b_2"]
     cache = dict(x=x, u=u, xhat1=xhat1, rstd1=rstd1, qr=qr, kr=kr, v=v, o=o, h=h,
-                 w=w, xhat2=xhat2, rstd2=rstd2, z=z, g=g, cos=cos, sin=sin)
+                 w=w, xhat2=xhat2, rstd2=rstd2, z=z, g=g, cos=cos, sin=sin, pk=pk, pv=pv)
     return y, cache
+
+
+def _prefix_kv(p: Dict[str, np.ndarray], nh: int, d: int):
+    """The block's P-tuning v2 prefix as [L_p, n_h, d] arrays, or (None, None)."""
+    if "prefix_k" not in p:
+        return None, None
+    return p["prefix_k"].reshape(-1, nh, d), p["prefix_v"].reshape(-1, nh, d)
+
+
+def zero_prefix_grads(num_prefix: int, hidden: int, dtype=np.float64) -> Dict[str, np.ndarray]:
+    return {"prefix_k": np.zeros((num_prefix, hidden), dtype), "prefix_v": np.zeros((num_prefix, hidden), dtype)}
 
 
 def zero_grads(shape, dtype=np.float64) -> Dict[str, np.ndarray]:
@@ -290,14 +335,18 @@ def zero_grads(shape, dtype=np.float64) -> Dict[str, np.ndarray]:
 def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape,
                    grads: Dict[str, np.ndarray], dtype=np.float64) -> np.ndarray:
     """Backward of ``block_forward``: returns dx and adds every parameter
-    gradient into ``grads`` (sum over all tokens of all clients).  The server
-    returns dx to the client in split learning (Section 3.1)."""
+    gradient named in ``grads`` into it (sum over all tokens of all clients).
+    The server returns dx to the client in split learning (Section 3.1).
+    With P-tuning v2 the block weights are frozen and only the prefix is
+    trained (Section 3.1, Appendix A): pass grads holding just "prefix_k" and
+    "prefix_v" and no weight gradient is formed."""
     p = _cast(p, dtype)
     dy = np.asarray(dy, dtype=dtype)
     c = cache
     T, H = dy.shape
     nh = shape.num_heads
     d = H // nh
+    grads = _Sink(grads)
 
     # y = h + g W_2^T + b_2
     grads["w_2"] += dy.T @ c["g"]
@@ -317,7 +366,12 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     grads["w_o"] += dh.T @ c["o"]
     grads["b_o"] += dh.sum(axis=0)
     do = (dh @ p["w_o"]).reshape(T, nh, d)
-    dqr, dkr, dv = attention_backward(c["qr"], c["kr"], c["v"], do, batch)
+    if c["pk"] is None:
+        dqr, dkr, dv = attention_backward(c["qr"], c["kr"], c["v"], do, batch)
+    else:
+        dqr, dkr, dv, dpk, dpv = attention_backward(c["qr"], c["kr"], c["v"], do, batch, c["pk"], c["pv"])
+        grads["prefix_k"] += dpk.reshape(-1, H)
+        grads["prefix_v"] += dpv.reshape(-1, H)
     dq = rope(dqr, c["cos"], c["sin"], shape.rotary_dim, inverse=True)
     dk = rope(dkr, c["cos"], c["sin"], shape.rotary_dim, inverse=True)
     dqkv = np.concatenate([dq.reshape(T, H), dk.reshape(T, H), dv.reshape(T, H)], axis=1)
@@ -330,6 +384,26 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     grads["ln1_g"] += dg1
     grads["ln1_b"] += db1
     return dh + dx_ln
+
+
+class _Sink:
+    """grads[name] += value for the names the caller asked for; others are
+    dropped (frozen parameters)."""
+
+    def __init__(self, grads: Dict[str, np.ndarray]):
+        self.g = grads
+
+    def __getitem__(self, k):
+        return self.g[k] if k in self.g else _Discard()
+
+    def __setitem__(self, k, v):
+        if k in self.g:
+            self.g[k] = v
+
+
+class _Discard:
+    def __iadd__(self, other):
+        return self
 
 
 # ----------------------------------------------------------------------------

@@ -36,6 +36,9 @@ def _rotate(x: torch.Tensor, pos: torch.Tensor, r: int, base: float) -> torch.Te
 
 
 def block(p, x, cu_seqlens, prefix_len, shape):
+    """One block; with "prefix_k" / "prefix_v" in p ([L_p, H], not rotated)
+    the P-tuning v2 prefix is concatenated in front of every sequence's keys
+    and values and is visible to every query."""
     T, H = x.shape
     nh = shape.num_heads
     d = H // nh
@@ -51,8 +54,14 @@ def block(p, x, cu_seqlens, prefix_len, shape):
         ks = _rotate(k[r0:r1].reshape(L, nh, d), pos, shape.rotary_dim, shape.rope_base)
         vs = v[r0:r1].reshape(L, nh, d)
         pre = None if prefix_len is None else int(prefix_len[s])
+        mask = _mask(L, pre)
+        if "prefix_k" in p:
+            Lp = p["prefix_k"].shape[0]
+            ks = torch.cat([p["prefix_k"].reshape(Lp, nh, d), ks], dim=0)
+            vs = torch.cat([p["prefix_v"].reshape(Lp, nh, d), vs], dim=0)
+            mask = torch.cat([torch.ones(L, Lp, dtype=torch.bool), mask], dim=1)
         o = F.scaled_dot_product_attention(qs.transpose(0, 1), ks.transpose(0, 1), vs.transpose(0, 1),
-                                           attn_mask=_mask(L, pre))
+                                           attn_mask=mask)
         outs.append(o.transpose(0, 1).reshape(L, H))
     o = torch.cat(outs, dim=0)
     h = x + F.linear(o, p["w_o"], p["b_o"])
