@@ -70,7 +70,13 @@ extern "C" {
 
 /* Shape of the server-held stack; all blocks are identical.  Supported:
  * hidden % 256 == 0, hidden / num_heads in {64, 128}, ffn_hidden % 256 == 0,
- * rotary_dim % 32 == 0 and <= head dim, hidden <= 4096, ln_eps > 0. */
+ * rotary_dim % 32 == 0 and <= head dim, hidden <= 4096, ln_eps > 0.
+ *
+ * num_prefix > 0 selects P-tuning v2 (Section 3.1 and Appendix A, P-tuning
+ * v2): every block has num_prefix learned key and value rows ([L_p, H],
+ * head h at columns h*d, not rotated) spliced in front of each sequence's
+ * own keys and values, K' = [prefix_key; key], V' = [prefix_value; value],
+ * and visible to every query of every sequence.  bf16 only; at most 4096. */
 typedef struct fl_stack_desc {
   int32_t num_layers;   /* N server blocks (26 for ChatGLM-6B's server part) */
   int32_t hidden;       /* H */
@@ -80,6 +86,7 @@ typedef struct fl_stack_desc {
   float rope_base;      /* 10000 */
   float ln_eps;         /* 1e-5 */
   int32_t dtype;        /* FL_BF16 or FL_F32 */
+  int32_t num_prefix;   /* L_p, P-tuning v2 prefix length; 0 = no prefix */
 } fl_stack_desc;
 
 /* A packed batch of clients (host arrays).  Sequence s covers packed rows
@@ -101,17 +108,24 @@ typedef struct fl_batch_desc {
  * out-features-major (y = x W^T + b): w_qkv [3H, H] (rows [0,H) query,
  * [H,2H) key, [2H,3H) value; head h owns rows h*d .. h*d+d-1 of each),
  * b_qkv [3H], w_o [H, H], b_o [H], w_1 [F, H], b_1 [F], w_2 [H, F], b_2 [H],
- * ln1_g, ln1_b, ln2_g, ln2_b [H]. */
+ * ln1_g, ln1_b, ln2_g, ln2_b [H].  prefix_k, prefix_v [L_p, H]: the
+ * P-tuning v2 prefix (required when num_prefix > 0, ignored otherwise). */
 typedef struct fl_layer_params {
   const void *w_qkv, *b_qkv, *w_o, *b_o, *w_1, *b_1, *w_2, *b_2;
   const void *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  const void *prefix_k, *prefix_v;
 } fl_layer_params;
 
 /* One block's gradient accumulators (device fp32, same shapes as the
- * parameters).  The backward adds into them. */
+ * parameters).  The backward adds into them.  The twelve weight pointers
+ * are either all set (full fine-tuning) or all NULL: frozen weights, as in
+ * P-tuning v2, where no weight gradient is formed at all.  prefix_k and
+ * prefix_v are required when num_prefix > 0 (the sum over every sequence of
+ * every client), ignored otherwise. */
 typedef struct fl_layer_grads {
   float *w_qkv, *b_qkv, *w_o, *b_o, *w_1, *b_1, *w_2, *b_2;
   float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  float *prefix_k, *prefix_v;
 } fl_layer_grads;
 
 typedef struct fl_stack fl_stack;
@@ -184,7 +198,8 @@ int fl_unpack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* p
 #define FL_PROF_LAYERNORM_BWD 10
 #define FL_PROF_COLSUM 11           /* bias and LayerNorm parameter gradients */
 #define FL_PROF_ATTN_BWD 12
-#define FL_PROF_NUM_CLASSES 13
+#define FL_PROF_PREFIX_GRAD 13      /* P-tuning v2 prefix gradients: sum over sequences */
+#define FL_PROF_NUM_CLASSES 14
 int fl_stack_profile(fl_stack* stack, int enable);
 /* Totals for one class over the records since profiling was enabled:
  * launch count, summed event time (ms), algorithmic flops and bytes.

@@ -58,17 +58,22 @@ int fl_test_colsum(int dtype, int mode, const void* X, const void* Y, const floa
 int fl_test_rope(int dtype, void* qkv, const int32_t* cu_dev, int S, int T, int max_seqlen, int H, int num_heads,
                  int rotary_dim, float base, int32_t* pos, float* cos_t, float* sin_t, void* stream);
 /* Attention forward over packed sequences (device cu_seqlens [S+1], device
- * prefix [S] or NULL for causal): qkv [T, 3H] -> o [T, H], lse [T, n_h]. */
+ * prefix [S] or NULL for causal): qkv [T, 3H] -> o [T, H], lse [T, n_h].
+ * pk, pv [num_prefix, H] (bf16, device): P-tuning v2 prefix keys / values in
+ * front of every sequence's (num_prefix 0: none). */
 int fl_test_attention_fwd(int dtype, const void* qkv, void* o, float* lse, const int32_t* cu_dev,
                           const int32_t* prefix_dev, int T, int S, int max_seqlen, int H, int num_heads,
-                          void* stream);
+                          const void* pk, const void* pv, int num_prefix, void* stream);
 /* Attention backward: dqkv [T, 3H] from dout [T, H]; delta scratch [T, n_h];
  * rotary_dim 0 disables the inverse rotation, otherwise pos/cos/sin come
- * from fl_test_rope's scratch. */
+ * from fl_test_rope's scratch.  With a prefix, dprefix_part receives the
+ * per-sequence prefix gradients, fp32 [2][S][num_prefix][H] (keys, then
+ * values). */
 int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float* lse, const void* dout, void* dqkv,
                           float* delta, const int32_t* cu_dev, const int32_t* prefix_dev, const int32_t* pos,
                           const float* cos_t, const float* sin_t, int rotary_dim, int T, int S, int max_seqlen, int H,
-                          int num_heads, void* stream);
+                          int num_heads, const void* pk, const void* pv, int num_prefix, float* dprefix_part,
+                          void* stream);
 
 #ifdef __cplusplus
 }

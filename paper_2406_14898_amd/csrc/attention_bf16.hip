@@ -162,6 +162,21 @@ __host__ __forceinline__ dim3 wg_grid(int ntiles, int nh, int nseq) {
   return dim3((unsigned)(groups * ntiles));
 }
 
+// The block's P-tuning v2 prefix for head h: n rows in ntiles key tiles;
+// buffer resources over [n, hidden] bf16 keys / values starting at column
+// h * D (rows past n read as zero).
+struct PrefixKV {
+  int n, ntiles;
+  i32x4 rk, rv;
+  __device__ __forceinline__ PrefixKV(const AttnDesc& a, int h, int D) {
+    n = a.num_prefix;
+    ntiles = (n + kRows - 1) / kRows;
+    const uint32_t bytes = n > 0 ? (uint32_t)(((long)n * a.hidden - (long)h * D) * 2) : 0u;
+    rk = buf_rsrc(static_cast<const bf16*>(a.pk) + h * D, bytes);
+    rv = buf_rsrc(static_cast<const bf16*>(a.pv) + h * D, bytes);
+  }
+};
+
 // Key tile [j0, j0 + 64) against queries [qlo, qlo + nq): none visible / all
 // visible (keys inside the sequence, each at or before every query or in the
 // prefix).  Wave-uniform, so only diagonal and ragged tiles pay for masking.
@@ -196,12 +211,20 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
   const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
   const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  // key tiles 0 .. ntp-1: the prefix (row stride H), then the sequence's own
+  const PrefixKV px(a, h, D);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
-  const int nkt = (kv_end + kRows - 1) / kRows;
+  const int nkt = px.ntiles + (kv_end + kRows - 1) / kRows;
   const uint32_t lds_k = FL_LDS_ADDR(&Ks[0][0]), lds_v = FL_LDS_ADDR(&Vs[0][0]);
   auto issue = [&](int kt) {
-    dma_tile<D>(rk, ld, kt * kRows, lds_k + (kt & 1) * (kRows * D * 2), w, lane);
-    dma_tile<D>(rv, ld, kt * kRows, lds_v + (kt & 1) * (kRows * D * 2), w, lane);
+    const uint32_t sk = lds_k + (kt & 1) * (kRows * D * 2), sv = lds_v + (kt & 1) * (kRows * D * 2);
+    if (kt < px.ntiles) {
+      dma_tile<D>(px.rk, H, kt * kRows, sk, w, lane);
+      dma_tile<D>(px.rv, H, kt * kRows, sv, w, lane);
+    } else {
+      dma_tile<D>(rk, ld, (kt - px.ntiles) * kRows, sk, w, lane);
+      dma_tile<D>(rv, ld, (kt - px.ntiles) * kRows, sv, w, lane);
+    }
   };
   issue(0);
 
@@ -235,9 +258,10 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     bar();  // tile kt landed for every wave; the other slot is free
     if (kt + 1 < nkt) issue(kt + 1);
-    const int j0 = kt * kRows;
-    if (tile_dark(j0, qlo, 32, si.P)) return;
-    const bool full = tile_full(j0, qlo, si.L, si.P);
+    const bool pre = kt < px.ntiles;
+    const int j0 = (pre ? kt : kt - px.ntiles) * kRows;
+    if (!pre && tile_dark(j0, qlo, 32, si.P)) return;
+    const bool full = pre ? j0 + kRows <= px.n : tile_full(j0, qlo, si.L, si.P);
     const bf16* ks = Ks[SL];
     const bf16* vs = Vs[SL];
     f32x4 st[QS][4];
@@ -263,7 +287,9 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
         for (int at = 0; at < 4; ++at)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            st[qs][at][i] = vis(qi, j0 + 16 * at + 4 * fg + i, si.L, si.P) ? st[qs][at][i] : -INFINITY;
+            st[qs][at][i] = (pre ? j0 + 16 * at + 4 * fg + i < px.n : vis(qi, j0 + 16 * at + 4 * fg + i, si.L, si.P))
+                                ? st[qs][at][i]
+                                : -INFINITY;
       }
       float mx = st[qs][0][0];
 #pragma unroll
@@ -357,12 +383,19 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
   const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
   const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
   const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  const PrefixKV px(a, h, D);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
-  const int nkt = (kv_end + kRows - 1) / kRows;
+  const int nkt = px.ntiles + (kv_end + kRows - 1) / kRows;
   const uint32_t lds_k = FL_LDS_ADDR(&Ks[0][0]), lds_v = FL_LDS_ADDR(&Vs[0][0]);
   auto issue = [&](int kt) {
-    dma_tile<D>(rk, ld, kt * kRows, lds_k + (kt & 1) * (kRows * D * 2), w, lane);
-    dma_tile<D>(rv, ld, kt * kRows, lds_v + (kt & 1) * (kRows * D * 2), w, lane);
+    const uint32_t sk = lds_k + (kt & 1) * (kRows * D * 2), sv = lds_v + (kt & 1) * (kRows * D * 2);
+    if (kt < px.ntiles) {
+      dma_tile<D>(px.rk, H, kt * kRows, sk, w, lane);
+      dma_tile<D>(px.rv, H, kt * kRows, sv, w, lane);
+    } else {
+      dma_tile<D>(rk, ld, (kt - px.ntiles) * kRows, sk, w, lane);
+      dma_tile<D>(rv, ld, (kt - px.ntiles) * kRows, sv, w, lane);
+    }
   };
   issue(0);
 
@@ -400,9 +433,10 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     bar();
     if (kt + 1 < nkt) issue(kt + 1);
-    const int j0 = kt * kRows;
-    if (tile_dark(j0, qlo, 32, si.P)) return;
-    const bool full = tile_full(j0, qlo, si.L, si.P);
+    const bool pre = kt < px.ntiles;
+    const int j0 = (pre ? kt : kt - px.ntiles) * kRows;
+    if (!pre && tile_dark(j0, qlo, 32, si.P)) return;
+    const bool full = pre ? j0 + kRows <= px.n : tile_full(j0, qlo, si.L, si.P);
     const bf16* ks = Ks[SL];
     const bf16* vs = Vs[SL];
     // keys in two halves of 32 (reduction half c2 of the dq product), which
@@ -437,7 +471,8 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             float pr = ex2(fmaf(st[qs][u][i], sl2, -lse2[qs]));
-            pr = (full | vis(qi, j0 + 16 * (2 * c2 + u) + 4 * fg + i, si.L, si.P)) ? pr : 0.f;
+            const int j = j0 + 16 * (2 * c2 + u) + 4 * fg + i;
+            pr = (full | (pre ? j < px.n : vis(qi, j, si.L, si.P))) ? pr : 0.f;
             st[qs][u][i] = pr * (dp[qs][u][i] - dlt[qs]);
           }
         df[qs] = pack_p(st[qs][0], st[qs][1]);
@@ -489,11 +524,17 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   __shared__ __attribute__((aligned(256))) float Ls[2][kRows];
   __shared__ __attribute__((aligned(256))) float Ds[2][kRows];
 
-  const WgCoord wc = wg_coord((a.max_seqlen + BK - 1) / BK, a.num_heads);
+  // Key tiles in work order u = 0, 1, ...: the prefix tiles (every query of
+  // the sequence sees them), then the sequence's own from row 0 (the tile at
+  // row k0 meets the queries from k0 on), i.e. longest-running first.
+  const int ntp = (a.num_prefix + BK - 1) / BK, nts = (a.max_seqlen + BK - 1) / BK;
+  const WgCoord wc = wg_coord(ntp + nts, a.num_heads);
   if (wc.s >= a.num_seqs) return;
-  const int s = wc.s, h = wc.h, k0 = wc.tile * BK;
+  const int u = ntp + nts - 1 - wc.tile;
+  const bool pre = u < ntp;
+  const int s = wc.s, h = wc.h, k0 = (pre ? u : u - ntp) * BK;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
-  if (k0 >= si.L) return;
+  if (!pre && k0 >= si.L) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
@@ -508,7 +549,7 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   const auto ro = buf_rsrc(dout + (long)si.r0 * a.ld_dout + h * D, (uint32_t)((long)si.L * a.ld_dout * 2));
   const auto rl = buf_rsrc(a.lse + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
   const auto rd = buf_rsrc(a.delta + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
-  const int qstart = ((k0 < si.P) ? 0 : k0) / kRows;
+  const int qstart = (pre || k0 < si.P) ? 0 : k0 / kRows;
   const int nqt = (si.L + kRows - 1) / kRows;
   const uint32_t lds_q = FL_LDS_ADDR(&Qs[0][0]), lds_o = FL_LDS_ADDR(&Os[0][0]);
   const uint32_t lds_l = FL_LDS_ADDR(&Ls[0][0]), lds_d = FL_LDS_ADDR(&Ds[0][0]);
@@ -524,17 +565,19 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   };
   issue(qstart);
 
-  const int klo = k0 + 16 * w;  // this wave's keys: klo + fr
+  const int klo = k0 + 16 * w;  // this wave's keys: klo + fr (prefix rows for a prefix tile)
   const int kj = klo + fr;
-  const bool kvalid = kj < si.L;
+  const bool kvalid = kj < (pre ? a.num_prefix : si.L);
+  // key / value rows of this lane: the prefix buffers (row stride H) or qkv
+  const bf16* krow = pre ? static_cast<const bf16*>(a.pk) + (long)kj * H + h * D
+                         : qkv + (long)(si.r0 + kj) * ld + H + h * D;
+  const bf16* vrow = pre ? static_cast<const bf16*>(a.pv) + (long)kj * H + h * D
+                         : qkv + (long)(si.r0 + kj) * ld + 2 * H + h * D;
   bf16x8 kf[NC], vf[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    kf[c] = kvalid ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + kj) * ld + H + h * D + 32 * c + 8 * fg))
-                   : bf16x8{};
-    vf[c] = kvalid
-                ? __builtin_bit_cast(bf16x8, ld16(qkv + (long)(si.r0 + kj) * ld + 2 * H + h * D + 32 * c + 8 * fg))
-                : bf16x8{};
+    kf[c] = kvalid ? __builtin_bit_cast(bf16x8, ld16(krow + 32 * c + 8 * fg)) : bf16x8{};
+    vf[c] = kvalid ? __builtin_bit_cast(bf16x8, ld16(vrow + 32 * c + 8 * fg)) : bf16x8{};
   }
 #pragma unroll
   for (int c = 0; c < NC; ++c) { settle(kf[c]); settle(vf[c]); }
@@ -548,9 +591,10 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
     bar();
     if (qt + 1 < nqt) issue(qt + 1);
     const int qb = qt * kRows;
-    // queries [qb, qb + 64) against keys [klo, klo + 16)
-    if (qb + kRows - 1 < klo && klo >= si.P) return;
-    const bool full = qb >= klo + 15 || klo + 15 < si.P;
+    // queries [qb, qb + 64) against keys [klo, klo + 16); prefix keys are
+    // visible to all
+    if (!pre && qb + kRows - 1 < klo && klo >= si.P) return;
+    const bool full = pre || qb >= klo + 15 || klo + 15 < si.P;
     const bf16* qs_ = Qs[SL];
     const bf16* os_ = Os[SL];
     const float* ls_ = Ls[SL];
@@ -630,6 +674,17 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   const float sc = 1.f / sqrtf((float)D);
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) dk[dt] *= sc;
+  if (pre) {
+    // this sequence's share of the prefix gradients, fp32, unrotated
+    float* pk_out = a.dprefix_part + ((long)s * a.num_prefix + kj) * H + h * D;
+    float* pv_out = pk_out + (long)a.num_seqs * a.num_prefix * H;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      st16(pk_out + 16 * dt + 4 * fg, __builtin_bit_cast(u32x4, dk[dt]));
+      st16(pv_out + 16 * dt + 4 * fg, __builtin_bit_cast(u32x4, dv[dt]));
+    }
+    return;
+  }
   rope_back<D>(dk, kj, a.rotary_dim, fg, a.cos_t, a.sin_t);
   bf16* row = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + kj) * a.ld_dqkv + h * D;
 #pragma unroll
@@ -655,7 +710,7 @@ template <int D>
 hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
   hipError_t e = attn_delta(DT_BF16, a, st);
   if (e != hipSuccess) return e;
-  const dim3 gkv = wg_grid((a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
+  const dim3 gkv = wg_grid((a.num_prefix + 63) / 64 + (a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((dkdv_kernel<D>), gkv, dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const dim3 gq = wg_grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);

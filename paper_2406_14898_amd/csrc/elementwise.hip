@@ -354,4 +354,35 @@ hipError_t pack_client(DType dt, const void* client, void* packed, const int32_t
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// P-tuning v2 prefix gradients: out_k[e] += sum_s part[0][s][e], out_v[e] +=
+// sum_s part[1][s][e] over e < n (n = num_prefix * hidden), sequences in
+// index order (deterministic).  Four elements per thread.
+// ---------------------------------------------------------------------------
+__global__ void prefix_grad_reduce_kernel(const float* part, int S, long n, float* out_k, float* out_v) {
+  const long e = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  const int which = blockIdx.y;
+  if (e >= n) return;
+  const float* src = part + (long)which * S * n + e;
+  float* dst = (which ? out_v : out_k) + e;
+  Vec4<float> acc;
+  acc.load(dst);
+  float a[4] = {acc.get(0), acc.get(1), acc.get(2), acc.get(3)};
+  for (int s = 0; s < S; ++s) {
+    Vec4<float> v;
+    v.load(src + (long)s * n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] += v.get(i);
+  }
+  acc.set(a);
+  acc.store(dst);
+}
+
+hipError_t prefix_grad_reduce(const float* part, int S, long n, float* out_k, float* out_v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const dim3 g((unsigned)((n / 4 + 255) / 256), 2);
+  hipLaunchKernelGGL(prefix_grad_reduce_kernel, g, dim3(256), 0, st, part, S, n, out_k, out_v);
+  return hipGetLastError();
+}
+
 }  // namespace flglm

@@ -91,7 +91,7 @@ namespace {
 
 const char* const kProfNames[FL_PROF_NUM_CLASSES] = {
     "plan",          "layernorm_fwd", "gemm_nt_bias", "rope_qk",  "attn_fwd",     "gemm_nt_bias_res", "gemm_nt_bias_gelu",
-    "gemm_tn_acc",   "gemm_nn_gelu_bwd", "gemm_nn",   "layernorm_bwd", "colsum", "attn_bwd"};
+    "gemm_tn_acc",   "gemm_nn_gelu_bwd", "gemm_nn",   "layernorm_bwd", "colsum", "attn_bwd", "prefix_grad"};
 
 hipError_t take_event(fl_stack* st, hipEvent_t* e) {
   if (!st->pool.empty()) {
@@ -195,6 +195,10 @@ int validate_desc(const fl_stack_desc* d) {
     return fail(FL_ERR_SHAPE, "rotary_dim %d must be a multiple of 32 in [0, head dim]", d->rotary_dim);
   if (!(d->rope_base > 0.f)) return fail(FL_ERR_SHAPE, "rope_base must be > 0");
   if (!(d->ln_eps > 0.f)) return fail(FL_ERR_SHAPE, "ln_eps must be > 0");
+  if (d->num_prefix < 0 || d->num_prefix > 4096)
+    return fail(FL_ERR_SHAPE, "num_prefix %d must be in [0, 4096]", d->num_prefix);
+  if (d->num_prefix > 0 && d->dtype != FL_BF16)
+    return fail(FL_ERR_SHAPE, "the P-tuning v2 prefix (num_prefix > 0) needs dtype FL_BF16");
   return FL_OK;
 }
 
@@ -257,6 +261,7 @@ struct Work {
   void *dz, *dh, *tmp, *dqkv;
   float* delta;
   float *part, *part2;
+  float* dprefix;
 };
 void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, T = bi.T;
@@ -274,6 +279,9 @@ void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   const size_t nmax = std::max(F, 3 * H);
   w->part = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
   w->part2 = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
+  // per-sequence P-tuning v2 prefix gradients, [2][S][L_p][H] fp32
+  const size_t np = st->d.num_prefix;
+  w->dprefix = np ? (float*)cv.take(sizeof(float) * 2 * bi.S * np * H) : nullptr;
 }
 
 size_t saved_bytes(const fl_stack* st, const BatchInfo& bi, bool recompute) {
@@ -301,11 +309,12 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 
 int check_params(const fl_stack* st, const fl_layer_params* layers) {
   if (!layers) return fail(FL_ERR_NULL, "layers is NULL");
+  const int n = st->d.num_prefix ? 14 : 12;
   for (int l = 0; l < st->d.num_layers; ++l) {
-    const void* ps[12] = {layers[l].w_qkv, layers[l].b_qkv, layers[l].w_o, layers[l].b_o,
-                          layers[l].w_1,   layers[l].b_1,   layers[l].w_2, layers[l].b_2,
-                          layers[l].ln1_g, layers[l].ln1_b, layers[l].ln2_g, layers[l].ln2_b};
-    for (int i = 0; i < 12; ++i) {
+    const void* ps[14] = {layers[l].w_qkv, layers[l].b_qkv, layers[l].w_o,   layers[l].b_o,   layers[l].w_1,
+                          layers[l].b_1,   layers[l].w_2,   layers[l].b_2,   layers[l].ln1_g, layers[l].ln1_b,
+                          layers[l].ln2_g, layers[l].ln2_b, layers[l].prefix_k, layers[l].prefix_v};
+    for (int i = 0; i < n; ++i) {
       if (!ps[i]) return fail(FL_ERR_NULL, "layer %d parameter %d is NULL", l, i);
       if (!aligned16(ps[i])) return fail(FL_ERR_ALIGN, "layer %d parameter %d is not 16-byte aligned", l, i);
     }
@@ -313,15 +322,25 @@ int check_params(const fl_stack* st, const fl_layer_params* layers) {
   return FL_OK;
 }
 
+// Weight gradients: all twelve set (trained) or all NULL (frozen).  Prefix
+// gradients: required with a prefix.
 int check_grads(const fl_stack* st, const fl_layer_grads* grads) {
   if (!grads) return fail(FL_ERR_NULL, "grads is NULL");
   for (int l = 0; l < st->d.num_layers; ++l) {
     const float* ps[12] = {grads[l].w_qkv, grads[l].b_qkv, grads[l].w_o, grads[l].b_o,
                            grads[l].w_1,   grads[l].b_1,   grads[l].w_2, grads[l].b_2,
                            grads[l].ln1_g, grads[l].ln1_b, grads[l].ln2_g, grads[l].ln2_b};
+    const bool frozen = ps[0] == nullptr;
     for (int i = 0; i < 12; ++i) {
-      if (!ps[i]) return fail(FL_ERR_NULL, "layer %d gradient %d is NULL", l, i);
-      if (!aligned16(ps[i])) return fail(FL_ERR_ALIGN, "layer %d gradient %d is not 16-byte aligned", l, i);
+      if (frozen != (ps[i] == nullptr))
+        return fail(FL_ERR_NULL, "layer %d: weight gradients must be all set or all NULL (gradient %d)", l, i);
+      if (ps[i] && !aligned16(ps[i])) return fail(FL_ERR_ALIGN, "layer %d gradient %d is not 16-byte aligned", l, i);
+    }
+    if (st->d.num_prefix) {
+      if (!grads[l].prefix_k || !grads[l].prefix_v)
+        return fail(FL_ERR_NULL, "layer %d: prefix gradients are NULL with num_prefix > 0", l);
+      if (!aligned16(grads[l].prefix_k) || !aligned16(grads[l].prefix_v))
+        return fail(FL_ERR_ALIGN, "layer %d prefix gradient is not 16-byte aligned", l);
     }
   }
   return FL_OK;
@@ -401,7 +420,9 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;
   ad.num_seqs = bi.S; ad.max_seqlen = bi.maxL; ad.num_heads = st->d.num_heads; ad.head_dim = st->hd;
   ad.hidden = H; ad.total_tokens = T;
-  LAUNCH(FL_PROF_ATTN_FWD, 4.0 * H * bi.pairs, 4 * TH * E + 4.0 * T * st->d.num_heads, attn_fwd(dt, ad, s));
+  ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix;
+  const double pairs = bi.pairs + (double)st->d.num_prefix * T;  // every query sees the whole prefix
+  LAUNCH(FL_PROF_ATTN_FWD, 4.0 * H * pairs, 4 * TH * E + 4.0 * T * st->d.num_heads, attn_fwd(dt, ad, s));
   g = GemmDesc();
   g.A = a.o; g.B = p.w_o; g.C = a.h; g.M = T; g.N = H; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.R = x; g.ldr = H;
@@ -441,6 +462,7 @@ int ln_backward(fl_stack* st, DType dt, const void* dy, const void* xin, const f
   const double TH = (double)T * H, E = st->E;
   LAUNCH(FL_PROF_LAYERNORM_BWD, 0, 4 * TH * E + 8.0 * T,
          layernorm_bwd_dx(dt, dy, xin, mean, rstd, gamma, dres, dx, T, H, s));
+  if (!dgamma) return FL_OK;  // frozen weights
   LAUNCH(FL_PROF_COLSUM, 0, 2 * TH * E + 8.0 * T, [&]() {
     hipError_t e = colsum_partial(dt, 1, dy, H, xin, mean, rstd, T, H, w.part, w.part2, s);
     if (e == hipSuccess) e = colsum_finish(w.part, colsum_blocks(T), H, dgamma, s);
@@ -455,22 +477,30 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   const DType dt = (DType)st->d.dtype;
   const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
   const double E = st->E;
+  // frozen weights (P-tuning v2): input gradients and prefix gradients only
+  const bool train_w = gr.w_qkv != nullptr;
   int rc;
   // y = h + g W_2^T + b_2
-  if ((rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
   GemmDesc g;
-  g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  if (train_w) {
+    if ((rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
+    g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
+    LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8),
+           gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  }
   g = GemmDesc();
   g.A = dy; g.B = p.w_2; g.C = w.dz; g.M = T; g.N = F; g.K = H; g.lda = H; g.ldb = F; g.ldc = F;
   g.Z = a.z; g.ldz = F;
   LAUNCH(FL_PROF_GEMM_NN_GELU_BWD, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
          gemm(dt, GEMM_NN, EPI_GELU_BWD, with_part(g, plan), s));
   // z = w W_1^T + b_1
-  if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
-  g = GemmDesc();
-  g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  if (train_w) {
+    if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
+    g = GemmDesc();
+    g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
+    LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8),
+           gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  }
   g = GemmDesc();
   g.A = w.dz; g.B = p.w_1; g.C = w.tmp; g.M = T; g.N = H; g.K = F; g.lda = F; g.ldb = H; g.ldc = H;
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E), gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
@@ -478,10 +508,13 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, gr.ln2_g, gr.ln2_b, T, H, w, s)))
     return rc;
   // h = x + o W_o^T + b_o
-  if ((rc = colsum_into(st, dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
-  g = GemmDesc();
-  g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8), gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  if (train_w) {
+    if ((rc = colsum_into(st, dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
+    g = GemmDesc();
+    g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
+    LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8),
+           gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  }
   g = GemmDesc();
   g.A = w.dh; g.B = p.w_o; g.C = w.tmp; g.M = T; g.N = H; g.K = H; g.lda = H; g.ldb = H; g.ldc = H;
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E), gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
@@ -493,13 +526,23 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.hidden = H; ad.total_tokens = T;
   ad.dout = w.tmp; ad.ld_dout = H; ad.delta = w.delta; ad.dqkv = w.dqkv; ad.ld_dqkv = 3 * H;
   ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t; ad.rotary_dim = st->d.rotary_dim;
-  LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * bi.pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
+  ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix; ad.dprefix_part = w.dprefix;
+  const double pairs = bi.pairs + (double)st->d.num_prefix * T;
+  LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
+  if (st->d.num_prefix) {
+    // sum of the per-sequence prefix gradients, in sequence order
+    const long n = (long)st->d.num_prefix * H;
+    LAUNCH(FL_PROF_PREFIX_GRAD, 0, (2.0 * bi.S + 4.0) * n * 4,
+           prefix_grad_reduce(w.dprefix, bi.S, n, gr.prefix_k, gr.prefix_v, s));
+  }
   // qkv = u W_qkv^T + b_qkv
-  if ((rc = colsum_into(st, dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
-  g = GemmDesc();
-  g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(3 * H, H, T), gemm_bytes(3 * H, H, T, E, 8),
-         gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  if (train_w) {
+    if ((rc = colsum_into(st, dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
+    g = GemmDesc();
+    g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
+    LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(3 * H, H, T), gemm_bytes(3 * H, H, T, E, 8),
+           gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
+  }
   g = GemmDesc();
   g.A = w.dqkv; g.B = p.w_qkv; g.C = w.tmp; g.M = T; g.N = H; g.K = 3 * H; g.lda = 3 * H; g.ldb = H; g.ldc = H;
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, 3 * H), gemm_bytes(T, H, 3 * H, E, E),

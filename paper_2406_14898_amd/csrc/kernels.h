@@ -72,6 +72,10 @@ hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const voi
                           const float* rstd, int T, int N, float* partial, float* partial2, hipStream_t st);
 hipError_t colsum_finish(const float* partial, int nblk, int N, float* out, hipStream_t st);
 
+// P-tuning v2 prefix gradients: out_k += sum_s part[0][s], out_v += sum_s
+// part[1][s] over n = num_prefix * hidden elements (n % 4 == 0; fixed order).
+hipError_t prefix_grad_reduce(const float* part, int S, long n, float* out_k, float* out_v, hipStream_t st);
+
 // Attention over packed ragged sequences.  qkv rows are [q | k | v] (each H
 // wide, head h at columns h*d); o is [T, H]; lse is [T, nh] fp32.
 struct AttnDesc {
@@ -94,6 +98,15 @@ struct AttnDesc {
   const float* sin_t = nullptr;
   int rotary_dim = 0;
   int total_tokens = 0;
+  // P-tuning v2 prefix (bf16 kernels): num_prefix rows of keys pk and values
+  // pv ([num_prefix, hidden], head h at columns h*d, not rotated) in front of
+  // every sequence's keys, visible to all of its queries.  The backward
+  // writes per-sequence prefix gradients to dprefix_part, fp32
+  // [2][num_seqs][num_prefix][hidden] (keys, then values).
+  const void* pk = nullptr;
+  const void* pv = nullptr;
+  int num_prefix = 0;
+  float* dprefix_part = nullptr;
 };
 hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st);
 hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st);

@@ -111,25 +111,36 @@ int fl_test_rope(int dtype, void* qkv, const int32_t* cu_dev, int S, int T, int 
   return herr(rope_qk((DType)dtype, qkv, 3L * H, pos, cos_t, sin_t, T, H, d, rotary_dim, s));
 }
 
+// P-tuning v2 prefix arguments shared by the attention test entries.
+int check_prefix(int dtype, const void* pk, const void* pv, int num_prefix) {
+  if (num_prefix < 0 || num_prefix > 4096) return set_error(FL_ERR_ARG, "bad num_prefix");
+  if (num_prefix && dtype != FL_BF16) return set_error(FL_ERR_ARG, "the prefix needs bf16");
+  if (num_prefix && (!pk || !pv || !al16(pk) || !al16(pv))) return set_error(FL_ERR_NULL, "prefix k / v missing");
+  return FL_OK;
+}
+
 int fl_test_attention_fwd(int dtype, const void* qkv, void* o, float* lse, const int32_t* cu_dev,
                           const int32_t* prefix_dev, int T, int S, int max_seqlen, int H, int num_heads,
-                          void* stream) {
+                          const void* pk, const void* pv, int num_prefix, void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!qkv || !o || !lse || !cu_dev) return set_error(FL_ERR_NULL, "NULL argument");
   if (num_heads <= 0 || H % num_heads) return set_error(FL_ERR_ARG, "bad heads");
   const int d = H / num_heads;
   if (d != 64 && d != 128) return set_error(FL_ERR_ARG, "head dim must be 64 or 128");
+  if (int rc = check_prefix(dtype, pk, pv, num_prefix)) return rc;
   AttnDesc a;
   a.qkv = qkv; a.ld_qkv = 3L * H; a.o = o; a.ld_o = H; a.lse = lse; a.cu_seqlens = cu_dev; a.prefix_len = prefix_dev;
   a.num_seqs = S; a.max_seqlen = max_seqlen; a.num_heads = num_heads; a.head_dim = d; a.hidden = H;
   a.total_tokens = T;
+  a.pk = pk; a.pv = pv; a.num_prefix = num_prefix;
   return herr(attn_fwd((DType)dtype, a, (hipStream_t)stream));
 }
 
 int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float* lse, const void* dout, void* dqkv,
                           float* delta, const int32_t* cu_dev, const int32_t* prefix_dev, const int32_t* pos,
                           const float* cos_t, const float* sin_t, int rotary_dim, int T, int S, int max_seqlen, int H,
-                          int num_heads, void* stream) {
+                          int num_heads, const void* pk, const void* pv, int num_prefix, float* dprefix_part,
+                          void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!qkv || !o || !lse || !dout || !dqkv || !delta || !cu_dev) return set_error(FL_ERR_NULL, "NULL argument");
   if (num_heads <= 0 || H % num_heads) return set_error(FL_ERR_ARG, "bad heads");
@@ -137,12 +148,15 @@ int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float
   if (d != 64 && d != 128) return set_error(FL_ERR_ARG, "head dim must be 64 or 128");
   if (rotary_dim < 0 || rotary_dim > d || rotary_dim % 32) return set_error(FL_ERR_ARG, "bad rotary_dim");
   if (rotary_dim && (!pos || !cos_t || !sin_t)) return set_error(FL_ERR_NULL, "rotary tables missing");
+  if (int rc = check_prefix(dtype, pk, pv, num_prefix)) return rc;
+  if (num_prefix && (!dprefix_part || !al16(dprefix_part))) return set_error(FL_ERR_NULL, "dprefix_part missing");
   AttnDesc a;
   a.qkv = qkv; a.ld_qkv = 3L * H; a.o = const_cast<void*>(o); a.ld_o = H; a.lse = const_cast<float*>(lse);
   a.cu_seqlens = cu_dev; a.prefix_len = prefix_dev; a.num_seqs = S; a.max_seqlen = max_seqlen;
   a.num_heads = num_heads; a.head_dim = d; a.hidden = H; a.total_tokens = T;
   a.dout = dout; a.ld_dout = H; a.delta = delta; a.dqkv = dqkv; a.ld_dqkv = 3L * H;
   a.pos = pos; a.cos_t = cos_t; a.sin_t = sin_t; a.rotary_dim = rotary_dim;
+  a.pk = pk; a.pv = pv; a.num_prefix = num_prefix; a.dprefix_part = dprefix_part;
   return herr(attn_bwd((DType)dtype, a, (hipStream_t)stream));
 }
 

@@ -24,10 +24,11 @@ FL_BF16, FL_F32 = 0, 1
 FL_MASK_CAUSAL, FL_MASK_PREFIX = 0, 1
 FL_GEMM_NT, FL_GEMM_NN, FL_GEMM_TN = 0, 1, 2
 FL_EPI_STORE, FL_EPI_BIAS, FL_EPI_BIAS_RES, FL_EPI_BIAS_GELU, FL_EPI_GELU_BWD, FL_EPI_ACC_F32 = range(6)
-FL_PROF_NUM_CLASSES = 13
+FL_PROF_NUM_CLASSES = 14
 
 PARAM_FIELDS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
                 "ln1_g", "ln1_b", "ln2_g", "ln2_b")
+PREFIX_FIELDS = ("prefix_k", "prefix_v")  # P-tuning v2 prefix keys / values
 
 #: every extern "C" symbol the headers declare
 EXPORTS = (
@@ -49,7 +50,7 @@ class FlglmError(RuntimeError):
 class fl_stack_desc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("ffn_hidden", ctypes.c_int32), ("rotary_dim", ctypes.c_int32), ("rope_base", ctypes.c_float),
-                ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32), ("num_prefix", ctypes.c_int32)]
 
 
 class fl_batch_desc(ctypes.Structure):
@@ -60,11 +61,11 @@ class fl_batch_desc(ctypes.Structure):
 
 
 class fl_layer_params(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS + PREFIX_FIELDS]
 
 
 class fl_layer_grads(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS + PREFIX_FIELDS]
 
 
 _lib = None
@@ -103,8 +104,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
         "fl_test_colsum": [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp],
         "fl_test_rope": [ctypes.c_int, vp, vp] + [ctypes.c_int] * 6 + [ctypes.c_float, vp, vp, vp, vp],
-        "fl_test_attention_fwd": [ctypes.c_int, vp, vp, vp, vp, vp] + [ctypes.c_int] * 5 + [vp],
-        "fl_test_attention_bwd": [ctypes.c_int] + [vp] * 11 + [ctypes.c_int] * 6 + [vp],
+        "fl_test_attention_fwd": [ctypes.c_int, vp, vp, vp, vp, vp] + [ctypes.c_int] * 5 + [vp, vp, ctypes.c_int, vp],
+        "fl_test_attention_bwd": [ctypes.c_int] + [vp] * 11 + [ctypes.c_int] * 6 + [vp, vp, ctypes.c_int, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -154,8 +155,9 @@ def _stream(s) -> Optional[int]:
 # ---------------------------------------------------------------------------
 
 def stack_desc(num_layers: int, hidden: int, num_heads: int, ffn_hidden: int, rotary_dim: int,
-               dtype: int = FL_BF16, rope_base: float = 10000.0, ln_eps: float = 1e-5) -> fl_stack_desc:
-    return fl_stack_desc(num_layers, hidden, num_heads, ffn_hidden, rotary_dim, rope_base, ln_eps, dtype)
+               dtype: int = FL_BF16, rope_base: float = 10000.0, ln_eps: float = 1e-5,
+               num_prefix: int = 0) -> fl_stack_desc:
+    return fl_stack_desc(num_layers, hidden, num_heads, ffn_hidden, rotary_dim, rope_base, ln_eps, dtype, num_prefix)
 
 
 class BatchDesc:
@@ -186,11 +188,14 @@ class BatchDesc:
 
 
 def layer_params(tensors: dict) -> fl_layer_params:
-    return fl_layer_params(*[_ptr(tensors[n]) for n in PARAM_FIELDS])
+    """Device tensors by name; the prefix entries are optional."""
+    return fl_layer_params(*[_ptr(tensors.get(n)) for n in PARAM_FIELDS + PREFIX_FIELDS])
 
 
 def layer_grads(tensors: dict) -> fl_layer_grads:
-    return fl_layer_grads(*[_ptr(tensors[n]) for n in PARAM_FIELDS])
+    """Device fp32 accumulators by name; a dict without the weight names
+    means frozen weights (P-tuning v2), the prefix entries are optional."""
+    return fl_layer_grads(*[_ptr(tensors.get(n)) for n in PARAM_FIELDS + PREFIX_FIELDS])
 
 
 # ---------------------------------------------------------------------------
@@ -316,13 +321,15 @@ def fl_test_rope(dtype, qkv, cu_dev, S, T, max_seqlen, H, num_heads, rotary_dim,
 
 
 def fl_test_attention_fwd(dtype, qkv, o, lse, cu_dev, prefix_dev, T, S, max_seqlen, H, num_heads,
-                          stream=None) -> None:
+                          pk=None, pv=None, num_prefix=0, stream=None) -> None:
     _check(load().fl_test_attention_fwd(dtype, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(cu_dev), _ptr(prefix_dev), T, S,
-                                        max_seqlen, H, num_heads, _stream(stream)))
+                                        max_seqlen, H, num_heads, _ptr(pk), _ptr(pv), num_prefix, _stream(stream)))
 
 
 def fl_test_attention_bwd(dtype, qkv, o, lse, dout, dqkv, delta, cu_dev, prefix_dev, pos, cos_t, sin_t, rotary_dim,
-                          T, S, max_seqlen, H, num_heads, stream=None) -> None:
+                          T, S, max_seqlen, H, num_heads, pk=None, pv=None, num_prefix=0, dprefix_part=None,
+                          stream=None) -> None:
     _check(load().fl_test_attention_bwd(dtype, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(dout), _ptr(dqkv), _ptr(delta),
                                         _ptr(cu_dev), _ptr(prefix_dev), _ptr(pos), _ptr(cos_t), _ptr(sin_t),
-                                        rotary_dim, T, S, max_seqlen, H, num_heads, _stream(stream)))
+                                        rotary_dim, T, S, max_seqlen, H, num_heads, _ptr(pk), _ptr(pv), num_prefix,
+                                        _ptr(dprefix_part), _stream(stream)))

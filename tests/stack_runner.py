@@ -15,10 +15,12 @@ from tests.gpu_helpers import dev, host
 
 
 class GpuStack:
-    def __init__(self, shape: synth.StackShape, layers: List[Dict[str, np.ndarray]], dt: str):
+    def __init__(self, shape: synth.StackShape, layers: List[Dict[str, np.ndarray]], dt: str, num_prefix: int = 0):
+        """num_prefix > 0: the layer dicts also carry "prefix_k" / "prefix_v"
+        [num_prefix, hidden] (P-tuning v2)."""
         self.shape, self.dt = shape, dt
         self.ss = ServerStack(shape.num_layers, shape.hidden, shape.num_heads, shape.ffn_hidden, shape.rotary_dim,
-                              dt, shape.rope_base, shape.ln_eps)
+                              dt, shape.rope_base, shape.ln_eps, num_prefix)
         cache = {}  # layers given as the same dict share one device copy
         self.params = []
         for lp in layers:
@@ -26,12 +28,13 @@ class GpuStack:
                 cache[id(lp)] = {k: dev(v, dt) for k, v in lp.items()}
             self.params.append(cache[id(lp)])
 
-    def zero_grads(self):
-        return [{k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()}
-                for p in self.params]
+    def zero_grads(self, frozen: bool = False):
+        """fp32 accumulators; frozen: only the prefix ones (weights frozen)."""
+        return [{k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()
+                 if not frozen or k.startswith("prefix_")} for p in self.params]
 
     def run(self, batch: synth.Batch, x: np.ndarray, dy: Optional[np.ndarray], recompute: bool = False,
-            grads=None):
+            grads=None, frozen: bool = False):
         bd = BatchDesc.from_batch(batch)
         saved, ws = self.ss.buffers(bd, recompute, with_saved=dy is not None)
         tx = dev(x, self.dt)
@@ -41,7 +44,7 @@ class GpuStack:
         if dy is not None:
             tdy = dev(dy, self.dt)
             tdx = torch.empty_like(tx)
-            g = grads if grads is not None else self.zero_grads()
+            g = grads if grads is not None else self.zero_grads(frozen)
             self.ss.backward(bd, self.params, g, tx, saved, tdy, tdx, ws, recompute)
             out["dx"] = tdx
             out["grads"] = g

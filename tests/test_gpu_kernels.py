@@ -307,3 +307,84 @@ def test_attention_fwd_bwd(dt, heads, bname):
         assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
         assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
         assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
+
+
+# ---------------------------------------------------------------------------
+# P-tuning v2 prefix keys / values (Appendix A, P-tuning v2 section)
+# ---------------------------------------------------------------------------
+
+def _lse_prefix_ref(q, k, pk, b):
+    """Natural-log sum-exp of the scaled scores over every key a query sees:
+    the whole prefix plus its visible own keys."""
+    T, nh, d = q.shape
+    out = np.zeros((T, nh))
+    for s in range(b.num_seqs):
+        r0, r1 = int(b.cu_seqlens[s]), int(b.cu_seqlens[s + 1])
+        L = r1 - r0
+        P = None if b.mask != "prefix" else int(b.prefix_len[s])
+        allowed = np.concatenate([np.ones((L, len(pk)), bool), oracle.allowed_mask(L, P)], axis=1)
+        for h in range(nh):
+            S = (q[r0:r1, h] @ np.concatenate([pk[:, h], k[r0:r1, h]]).T) / math.sqrt(d)
+            S = np.where(allowed, S, -np.inf)
+            m = S.max(axis=1, keepdims=True)
+            out[r0:r1, h] = (m + np.log(np.exp(S - m).sum(1, keepdims=True)))[:, 0]
+    return out
+
+
+@pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
+@pytest.mark.parametrize("bname", list(BATCHES))
+@pytest.mark.parametrize("num_prefix", [1, 64, 70])
+def test_attention_prefix_fwd_bwd(heads, bname, num_prefix):
+    """bf16 attention with num_prefix prefix keys / values in front of every
+    sequence: o, LSE, dq / dk / dv (with and without the inverse rotation)
+    and the prefix gradients summed over the sequences, against the oracle."""
+    nh, d = heads
+    H = nh * d
+    b = BATCHES[bname]
+    T, S = b.total_tokens, b.num_seqs
+    qkv = _qkv(T, H, 50 + num_prefix, "bf16")
+    pk, pv = rnd((num_prefix, H), 51), rnd((num_prefix, H), 52)
+    q = qkv[:, :H].astype(np.float64).reshape(T, nh, d)
+    k = qkv[:, H:2 * H].astype(np.float64).reshape(T, nh, d)
+    v = qkv[:, 2 * H:].astype(np.float64).reshape(T, nh, d)
+    pk3, pv3 = pk.astype(np.float64).reshape(-1, nh, d), pv.astype(np.float64).reshape(-1, nh, d)
+    o_ref = oracle.attention_forward(q, k, v, b, pk3, pv3).reshape(T, H)
+    cu = dev_i32(b.cu_seqlens)
+    pre = dev_i32(b.prefix_len) if b.mask == "prefix" else None
+    t, tpk, tpv = dev(qkv, "bf16"), dev(pk, "bf16"), dev(pv, "bf16")
+    o = torch.full((T, H), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((T, nh), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_fwd(F.FL_BF16, t, o, lse, cu, pre, T, S, b.max_seqlen, H, nh, tpk, tpv, num_prefix)
+    sync()
+    assert rel_l2(host(o), o_ref) < TOL["bf16"] / 2
+    assert rel_l2(host(lse), _lse_prefix_ref(q, k, pk3, b)) < 1e-5
+
+    do = rnd((T, H), 53)
+    dq, dk, dv, dpk, dpv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b, pk3, pv3)
+    for r in (0, d // 2):
+        dqr, dkr = dq, dk
+        pos = ct = st = None
+        if r:
+            p = oracle.positions(b.cu_seqlens)
+            cos, sin = oracle.rope_tables(p, r, 10000.0)
+            dqr = oracle.rope(dq, cos, sin, r, inverse=True)
+            dkr = oracle.rope(dk, cos, sin, r, inverse=True)
+            pos = torch.empty(T, dtype=torch.int32, device="cuda")
+            ct = torch.empty(b.max_seqlen * r // 2, dtype=torch.float32, device="cuda")
+            st = torch.empty_like(ct)
+            scratch = torch.zeros((T, 3 * H), dtype=torch.bfloat16, device="cuda")
+            F.fl_test_rope(F.FL_BF16, scratch, cu, S, T, b.max_seqlen, H, nh, r, 10000.0, pos, ct, st)
+        dqkv = torch.full((T, 3 * H), float("nan"), dtype=torch.bfloat16, device="cuda")
+        delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+        part = torch.full((2, S, num_prefix, H), float("nan"), dtype=torch.float32, device="cuda")
+        F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, dev(do, "bf16"), dqkv, delta, cu, pre, pos, ct, st, r, T, S,
+                                b.max_seqlen, H, nh, tpk, tpv, num_prefix, part)
+        sync()
+        g = host(dqkv)
+        tol = TOL["bf16"] / 2
+        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
+        pg = host(part).sum(axis=1)  # sequence partials -> the batch's prefix gradients
+        assert rel_l2(pg[0], dpk.reshape(-1, H)) < tol, r
+        assert rel_l2(pg[1], dpv.reshape(-1, H)) < tol, r

@@ -184,3 +184,37 @@ def test_pack_unpack_bit_exact(dt):
     for c in range(b.num_clients):
         assert F.fl_client_token_range(bd, c) == tuple(rng_[c])
     g.close()
+
+
+# ---------------------------------------------------------------------------
+# P-tuning v2 (Section 3.1, Appendix A): prefix keys / values per block,
+# weights frozen or trained
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("frozen", [True, False])
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+@pytest.mark.parametrize("num_prefix", [16, 70])
+def test_ptuning_stack_matches_oracle(frozen, mask, num_prefix):
+    """bf16, 2 blocks, head dim 128, ragged clients; the prefix gradients are
+    the sum over every sequence of every client.  Frozen: only prefix
+    gradients are formed (the weight-gradient pointers are NULL)."""
+    shape = synth.StackShape(num_layers=2, hidden=256, num_heads=2, ffn_hidden=512, rotary_dim=64)
+    cu = np.array([0, 1, 67, 200, 400, 529, 530], np.int32)
+    csp = np.array([0, 2, 3, 6], np.int32)
+    pre = np.array([0, 16, 40, 200, 3, 1], np.int32) if mask == "prefix" else None
+    b = synth.Batch(cu, csp, mask, pre)
+    layers, x, dy = _inputs(b, "bf16", seed=5, shape=shape)
+    rng = np.random.default_rng(7)
+    for lp in layers:
+        for k in ("prefix_k", "prefix_v"):
+            lp[k] = synth.bf16_round(rng.standard_normal((num_prefix, shape.hidden)).astype(np.float32))
+    g = GpuStack(shape, layers, "bf16", num_prefix)
+    res = g.to_host(g.run(b, x, dy, frozen=frozen))
+    g.close()
+    y, xs = oracle.stack_forward(layers, shape.num_layers, x, b, shape)
+    want = [oracle.zero_prefix_grads(num_prefix, shape.hidden) for _ in layers]
+    if not frozen:
+        want = [dict(oracle.zero_grads(shape), **w) for w in want]
+    dx, grads = oracle.stack_backward(layers, shape.num_layers, xs, dy, b, shape, want)
+    assert all(set(r) == set(w) for r, w in zip(res["grads"], grads))
+    _check(res, (y, dx, grads), b, TOL["bf16"])
