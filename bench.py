@@ -205,17 +205,18 @@ def copy_calibration(mib: int) -> None:
 
 
 def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
-    """Per step: GEMM 24 H^2 per token per block forward, 48 H^2 backward;
-    attention 4 H per visible (query, key) pair forward, 8 H backward.
-    Recomputation is not counted."""
+    """Per step: GEMM 24 H^2 per token per block forward, 48 H^2 backward
+    (24 H^2 with frozen weights: input gradients only); attention 4 H per
+    visible (query, key) pair forward, 8 H backward, a P-tuning v2 prefix
+    adding L_p pairs per token.  Recomputation is not counted."""
     H = w.shape.hidden
     T = b.total_tokens
-    pairs = 0.0
+    pairs = float(w.num_prefix) * T
     for s in range(b.num_seqs):
         L = float(b.seqlens[s])
         P = float(b.prefix_len[s]) if b.mask == "prefix" else 0.0
         pairs += L * (L + 1) / 2 + (P * (P - 1) / 2 if P > 1 else 0.0)
-    mult_g = 72 if w.backward else 24
+    mult_g = (48 if w.frozen else 72) if w.backward else 24
     mult_a = 12 if w.backward else 4
     g = mult_g * H * H * T * w.shape.num_layers
     a = mult_a * H * pairs * w.shape.num_layers
@@ -240,8 +241,11 @@ def device_inputs(w: synth.Workload, b: synth.Batch, seed: int):
                 t += 1.0
             p[name] = t.to(dt)
             del t
+        for name in ("prefix_k", "prefix_v")[:2 if w.num_prefix else 0]:  # P-tuning v2 prefix ~ N(0, 1)
+            p[name] = torch.randn((w.num_prefix, w.shape.hidden), generator=gen, device="cuda").to(dt)
         params.append(p)
-        grads.append({k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()})
+        grads.append({k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()
+                      if not w.frozen or k.startswith("prefix_")})
     gen.manual_seed(seed * 100003 + 99991)
     T, H = b.total_tokens, w.shape.hidden
     x = torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)
@@ -272,6 +276,9 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
     one = synth.StackShape(1, w.shape.hidden, w.shape.num_heads, w.shape.ffn_hidden, w.shape.rotary_dim,
                            w.shape.rope_base, w.shape.ln_eps)
     layer = synth.layer_params(w.shape, 0, seed=0, bf16=w.dtype == "bf16")
+    if w.num_prefix:
+        layer.update(synth.prefix_params(w.shape, 0, w.num_prefix, seed=0, bf16=w.dtype == "bf16"))
+    grads = ([oracle.zero_prefix_grads(w.num_prefix, w.shape.hidden)] if w.frozen else None)
     order = np.argsort(b.seqlens, kind="stable")
     done_tokens, spent = 0, 0.0
     seqs = []
@@ -284,7 +291,7 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
         t0 = time.perf_counter()
         y, xs = oracle.stack_forward([layer], 1, x, sub, one)
         if w.backward:
-            oracle.stack_backward([layer], 1, xs, dy, sub, one)
+            oracle.stack_backward([layer], 1, xs, dy, sub, one, grads)
         spent += time.perf_counter() - t0
         done_tokens += L
         seqs.append(L)
@@ -350,7 +357,7 @@ def main() -> int:
           flush=True)
     params, grads, x, dy = device_inputs(w, b, args.seed)
     ss = ServerStack(w.shape.num_layers, w.shape.hidden, w.shape.num_heads, w.shape.ffn_hidden, w.shape.rotary_dim,
-                     w.dtype, w.shape.rope_base, w.shape.ln_eps)
+                     w.dtype, w.shape.rope_base, w.shape.ln_eps, w.num_prefix)
     bd = BatchDesc.from_batch(b)
     saved, ws = ss.buffers(bd, w.recompute, with_saved=w.backward)
     y = torch.empty_like(x)
@@ -431,7 +438,8 @@ def main() -> int:
         "config": {"workload": w.name, "clients": b.num_clients, "seqs": b.num_seqs, "total_tokens": T,
                    "max_seqlen": b.max_seqlen, "blocks": w.shape.num_layers, "hidden": w.shape.hidden,
                    "heads": w.shape.num_heads, "ffn": w.shape.ffn_hidden, "mask": w.mask,
-                   "backward": w.backward, "recompute": w.recompute, "parallelism": "single GPU"},
+                   "backward": w.backward, "recompute": w.recompute, "parallelism": "single GPU",
+                   "ptuning_prefix": w.num_prefix, "weights_frozen": w.frozen},
         "ms_per_step_median": round(per_step[len(per_step) // 2], 3),
         "ms_per_step_min": round(per_step[0], 3),
         "mfma_util": round(flops["total"] / (ms / 1e3) / (peak * 1e12), 4),

@@ -34,7 +34,7 @@ __all__ = [
     "param_shapes", "layer_params", "activations", "upstream_grad",
 ]
 
-STREAM_PARAMS, STREAM_X, STREAM_DY, STREAM_LENS = 0, 1, 2, 3
+STREAM_PARAMS, STREAM_X, STREAM_DY, STREAM_LENS, STREAM_PREFIX = 0, 1, 2, 3, 4
 
 PARAM_NAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
                "ln1_g", "ln1_b", "ln2_g", "ln2_b")
@@ -211,6 +211,21 @@ def layer_params(shape: StackShape, layer: int, seed: int = 0, bf16: bool = True
     return out
 
 
+def prefix_params(shape: StackShape, layer: int, num_prefix: int, seed: int = 0, bf16: bool = True,
+                  std: float = 1.0) -> Dict[str, np.ndarray]:
+    """One layer's P-tuning v2 prefix: "prefix_k", "prefix_v" [num_prefix,
+    hidden] ~ N(0, std) (an embedding table's default initialisation; keys
+    of the frozen model have a comparable scale)."""
+    g = rng(seed, STREAM_PREFIX, layer)
+    out: Dict[str, np.ndarray] = {}
+    for name in ("prefix_k", "prefix_v"):
+        a = g.standard_normal(size=(num_prefix, shape.hidden), dtype=np.float32)
+        if std != 1.0:
+            a *= np.float32(std)
+        out[name] = bf16_round(a) if bf16 else a
+    return out
+
+
 def _normal(seed: int, stream: int, n_rows: int, n_cols: int, std: float, bf16: bool) -> np.ndarray:
     a = rng(seed, stream).standard_normal(size=(n_rows, n_cols), dtype=np.float32)
     if std != 1.0:
@@ -250,6 +265,8 @@ class Workload:
     recompute: bool
     dy_std: float
     description: str = ""
+    num_prefix: int = 0            # P-tuning v2 prefix length (0: none)
+    frozen: bool = False           # weights frozen: no weight gradients
 
     def batch(self, seed: int = 0) -> Batch:
         return make_batch(self.num_clients, self.per_client, self.seqlen, self.mask, 0.25, seed)
@@ -282,4 +299,11 @@ WORKLOADS: Dict[str, Workload] = {
         32, 1, (512, 2048), "causal", "bf16", True, True, 1e-2,
         "26 ChatGLM-6B-shaped blocks, fwd+bwd with per-block recompute, 32 clients x 1 seq, "
         "lengths U[512,2048], causal, bf16"),
+    "chatglm6b_26blk_ptuning128_ragged_32x1_recompute": Workload(
+        "chatglm6b_26blk_ptuning128_ragged_32x1_recompute",
+        StackShape(num_layers=26, **CHATGLM6B),
+        32, 1, (512, 2048), "causal", "bf16", True, True, 1e-2,
+        "the 32 x 1 U[512,2048] batch under P-tuning v2: 128 prefix keys / values per block, weights frozen "
+        "(input and prefix gradients only), per-block recompute, bf16",
+        num_prefix=128, frozen=True),
 }

@@ -153,3 +153,63 @@ def test_cfg4_recompute_is_bitwise_identical(layers2):
         for k in ga[l]:
             assert torch.equal(r["grads"][l][k], ga[l][k]), (l, k)
     g.close()
+
+
+# ---------------------------------------------------------------------------
+# P-tuning v2 at the full block shape: 128 prefix rows per block, weights frozen
+# ---------------------------------------------------------------------------
+
+NP = synth.WORKLOADS["chatglm6b_26blk_ptuning128_ragged_32x1_recompute"].num_prefix
+
+
+def _with_prefix(lp, l):
+    out = dict(lp)
+    out.update(synth.prefix_params(ONE, l, NP, seed=0))
+    return out
+
+
+def test_ptuning_prefix_grads_full_shape(layers2):
+    """1 block at the ChatGLM-6B shape, 2 clients / 3 ragged sequences: y, dx
+    and both prefix gradients (summed over the sequences) against the oracle;
+    no weight gradient is formed."""
+    b = synth.Batch(np.array([0, 100, 357, 421], np.int32), np.array([0, 2, 3], np.int32))
+    lp = _with_prefix(layers2[0], 0)
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=4)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=4, std=1e-2)
+    g = GpuStack(ONE, [lp], "bf16", NP)
+    res = g.to_host(g.run(b, x, dy, frozen=True))
+    g.close()
+    assert set(res["grads"][0]) == {"prefix_k", "prefix_v"}
+    yo, xs = oracle.stack_forward([lp], 1, x, b, ONE)
+    dxo, go = oracle.stack_backward([lp], 1, xs, dy, b, ONE, [oracle.zero_prefix_grads(NP, ONE.hidden)])
+    errs = {"y": rel_l2(res["y"], yo), "dx": rel_l2(res["dx"], dxo)}
+    for k in ("prefix_k", "prefix_v"):
+        errs[k] = rel_l2(res["grads"][0][k], go[0][k])
+    print(f"[fullsize] ptuning 1 block: {errs}", flush=True)
+    assert all(v < TOL for v in errs.values()), errs
+
+
+def test_ptuning_26_blocks_sampled(layers2):
+    """The P-tuning workload (26 blocks, 32 x 1 U[512,2048], recompute,
+    frozen weights): the shortest sequence's y and dx against the float32
+    oracle."""
+    w = synth.WORKLOADS["chatglm6b_26blk_ptuning128_ragged_32x1_recompute"]
+    b = w.batch()
+    n = w.shape.num_layers
+    pl = [_with_prefix(layers2[l], l) for l in range(2)]
+    layers = [pl[l % 2] for l in range(n)]
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=w.dy_std)
+    g = GpuStack(w.shape, layers, "bf16", NP)
+    res = g.run(b, x, dy, recompute=True, frozen=True)
+    host = {"y": res["y"].float().cpu().numpy(), "dx": res["dx"].float().cpu().numpy()}
+    del res
+    g.close()
+    s = int(np.argmin(b.seqlens))
+    sb, r0, r1 = _seq_batch(b, s)
+    yo, xs = oracle.stack_forward(layers, n, x[r0:r1], sb, w.shape, dtype=np.float32)
+    grads = [oracle.zero_prefix_grads(NP, ONE.hidden, np.float32) for _ in range(n)]
+    dxo, _ = oracle.stack_backward(layers, n, xs, dy[r0:r1], sb, w.shape, grads, dtype=np.float32)
+    ey, edx = rel_l2(host["y"][r0:r1], yo), rel_l2(host["dx"][r0:r1], dxo)
+    print(f"[fullsize] ptuning 26 blocks seq {s} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e}", flush=True)
+    assert ey < TOL and edx < TOL
