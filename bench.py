@@ -434,7 +434,8 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": w.dtype,
-        "data": "synthetic (seeded device draws: weights N(0,0.02), x N(0,1), dy N(0,%g))" % w.dy_std,
+        "data": "synthetic (seeded device draws: weights N(0,0.02), x N(0,1), dy N(0,%g)%s)" % (
+            w.dy_std, ", prefix keys/values N(0,1)" if w.num_prefix else ""),
         "config": {"workload": w.name, "clients": b.num_clients, "seqs": b.num_seqs, "total_tokens": T,
                    "max_seqlen": b.max_seqlen, "blocks": w.shape.num_layers, "hidden": w.shape.hidden,
                    "heads": w.shape.num_heads, "ffn": w.shape.ffn_hidden, "mask": w.mask,
