@@ -15,6 +15,9 @@ What it follows:
     scores are softmax(Q K^T / sqrt(d_h)).
   * Section 3.3 (Parallel Acceleration): client-batch training stacks the
     smashed data of M clients into one batch; nothing mixes across clients.
+  * Section 4.1.4 (Parameter Settings) and Section 3.3: the server update
+    after the backward (Adam) and the server-hierarchical replica averaging
+    (``oracle.optim``).
   * Block internals the paper does not give (pre-LN with residual, rotary on
     the first half of each head, tanh GeLU, FFN width, biases, LayerNorm eps)
     follow the readings listed in the design notes (pre-LN residual form,
@@ -31,4 +34,7 @@ from .block import (  # noqa: F401
     rope, allowed_mask, attention_forward, attention_backward, block_forward,
     block_backward, stack_forward, stack_backward, zero_grads, zero_prefix_grads, client_token_ranges,
     pack_clients, unpack_clients,
+)
+from .optim import (  # noqa: F401
+    ADAM_LR, ADAM_BETA1, ADAM_BETA2, ADAM_EPS, adam_step, average_replicas,
 )
