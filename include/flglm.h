@@ -180,6 +180,44 @@ int fl_pack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* con
 int fl_unpack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* packed, void* const* client_bufs,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Server update (Section 4.1.4, Parameter Settings: Adam, learning rate
+ * 2e-2, batch size 1, no warmup, no weight decay).  One step of Algorithm 1
+ * of the Adam paper (Kingma & Ba) over n fp32 elements, elementwise in
+ * fp32:  m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ * param -= lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps).
+ * The hyper-parameters are doubles: 1 - beta and the bias corrections
+ * 1 - beta^step are formed in double on the host and rounded to fp32 once
+ * (subtracting a beta near 1 in fp32 would lose digits).  The paper gives no betas or eps; the Adam paper's
+ * defaults (0.9, 0.999, 1e-8) are the usual choice.
+ *   param, grad, exp_avg, exp_avg_sq: device fp32 [n], caller-owned, updated
+ *     in place (grad only read unless zero_grad); exp_avg / exp_avg_sq start
+ *     at zero before step 1.
+ *   param_bf16: device bf16 [n] or NULL; when set, receives the updated
+ *     parameters rounded to nearest even (the compute copy the stack reads).
+ *   step: the 1-based time step t.  zero_grad = 1 also clears grad, ready
+ *     for the next backward's accumulation (the stack accumulates, += ).
+ * Any layout works as long as the five buffers index the same parameters
+ * element by element: one flat arena per role updates a whole stack (or
+ * every block's P-tuning prefix) in one launch.
+ * Errors: FL_ERR_NULL, FL_ERR_ALIGN (16 bytes), FL_ERR_ALIAS (buffers
+ * overlap), FL_ERR_ARG (n < 0, step < 1, lr < 0 or not finite, beta outside
+ * [0, 1), eps < 0); nothing is enqueued then.  n = 0 is a no-op. */
+int fl_adam_step(float* param, float* grad, float* exp_avg, float* exp_avg_sq, void* param_bf16, int64_t n,
+                 int64_t step, double lr, double beta1, double beta2, double eps, int zero_grad, void* stream);
+
+/* Server-hierarchical aggregation (Section 3.3, Parallel Acceleration: one
+ * server-side model per client, parameters averaged at the end of each
+ * training period; the paper's periods are 50 or 100 steps).  params is a
+ * host array of num_replicas (1..32) device pointers to fp32 [n]; every
+ * replica is overwritten with the elementwise mean (sum in replica order,
+ * divided by num_replicas, fp32).  params_bf16: NULL, or a host array of
+ * num_replicas device pointers to bf16 [n] compute copies that receive the
+ * mean rounded to nearest even.  Only parameters are averaged; optimizer
+ * moments stay with their replica.  No two buffers may overlap
+ * (FL_ERR_ALIAS); FL_ERR_NULL / FL_ERR_ALIGN / FL_ERR_ARG as above. */
+int fl_average_replicas(int32_t num_replicas, float* const* params, void* const* params_bf16, int64_t n,
+                        void* stream);
+
 /* Launch timing (off by default).  While enabled, every kernel launch the
  * handle enqueues is bracketed by two HIP events on the call's stream and
  * tagged with its class and its algorithmic work (flops of the contraction,

@@ -8,3 +8,4 @@ no CPU path.
 from . import flglm  # noqa: F401
 from .flglm import BatchDesc, FlglmError, load  # noqa: F401
 from .stack import ServerStack  # noqa: F401
+from .optim import ParamArena, average  # noqa: F401

@@ -35,6 +35,7 @@ EXPORTS = (
     "fl_stack_create", "fl_stack_destroy", "fl_stack_saved_bytes", "fl_stack_workspace_bytes",
     "fl_server_stack_forward", "fl_server_stack_backward", "fl_client_token_range",
     "fl_pack_clients", "fl_unpack_clients", "fl_last_error",
+    "fl_adam_step", "fl_average_replicas",
     "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_colsum",
     "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
@@ -94,6 +95,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_client_token_range": [P(fl_batch_desc), i32, P(i64), P(i64)],
         "fl_pack_clients": [vp, P(fl_batch_desc), P(vp), vp, vp, sz, vp],
         "fl_unpack_clients": [vp, P(fl_batch_desc), vp, P(vp), vp, sz, vp],
+        "fl_adam_step": [vp, vp, vp, vp, vp, i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                         ctypes.c_double, ctypes.c_int, vp],
+        "fl_average_replicas": [i32, P(vp), P(vp), i64, vp],
         "fl_stack_profile": [vp, ctypes.c_int],
         "fl_stack_profile_read": [vp, ctypes.c_int, P(i64), P(ctypes.c_double), P(ctypes.c_double),
                                   P(ctypes.c_double)],
@@ -259,6 +263,19 @@ def fl_unpack_clients(handle: int, batch: BatchDesc, packed, client_bufs, worksp
     arr = (ctypes.c_void_p * len(client_bufs))(*[_ptr(c) for c in client_bufs])
     _check(load().fl_unpack_clients(handle, ctypes.byref(batch.desc), _ptr(packed), arr, _ptr(workspace),
                                     workspace_bytes, _stream(stream)))
+
+
+def fl_adam_step(param, grad, exp_avg, exp_avg_sq, param_bf16, n: int, step: int, lr: float = 2e-2,
+                 beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8, zero_grad: bool = False,
+                 stream=None) -> None:
+    _check(load().fl_adam_step(_ptr(param), _ptr(grad), _ptr(exp_avg), _ptr(exp_avg_sq), _ptr(param_bf16), n, step,
+                               lr, beta1, beta2, eps, int(zero_grad), _stream(stream)))
+
+
+def fl_average_replicas(params, params_bf16, n: int, stream=None) -> None:
+    arr = (ctypes.c_void_p * len(params))(*[_ptr(p) for p in params])
+    arr16 = None if params_bf16 is None else (ctypes.c_void_p * len(params_bf16))(*[_ptr(p) for p in params_bf16])
+    _check(load().fl_average_replicas(len(params), arr, arr16, n, _stream(stream)))
 
 
 def fl_stack_profile(handle: int, enable: bool) -> None:

@@ -152,3 +152,44 @@ def test_forward_rejects_before_any_device_work():
                                       1 << 34, ws_n, None)
     assert rc == F.FL_ERR_ALIAS
     F.fl_stack_destroy(h)
+
+
+def test_adam_and_average_reject_before_any_device_work():
+    """The server-update entry points validate on the host (fake device
+    addresses are never dereferenced when validation fails)."""
+    lib = _lib()
+    A, B, C, D, E = 1 << 30, 1 << 31, 3 << 30, 1 << 32, 5 << 30
+    n = 1 << 20
+    adam = lambda p=A, g=B, m=C, v=D, p16=None, n=n, step=1, lr=2e-2, b1=0.9, b2=0.999, eps=1e-8, zg=0: \
+        lib.fl_adam_step(p, g, m, v, p16, n, step, lr, b1, b2, eps, zg, None)
+    assert adam(p=None) == F.FL_ERR_NULL
+    assert adam(v=None) == F.FL_ERR_NULL
+    assert adam(g=B + 4) == F.FL_ERR_ALIGN
+    assert adam(p16=E + 8) == F.FL_ERR_ALIGN
+    assert adam(m=A + 16) == F.FL_ERR_ALIAS
+    assert adam(p16=D + 4 * n - 16) == F.FL_ERR_ALIAS
+    assert adam(step=0) == F.FL_ERR_ARG
+    assert adam(n=-1) == F.FL_ERR_ARG
+    assert adam(lr=-1.0) == F.FL_ERR_ARG
+    assert adam(lr=float("nan")) == F.FL_ERR_ARG
+    assert adam(b1=1.0) == F.FL_ERR_ARG
+    assert adam(b2=-0.1) == F.FL_ERR_ARG
+    assert adam(eps=-1e-8) == F.FL_ERR_ARG
+    assert adam(zg=2) == F.FL_ERR_ARG
+    assert adam(n=0) == F.FL_OK  # no-op, nothing launched
+
+    def avg(ptrs, ptrs16=None, n=n):
+        arr = (ctypes.c_void_p * len(ptrs))(*ptrs)
+        arr16 = None if ptrs16 is None else (ctypes.c_void_p * len(ptrs16))(*ptrs16)
+        return lib.fl_average_replicas(len(ptrs), arr, arr16, n, None)
+
+    assert lib.fl_average_replicas(0, None, None, n, None) == F.FL_ERR_ARG
+    assert lib.fl_average_replicas(1, None, None, n, None) == F.FL_ERR_NULL
+    assert avg([A + (i << 28) for i in range(33)]) == F.FL_ERR_ARG
+    assert avg([A, None]) == F.FL_ERR_NULL
+    assert avg([A, B], [C, None]) == F.FL_ERR_NULL
+    assert avg([A, B + 4]) == F.FL_ERR_ALIGN
+    assert avg([A, A + 16]) == F.FL_ERR_ALIAS
+    assert avg([A, B], [C, A + 4 * n - 16]) == F.FL_ERR_ALIAS
+    assert avg([A, B], n=-5) == F.FL_ERR_ARG
+    assert avg([A, B], n=0) == F.FL_OK

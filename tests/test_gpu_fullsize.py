@@ -213,3 +213,67 @@ def test_ptuning_26_blocks_sampled(layers2):
     ey, edx = rel_l2(host["y"][r0:r1], yo), rel_l2(host["dx"][r0:r1], dxo)
     print(f"[fullsize] ptuning 26 blocks seq {s} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e}", flush=True)
     assert ey < TOL and edx < TOL
+
+
+# ---------------------------------------------------------------------------
+# Server update at the full size: every parameter of the 26-block stack
+# ---------------------------------------------------------------------------
+
+def _sample_idx(n, k, seed):
+    """k sorted indices: random ones plus both ends and the 2^31 / 2^32 marks."""
+    g = np.random.default_rng(seed)
+    marks = [0, 1, 2, 3, n - 5, n - 4, n - 3, n - 2, n - 1]
+    for b in (1 << 31, 1 << 32):
+        marks += [b + d for d in range(-4, 4) if 0 <= b + d < n]
+    return np.unique(np.concatenate([g.integers(0, n, k), np.array(marks, np.int64)]))
+
+
+def test_adam_full_stack_sampled():
+    """One Adam step over all 5.24e9 parameters of the 26-block ChatGLM-6B
+    shaped stack in one launch (indices past 2^32), with the bf16 copy and
+    the gradient clear: 200k sampled elements against the oracle."""
+    from tests.test_gpu_optim import check_adam
+    n = W5.shape.num_layers * W5.shape.params_per_layer()
+    assert n > (1 << 32)
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    p = torch.randn(n, generator=gen, device="cuda")
+    gr = torch.randn(n, generator=gen, device="cuda").mul_(1e-3)
+    m = torch.randn(n, generator=gen, device="cuda").mul_(1e-4)
+    v = torch.rand(n, generator=gen, device="cuda").mul_(1e-6)
+    p16 = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    idx = torch.from_numpy(_sample_idx(n, 200_000, 1)).cuda()
+    before = [t[idx].cpu().numpy() for t in (p, gr, m, v)]
+    from paper_2406_14898_amd import flglm as F
+    F.fl_adam_step(p, gr, m, v, p16, n, 5, 2e-2, 0.9, 0.999, 1e-8, True)
+    torch.cuda.synchronize()
+    after = [t[idx].cpu().numpy() for t in (p, m, v)]
+    check_adam(*before, 5, *after)
+    assert np.array_equal(p16[idx].view(torch.int16).cpu().numpy().view(np.uint16), synth.bf16_bits(after[0]))
+    assert int(torch.count_nonzero(gr)) == 0
+    print(f"[fullsize] adam over {n} parameters: sampled {idx.numel()} ok", flush=True)
+    del p, gr, m, v, p16
+    torch.cuda.empty_cache()
+
+
+def test_average_full_stack_sampled():
+    """Averaging four replicas of every parameter of the 26-block stack (with
+    bf16 copies): sampled elements against the oracle, replicas equal."""
+    n = W5.shape.num_layers * W5.shape.params_per_layer()
+    gen = torch.Generator(device="cuda").manual_seed(1)
+    reps = [torch.randn(n, generator=gen, device="cuda") for _ in range(4)]
+    c16 = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    idx = torch.from_numpy(_sample_idx(n, 200_000, 2)).cuda()
+    before = [r[idx].cpu().numpy() for r in reps]
+    from paper_2406_14898_amd import flglm as F
+    F.fl_average_replicas(reps, c16, n)
+    torch.cuda.synchronize()
+    ref = oracle.average_replicas(before)
+    out = [r[idx].cpu().numpy() for r in reps]
+    bound = 8e-7 * np.max(np.abs(np.stack(before)), axis=0) + 1e-38
+    for o, c in zip(out, c16):
+        assert np.array_equal(o, out[0])
+        assert np.array_equal(c[idx].view(torch.int16).cpu().numpy().view(np.uint16), synth.bf16_bits(o))
+    assert np.all(np.abs(out[0] - ref) <= bound)
+    print(f"[fullsize] average of 4 x {n} parameters: sampled {idx.numel()} ok", flush=True)
+    del reps, c16
+    torch.cuda.empty_cache()
