@@ -54,10 +54,15 @@ CLASS_KERNELS = {
     "layernorm_bwd": ("ln_bwd_dx_kernel",),
     "rope_qk": ("rope_qk_kernel",),
     "colsum": ("colsum_partial_kernel", "colsum_finish_kernel"),
+    "prefix_grad": ("prefix_grad_reduce_kernel",),
+    "adam": ("adam_kernel",),
+    "average": ("average_kernel",),
 }
 CSRC = os.path.join(ROOT, "paper_2406_14898_amd", "csrc")
 CLASS_SOURCES = {"gemm": ("gemm_bf16.hip", "common.h", "kernels.h"),
                  "attn": ("attention_bf16.hip", "attention.hip", "common.h", "kernels.h"),
+                 "adam": ("optim.hip", "common.h"),
+                 "average": ("optim.hip", "common.h"),
                  "": ("elementwise.hip", "common.h", "kernels.h")}
 COPY_KERNEL = "neg_kernel"   # calibration: y = -x over float32, reads and writes the same bytes
 
@@ -223,34 +228,102 @@ def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
     return {"gemm": g, "attention": a, "total": g + a, "pairs": pairs}
 
 
-def device_inputs(w: synth.Workload, b: synth.Batch, seed: int):
+def trained_shapes(w: synth.Workload):
+    """(name, shape) of every trained tensor, layer-major: the P-tuning v2
+    prefixes when the weights are frozen, else every weight and bias."""
+    out = []
+    for l in range(w.shape.num_layers):
+        if w.frozen:
+            out += [(f"{l}.{k}", (w.num_prefix, w.shape.hidden)) for k in ("prefix_k", "prefix_v")]
+        else:
+            out += [(f"{l}.{k}", s) for k, s in synth.param_shapes(w.shape).items()]
+            out += [(f"{l}.{k}", (w.num_prefix, w.shape.hidden)) for k in ("prefix_k", "prefix_v")[
+                :2 if w.num_prefix else 0]]
+    return out
+
+
+def device_inputs(w: synth.Workload, b: synth.Batch, seed: int, arena: bool = False):
     """Seeded device-side draws (torch Philox on the GPU) with the workload's
     distributions: weights and biases N(0, 0.02), LayerNorm gains 1 + N(0, 0.02),
-    x ~ N(0, 1), dy ~ N(0, dy_std); rounded to bf16 for bf16 workloads."""
+    x ~ N(0, 1), dy ~ N(0, dy_std); rounded to bf16 for bf16 workloads.
+    arena: the trained tensors live in one ParamArena (fp32 masters holding
+    the draws, fp32 gradients and Adam moments, bf16 compute copy); the stack
+    reads and accumulates into views of it.  Returns (params, grads, x, dy,
+    arena or None)."""
     import torch
+
+    from paper_2406_14898_amd import ParamArena
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     shapes = synth.param_shapes(w.shape)
     gen = torch.Generator(device="cuda")
+    ar = ParamArena(trained_shapes(w), bf16_copy=w.dtype == "bf16") if arena else None
+    mv = ar.master_views() if ar else {}
     params, grads = [], []
     for l in range(w.shape.num_layers):
         gen.manual_seed(seed * 100003 + l)
-        p = {}
+        draws = {}
         for name, shp in shapes.items():
             t = torch.randn(shp, generator=gen, device="cuda", dtype=torch.float32) * 0.02
             if name in ("ln1_g", "ln2_g"):
                 t += 1.0
-            p[name] = t.to(dt)
-            del t
+            draws[name] = t
         for name in ("prefix_k", "prefix_v")[:2 if w.num_prefix else 0]:  # P-tuning v2 prefix ~ N(0, 1)
-            p[name] = torch.randn((w.num_prefix, w.shape.hidden), generator=gen, device="cuda").to(dt)
+            draws[name] = torch.randn((w.num_prefix, w.shape.hidden), generator=gen, device="cuda")
+        p = {}
+        for name, t in draws.items():
+            if f"{l}.{name}" in mv:
+                mv[f"{l}.{name}"].copy_(t)
+            else:
+                p[name] = t.to(dt)
+        del draws
         params.append(p)
         grads.append({k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()
                       if not w.frozen or k.startswith("prefix_")})
+    if ar:
+        ar.refresh_compute()
+        cv, gv = ar.compute_views(), ar.grad_views()
+        for key in ar.names:
+            l, name = key.split(".", 1)
+            params[int(l)][name] = cv[key]
+            grads[int(l)][name] = gv[key]
     gen.manual_seed(seed * 100003 + 99991)
     T, H = b.total_tokens, w.shape.hidden
     x = torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)
     dy = (torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32) * w.dy_std).to(dt)
-    return params, grads, x, dy
+    return params, grads, x, dy, ar
+
+
+def average_bench(w: synth.Workload, replicas: int, launches: int) -> dict:
+    """Times the server-hierarchical aggregation alone: the mean of
+    `replicas` copies of the workload's trained parameters (fp32, with bf16
+    compute copies for bf16 workloads), written back to every replica."""
+    import torch
+
+    from paper_2406_14898_amd import flglm as F
+    n = sum(int(np.prod(s)) for _, s in trained_shapes(w))
+    per = 4 + 4 + (2 if w.dtype == "bf16" else 0)   # read fp32, write fp32 (+ bf16) per replica and element
+    if replicas * n * (6 if w.dtype == "bf16" else 4) > 200e9:
+        raise SystemExit(f"{replicas} replicas of {n} parameters do not fit beside the allocator's headroom")
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    reps = [torch.randn(n, generator=gen, device="cuda") for _ in range(replicas)]
+    c16 = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(replicas)] \
+        if w.dtype == "bf16" else None
+    stream = torch.cuda.current_stream()
+    F.fl_average_replicas(reps, c16, n, stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(launches):
+        F.fl_average_replicas(reps, c16, n, stream)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = ev[0].elapsed_time(ev[-1]) / launches * 1e3
+    nbytes = replicas * n * per
+    gbs = nbytes / (us / 1e6) / 1e9
+    return {"metric": "server-hierarchical replica averaging (one launch)", "kernel": "average",
+            "workload": w.name, "replicas": replicas, "params": n, "launches": launches,
+            "avg_launch_us": round(us, 2), "bytes_per_launch": nbytes, "achieved_gbs": round(gbs, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
@@ -327,6 +400,11 @@ def main() -> int:
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print the per-kernel table of a rocprofv3 --kernel-trace --stats run (no GPU)")
     ap.add_argument("--copy-mib", type=int, default=1024, help="size the calibration run used")
+    ap.add_argument("--update", choices=("none", "adam"), default="none",
+                    help="adam: each step ends with the Adam update of every trained parameter "
+                         "(one launch over a flat arena; gradients cleared in the same pass)")
+    ap.add_argument("--average-bench", type=int, metavar="M",
+                    help="only time the averaging of M replicas of the workload's trained parameters")
     args = ap.parse_args()
     if args.summarize_traffic:
         print(summarize_traffic(args.summarize_traffic, args.copy_mib, args.workload))
@@ -355,7 +433,12 @@ def main() -> int:
     T = b.total_tokens
     print(f"[bench] workload {w.name}: T={T} S={b.num_seqs} C={b.num_clients} maxL={b.max_seqlen}", file=sys.stderr,
           flush=True)
-    params, grads, x, dy = device_inputs(w, b, args.seed)
+    if args.average_bench:
+        print(json.dumps(average_bench(w, args.average_bench, max(args.steps, 1))))
+        return 0
+    params, grads, x, dy, arena = device_inputs(w, b, args.seed, arena=args.update == "adam")
+    if arena is not None and not w.backward:
+        raise SystemExit("--update adam needs a workload with a backward pass")
     ss = ServerStack(w.shape.num_layers, w.shape.hidden, w.shape.num_heads, w.shape.ffn_hidden, w.shape.rotary_dim,
                      w.dtype, w.shape.rope_base, w.shape.ln_eps, w.num_prefix)
     bd = BatchDesc.from_batch(b)
@@ -364,15 +447,24 @@ def main() -> int:
     dx = torch.empty_like(x) if w.backward else None
     stream = torch.cuda.current_stream()
 
+    upd_events = []
+
     def step():
         ss.forward(bd, params, x, y, saved, ws, w.recompute, stream)
         if w.backward:
             ss.backward(bd, params, grads, x, saved, dy, dx, ws, w.recompute, stream)
+        if arena is not None:
+            e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            e[0].record(stream)
+            arena.adam_step(zero_grad=True, stream=stream)
+            e[1].record(stream)
+            upd_events.append(e)
 
     for i in range(args.warmup):
         step()
         torch.cuda.synchronize()
         print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    upd_events.clear()
     F.fl_stack_profile(ss.handle, not args.no_profile)
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
@@ -452,6 +544,16 @@ def main() -> int:
         "kernels": kernels,
         "cpu_baseline": None,
     }
+    if arena is not None:
+        # read p, g, m, v; write p, m, v, the bf16 copy and the cleared g
+        per = 16 + 12 + 4 + (2 if arena.compute is not None else 0)
+        us = sum(a.elapsed_time(c) for a, c in upd_events) / len(upd_events) * 1e3
+        gbs = per * arena.n / (us / 1e6) / 1e9
+        out["config"]["update"] = "adam"
+        out["update"] = {"kernel": "adam", "params": arena.n, "launches": len(upd_events),
+                         "avg_launch_us": round(us, 2), "bytes_per_launch": per * arena.n,
+                         "achieved_gbs": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4)}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, b, args.cpu_budget)

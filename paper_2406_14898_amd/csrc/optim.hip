@@ -10,7 +10,9 @@
 //    training period): every replica receives the elementwise mean.
 //
 // Both are pure streams over HBM: 16-byte vector accesses, four elements per
-// lane and two lane groups in flight per thread, all arithmetic in fp32.
+// lane, non-temporal loads and stores (nothing is re-read, so nothing is worth
+// keeping in the caches; measured +8 % over cached accesses for Adam's nine
+// streams), all arithmetic in fp32.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -27,8 +29,17 @@ using namespace flglm;
 
 namespace {
 
+__device__ __forceinline__ f32x4 ld_nt(const float* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+}
+__device__ __forceinline__ void st_nt(float* p, f32x4 v) { __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p)); }
+__device__ __forceinline__ void st_nt(bf16* p, const float (&v)[4]) {
+  const bf16x4 b = {from_f32<bf16>(v[0]), from_f32<bf16>(v[1]), from_f32<bf16>(v[2]), from_f32<bf16>(v[3])};
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x2, b), reinterpret_cast<u32x2*>(p));
+}
+
 constexpr int kThreads = 256;
-constexpr int kUnroll = 2;                       // float4 groups per thread
+constexpr int kUnroll = 1;                       // float4 groups per thread (1 measured best)
 constexpr long kPerBlock = 4L * kThreads * kUnroll;
 constexpr int kMaxReplicas = 32;
 
@@ -56,16 +67,16 @@ __global__ void __launch_bounds__(kThreads) adam_kernel(AdamArgs a) {
   const long base = (long)blockIdx.x * kPerBlock + (long)threadIdx.x * 4;
   long e[kUnroll];
   bool full[kUnroll];
-  Vec4<float> P[kUnroll], G[kUnroll], M[kUnroll], V[kUnroll];
+  f32x4 P[kUnroll], G[kUnroll], M[kUnroll], V[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     e[u] = base + (long)u * 4 * kThreads;
     full[u] = e[u] + 4 <= a.n;
     if (full[u]) {
-      P[u].load(a.p + e[u]);
-      G[u].load(a.g + e[u]);
-      M[u].load(a.m + e[u]);
-      V[u].load(a.v + e[u]);
+      P[u] = ld_nt(a.p + e[u]);
+      G[u] = ld_nt(a.g + e[u]);
+      M[u] = ld_nt(a.m + e[u]);
+      V[u] = ld_nt(a.v + e[u]);
     }
   }
 #pragma unroll
@@ -74,28 +85,16 @@ __global__ void __launch_bounds__(kThreads) adam_kernel(AdamArgs a) {
       float p[4], m[4], v[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[i] = P[u].get(i);
-        m[i] = M[u].get(i);
-        v[i] = V[u].get(i);
-        adam_elem(a, p[i], G[u].get(i), m[i], v[i]);
+        p[i] = P[u][i];
+        m[i] = M[u][i];
+        v[i] = V[u][i];
+        adam_elem(a, p[i], G[u][i], m[i], v[i]);
       }
-      P[u].set(p);
-      M[u].set(m);
-      V[u].set(v);
-      P[u].store(a.p + e[u]);
-      M[u].store(a.m + e[u]);
-      V[u].store(a.v + e[u]);
-      if (a.p16) {
-        Vec4<bf16> b;
-        b.set(p);
-        b.store(a.p16 + e[u]);
-      }
-      if (a.zero_grad) {
-        Vec4<float> z;
-        const float zf[4] = {0.f, 0.f, 0.f, 0.f};
-        z.set(zf);
-        z.store(a.g + e[u]);
-      }
+      st_nt(a.p + e[u], f32x4{p[0], p[1], p[2], p[3]});
+      st_nt(a.m + e[u], f32x4{m[0], m[1], m[2], m[3]});
+      st_nt(a.v + e[u], f32x4{v[0], v[1], v[2], v[3]});
+      if (a.p16) st_nt(a.p16 + e[u], p);
+      if (a.zero_grad) st_nt(a.g + e[u], f32x4{0.f, 0.f, 0.f, 0.f});
     } else if (e[u] < a.n) {
       // ragged tail: fewer than four elements left, element by element
       for (long j = e[u]; j < a.n; ++j) {
@@ -118,17 +117,6 @@ struct AvgArgs {
   long n;
 };
 
-__device__ __forceinline__ void avg_store(const AvgArgs& a, long e, const float (&mean)[4]) {
-  Vec4<float> o;
-  o.set(mean);
-  Vec4<bf16> ob;
-  ob.set(mean);
-  for (int r = 0; r < a.num; ++r) {
-    o.store(a.rep[r] + e);
-    if (a.rep16[0]) ob.store(a.rep16[r] + e);
-  }
-}
-
 __global__ void __launch_bounds__(kThreads) average_kernel(AvgArgs a) {
   const long base = (long)blockIdx.x * kPerBlock + (long)threadIdx.x * 4;
   const float num_f = (float)a.num;
@@ -138,15 +126,17 @@ __global__ void __launch_bounds__(kThreads) average_kernel(AvgArgs a) {
     if (e + 4 <= a.n) {
       float s[4] = {0.f, 0.f, 0.f, 0.f};
       for (int r = 0; r < a.num; ++r) {  // replica order is the summation order
-        Vec4<float> x;
-        x.load(a.rep[r] + e);
+        const f32x4 x = ld_nt(a.rep[r] + e);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) s[i] += x.get(i);
+        for (int i = 0; i < 4; ++i) s[i] += x[i];
       }
       float mean[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) mean[i] = s[i] / num_f;
-      avg_store(a, e, mean);
+      for (int r = 0; r < a.num; ++r) {
+        st_nt(a.rep[r] + e, f32x4{mean[0], mean[1], mean[2], mean[3]});
+        if (a.rep16[0]) st_nt(a.rep16[r] + e, mean);
+      }
     } else if (e < a.n) {
       for (long j = e; j < a.n; ++j) {
         float s = 0.f;

@@ -61,6 +61,11 @@ class ParamArena:
         """Sets the masters (and the bf16 copy, rounded) from tensors."""
         for k, v in values.items():
             self._view(self.master, k).copy_(v)
+        self.refresh_compute()
+
+    def refresh_compute(self) -> None:
+        """bf16 copy := the masters rounded to nearest even (after the
+        masters were written directly through master_views())."""
         if self.compute is not None:
             self.compute.copy_(self.master)
 
