@@ -18,6 +18,8 @@ What it follows:
   * Section 4.1.4 (Parameter Settings) and Section 3.3: the server update
     after the backward (Adam) and the server-hierarchical replica averaging
     (``oracle.optim``).
+  * Section 3.1 (Model Split), client side: embedding, block 0, block N-1,
+    the final linear layer and the cross-entropy loss (``oracle.client``).
   * Block internals the paper does not give (pre-LN with residual, rotary on
     the first half of each head, tanh GeLU, FFN width, biases, LayerNorm eps)
     follow the readings listed in the design notes (pre-LN residual form,
@@ -38,3 +40,4 @@ from .block import (  # noqa: F401
 from .optim import (  # noqa: F401
     ADAM_LR, ADAM_BETA1, ADAM_BETA2, ADAM_EPS, adam_step, average_replicas,
 )
+from . import client  # noqa: F401,E402
