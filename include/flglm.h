@@ -180,6 +180,65 @@ int fl_pack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* con
 int fl_unpack_clients(fl_stack* stack, const fl_batch_desc* batch, const void* packed, void* const* client_bufs,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Client side of the split model (Section 3.1, Model Split): the client
+ * holds the embedding layer, block 0, block N-1 and the final linear layer;
+ * it computes h_0 = Block_0(Embedding(x)), receives the server's h_{N-2}, and
+ * finishes with y' = Linear(Block_{N-1}(h_{N-2})) and the cross-entropy loss
+ * against the next-token labels.  Blocks 0 and N-1 are one-block stacks
+ * (fl_stack_create with num_layers = 1); the entry points below are the
+ * embedding and the final linear layer with the loss.
+ *
+ * The final linear layer has no bias and no normalisation in front of it
+ * (the paper applies Linear directly to Block_{N-1}'s output).  Its weight
+ * is [vocab, hidden] (out-features-major, like the block weights).
+ * Token ids and labels are host arrays (the client's own tokens), copied to
+ * the device through pinned staging during the call.
+ * ------------------------------------------------------------------------ */
+typedef struct fl_client fl_client;
+
+typedef struct {
+  int64_t vocab;   /* multiple of 8, <= 2^24 (ChatGLM-6B: 130528) */
+  int32_t hidden;  /* multiple of 256, <= 16384 */
+  int32_t dtype;   /* FL_BF16 | FL_F32: element type of tables, weights, activations */
+} fl_client_desc;
+
+/* FL_ERR_SHAPE for an unsupported descriptor. */
+int fl_client_create(const fl_client_desc* desc, fl_client** out);
+int fl_client_destroy(fl_client* client);
+/* Workspace for T tokens (1 <= T <= 2^26): the logits [T, vocab rounded up
+ * to 256] in the element type, per-token log-sum-exp, labels, ids and the
+ * embedding-gradient plan.  Caller-allocated device memory. */
+int fl_client_workspace_bytes(const fl_client* client, int64_t T, size_t* bytes);
+
+/* Embedding(x): out [T, hidden] (device) = rows ids[t] (host [T], each in
+ * [0, vocab), else FL_ERR_ARG) of table [vocab, hidden] (device).  Copies:
+ * exact. */
+int fl_embedding_forward(fl_client* client, const void* table, const int32_t* ids, int64_t T, void* out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+/* Gradient of the table: dtable [vocab, hidden] (device fp32) += for every
+ * token t, dout[t] (device [T, hidden]) into row ids[t] (host).  Tokens of one
+ * id are added in token order (deterministic, no atomics). */
+int fl_embedding_backward(fl_client* client, const int32_t* ids, int64_t T, const void* dout, float* dtable,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* y' = h W^T and the cross-entropy: for every token t with labels[t] >= 0
+ * (host [T]; a negative label marks a token without target; labels >= vocab
+ * give FL_ERR_ARG), loss_tok[t] = logsumexp(y'_t) - y'_t[labels[t]], else 0;
+ * loss_sum = the sum of loss_tok in a fixed order.  h [T, hidden], W
+ * [vocab, hidden] device; loss_tok [T] and loss_sum [1] device fp32.  The
+ * logits and log-sum-exp stay in the workspace for fl_lm_head_backward. */
+int fl_lm_head_forward(fl_client* client, const void* h, const void* w, const int32_t* labels, int64_t T,
+                       float* loss_tok, float* loss_sum, void* workspace, size_t workspace_bytes, void* stream);
+/* Backward of grad_scale * loss_sum (grad_scale = 1 / labelled tokens gives
+ * the mean): dlogits = grad_scale (softmax - onehot) on labelled tokens, 0
+ * on the others (computed in place in the workspace, which must still hold
+ * the forward's logits: same T, no other head call in between); dh [T,
+ * hidden] = dlogits W; dw [vocab, hidden] fp32 += dlogits^T h, or NULL when
+ * the weight is frozen (P-tuning v2). */
+int fl_lm_head_backward(fl_client* client, const void* h, const void* w, int64_t T, float grad_scale, void* dh,
+                        float* dw, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Server update (Section 4.1.4, Parameter Settings: Adam, learning rate
  * 2e-2, batch size 1, no warmup, no weight decay).  One step of Algorithm 1
  * of the Adam paper (Kingma & Ba) over n fp32 elements, elementwise in

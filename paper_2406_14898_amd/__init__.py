@@ -9,3 +9,4 @@ from . import flglm  # noqa: F401
 from .flglm import BatchDesc, FlglmError, load  # noqa: F401
 from .stack import ServerStack  # noqa: F401
 from .optim import ParamArena, average  # noqa: F401
+from .client import ClientHead, SplitModel  # noqa: F401

@@ -17,6 +17,8 @@
 // matrix-core tile is issued as D[n][m] (B rows first) so that a lane ends
 // up with four consecutive output columns of one row, which the epilogue
 // stores as one 8- or 16-byte vector.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -36,6 +38,7 @@ struct GemmArgs {
   long ldc2;
   const void* Z;
   long ldz;
+  int nb;  // rows of B that exist (see GemmDesc::b_rows)
 };
 
 __device__ __forceinline__ float gelu_f(float z) {
@@ -166,8 +169,8 @@ gemm_kernel(GemmArgs p) {
   auto load_tiles = [&](int k0) {
     if constexpr (AK) la.load(A, p.lda, m0, p.M, k0, tid);
     else la.load(A, p.lda, m0, p.M, k0, p.K, tid);
-    if constexpr (BKc) lb.load(B, p.ldb, n0, p.N, k0, tid);
-    else lb.load(B, p.ldb, n0, p.N, k0, p.K, tid);
+    if constexpr (BKc) lb.load(B, p.ldb, n0, p.nb, k0, tid);
+    else lb.load(B, p.ldb, n0, p.N, k0, p.nb, tid);
   };
 
   f32x4 acc[WTN][WTM];
@@ -315,11 +318,36 @@ static hipError_t dispatch_layout(int epi, const GemmArgs& a, hipStream_t st) {
 
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st) {
   if (dt == DT_BF16 && gemm_bf16_dma_ok(layout, d)) return gemm_bf16_dma(layout, epi, d, st);
+  // A weight-gradient GEMM whose operands span 2^31 bytes or more along the
+  // reduction (many tokens times a wide row) is cut along the reduction into
+  // pieces the DMA kernel can address; its epilogue accumulates, so the
+  // pieces add up in order.
+  if (dt == DT_BF16 && layout == GEMM_TN && epi == EPI_ACC_F32 && d.K > 64) {
+    const long ld = d.lda > d.ldb ? d.lda : d.ldb;
+    const long kc = ((1L << 30) / (ld * 2)) / 64 * 64;  // rows per piece, half the limit
+    if (kc >= 64 && kc < d.K) {
+      GemmDesc c = d;
+      c.K = (int)kc;
+      if (gemm_bf16_dma_ok(layout, c)) {
+        const int nbr = gemm_b_rows(false, d);
+        for (long k0 = 0; k0 < d.K && k0 < nbr; k0 += kc) {  // rows of B past nbr add zero
+          c.K = (int)std::min<long>(kc, d.K - k0);
+          c.A = static_cast<const bf16*>(d.A) + k0 * d.lda;
+          c.B = static_cast<const bf16*>(d.B) + k0 * d.ldb;
+          c.b_rows = (int)std::min<long>(c.K, nbr - k0);
+          hipError_t e = gemm_bf16_dma(layout, epi, c, st);
+          if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+      }
+    }
+  }
   GemmArgs a;
   a.A = d.A; a.B = d.B; a.C = d.C;
   a.M = d.M; a.N = d.N; a.K = d.K;
   a.lda = d.lda; a.ldb = d.ldb; a.ldc = d.ldc;
   a.bias = d.bias; a.R = d.R; a.ldr = d.ldr; a.C2 = d.C2; a.ldc2 = d.ldc2; a.Z = d.Z; a.ldz = d.ldz;
+  a.nb = gemm_b_rows(layout == GEMM_NT, d);
   if (dt == DT_BF16) {
     switch (layout) {
       case GEMM_NT: return dispatch_layout<bf16, GEMM_NT>(epi, a, st);

@@ -59,6 +59,7 @@ struct G2Args {
   // fixed order and runs the epilogue.
   float* part;
   int tail, splits, fixup;
+  int nb;  // rows of B that exist (see GemmDesc::b_rows)
 };
 
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
@@ -200,10 +201,12 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     ra = buf_rsrc(p.A + m0, (uint32_t)(((long)p.K * p.lda - m0) * 2));
   }
   if constexpr (BKc) {
-    const int rows = min(kBN, p.N - n0);
+    // rows of B past p.nb (a padded N) do not exist: num_records 0 for a
+    // tile wholly past them, so nothing is read there
+    const int rows = p.nb > n0 ? min(kBN, p.nb - n0) : 0;
     rb = buf_rsrc(p.B + (long)n0 * p.ldb, (uint32_t)((long)rows * p.ldb * 2));
   } else {
-    rb = buf_rsrc(p.B + n0, (uint32_t)(((long)p.K * p.ldb - n0) * 2));
+    rb = buf_rsrc(p.B + n0, (uint32_t)(((long)p.nb * p.ldb - n0) * 2));
   }
   // DMA bookkeeping.  Instruction i (0..3) of this wave fills 1 KB of an
   // operand tile at byte (8 i + wave) * 1024; its per-lane source offset is
@@ -464,6 +467,7 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.bias = (const bf16*)d.bias; a.R = (const bf16*)d.R; a.ldr = d.ldr;
   a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
   a.part = d.part; a.tail = 0; a.splits = 1; a.fixup = 0;
+  a.nb = gemm_b_rows(BKc, d);
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
   const int cus = num_cus();

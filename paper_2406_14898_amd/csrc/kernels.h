@@ -27,7 +27,15 @@ struct GemmDesc {
   // round of tiles (bf16 LDS-DMA kernel); null = never split.
   float* part = nullptr;
   size_t part_bytes = 0;
+  // Rows B really has (the N index for NT, the reduction index for NN / TN);
+  // rows at or past it read as zero.  0 = as many as the shape implies.
+  int b_rows = 0;
 };
+// Rows of B a kernel may read for a layout and shape.
+inline int gemm_b_rows(bool b_kcontig, const GemmDesc& d) {
+  const int full = b_kcontig ? d.N : d.K;
+  return d.b_rows > 0 && d.b_rows < full ? d.b_rows : full;
+}
 // Scratch that lets gemm() split the partial last round of tiles (one
 // 256 KB slice per compute unit).
 size_t gemm_part_bytes();

@@ -28,7 +28,8 @@ extern "C" {
 
 int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, void* C, int M, int N, int K,
                  int64_t lda, int64_t ldb, int64_t ldc, const void* bias, const void* R, int64_t ldr, void* C2,
-                 int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, void* stream) {
+                 int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, int b_rows,
+                 void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!A || !B || !C) return set_error(FL_ERR_NULL, "A / B / C is NULL");
   if (!al16(A) || !al16(B) || !al16(C)) return set_error(FL_ERR_ALIGN, "A / B / C not 16-byte aligned");
@@ -58,10 +59,12 @@ int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, v
     return set_error(FL_ERR_NULL, "C2 missing");
   if (epi == FL_EPI_GELU_BWD && (!Z || !al16(Z) || ldz % 8 || ldz < N)) return set_error(FL_ERR_NULL, "Z missing");
   if (part && (!al16(part) || part_bytes < 0)) return set_error(FL_ERR_ALIGN, "part misaligned");
+  if (b_rows < 0) return set_error(FL_ERR_ARG, "b_rows < 0");
   GemmDesc d;
   d.A = A; d.B = B; d.C = C; d.M = M; d.N = N; d.K = K; d.lda = lda; d.ldb = ldb; d.ldc = ldc;
   d.bias = bias; d.R = R; d.ldr = ldr; d.C2 = C2; d.ldc2 = ldc2; d.Z = Z; d.ldz = ldz;
   d.part = part; d.part_bytes = part ? (size_t)part_bytes : 0;
+  d.b_rows = b_rows;
   return herr(gemm((DType)dtype, (GemmLayout)layout, epi, d, (hipStream_t)stream));
 }
 

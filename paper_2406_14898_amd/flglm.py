@@ -36,6 +36,8 @@ EXPORTS = (
     "fl_server_stack_forward", "fl_server_stack_backward", "fl_client_token_range",
     "fl_pack_clients", "fl_unpack_clients", "fl_last_error",
     "fl_adam_step", "fl_average_replicas",
+    "fl_client_create", "fl_client_destroy", "fl_client_workspace_bytes", "fl_embedding_forward",
+    "fl_embedding_backward", "fl_lm_head_forward", "fl_lm_head_backward",
     "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_colsum",
     "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
@@ -59,6 +61,10 @@ class fl_batch_desc(ctypes.Structure):
                 ("max_seqlen", ctypes.c_int32), ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
                 ("client_seq_ptr", ctypes.POINTER(ctypes.c_int32)), ("mask_kind", ctypes.c_int32),
                 ("prefix_len", ctypes.POINTER(ctypes.c_int32))]
+
+
+class fl_client_desc(ctypes.Structure):
+    _fields_ = [("vocab", ctypes.c_int64), ("hidden", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class fl_layer_params(ctypes.Structure):
@@ -98,11 +104,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_adam_step": [vp, vp, vp, vp, vp, i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                          ctypes.c_double, ctypes.c_int, vp],
         "fl_average_replicas": [i32, P(vp), P(vp), i64, vp],
+        "fl_client_create": [P(fl_client_desc), P(vp)],
+        "fl_client_destroy": [vp],
+        "fl_client_workspace_bytes": [vp, i64, P(sz)],
+        "fl_embedding_forward": [vp, vp, P(i32), i64, vp, vp, sz, vp],
+        "fl_embedding_backward": [vp, P(i32), i64, vp, vp, vp, sz, vp],
+        "fl_lm_head_forward": [vp, vp, vp, P(i32), i64, vp, vp, vp, sz, vp],
+        "fl_lm_head_backward": [vp, vp, vp, i64, ctypes.c_float, vp, vp, vp, sz, vp],
         "fl_stack_profile": [vp, ctypes.c_int],
         "fl_stack_profile_read": [vp, ctypes.c_int, P(i64), P(ctypes.c_double), P(ctypes.c_double),
                                   P(ctypes.c_double)],
         "fl_test_gemm": [ctypes.c_int] * 3 + [vp] * 3 + [ctypes.c_int] * 3 + [i64] * 3 + [vp, vp, i64, vp, i64, vp,
-                                                                                          i64, vp, i64, vp],
+                                                                                          i64, vp, i64, ctypes.c_int,
+                                                                                          vp],
         "fl_test_layernorm_fwd": [ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                   vp],
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
@@ -278,6 +292,53 @@ def fl_average_replicas(params, params_bf16, n: int, stream=None) -> None:
     _check(load().fl_average_replicas(len(params), arr, arr16, n, _stream(stream)))
 
 
+def _host_i32(a):
+    import numpy as np
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def fl_client_create(vocab: int, hidden: int, dtype: int = FL_BF16) -> int:
+    h = ctypes.c_void_p()
+    _check(load().fl_client_create(ctypes.byref(fl_client_desc(vocab, hidden, dtype)), ctypes.byref(h)))
+    return h.value
+
+
+def fl_client_destroy(handle: int) -> None:
+    _check(load().fl_client_destroy(handle))
+
+
+def fl_client_workspace_bytes(handle: int, T: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load().fl_client_workspace_bytes(handle, T, ctypes.byref(n)))
+    return n.value
+
+
+def fl_embedding_forward(handle: int, table, ids, out, workspace, stream=None) -> None:
+    arr, p = _host_i32(ids)
+    _check(load().fl_embedding_forward(handle, _ptr(table), p, len(arr), _ptr(out), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def fl_embedding_backward(handle: int, ids, dout, dtable, workspace, stream=None) -> None:
+    arr, p = _host_i32(ids)
+    _check(load().fl_embedding_backward(handle, p, len(arr), _ptr(dout), _ptr(dtable), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def fl_lm_head_forward(handle: int, h, w, labels, loss_tok, loss_sum, workspace, stream=None) -> None:
+    arr, p = _host_i32(labels)
+    _check(load().fl_lm_head_forward(handle, _ptr(h), _ptr(w), p, len(arr), _ptr(loss_tok), _ptr(loss_sum),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(stream)))
+
+
+def fl_lm_head_backward(handle: int, h, w, T: int, grad_scale: float, dh, dw, workspace, stream=None) -> None:
+    _check(load().fl_lm_head_backward(handle, _ptr(h), _ptr(w), T, grad_scale, _ptr(dh), _ptr(dw),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+
+
 def fl_stack_profile(handle: int, enable: bool) -> None:
     _check(load().fl_stack_profile(handle, int(enable)))
 
@@ -309,11 +370,13 @@ def profile_table(handle: int):
 # ---------------------------------------------------------------------------
 
 def fl_test_gemm(dtype, layout, epi, A, B, C, M, N, K, lda, ldb, ldc, bias=None, R=None, ldr=0, C2=None, ldc2=0,
-                 Z=None, ldz=0, part=None, stream=None) -> None:
-    """part: optional fp32 device tensor, split-reduction scratch."""
+                 Z=None, ldz=0, part=None, b_rows=0, stream=None) -> None:
+    """part: optional fp32 device tensor, split-reduction scratch; b_rows:
+    rows B really has (0 = all)."""
     nbytes = part.numel() * part.element_size() if part is not None else 0
     _check(load().fl_test_gemm(dtype, layout, epi, _ptr(A), _ptr(B), _ptr(C), M, N, K, lda, ldb, ldc, _ptr(bias),
-                               _ptr(R), ldr, _ptr(C2), ldc2, _ptr(Z), ldz, _ptr(part), nbytes, _stream(stream)))
+                               _ptr(R), ldr, _ptr(C2), ldc2, _ptr(Z), ldz, _ptr(part), nbytes, b_rows,
+                               _stream(stream)))
 
 
 def fl_test_layernorm_fwd(dtype, x, g, b, y, mean, rstd, T, H, eps, stream=None) -> None:

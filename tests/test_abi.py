@@ -193,3 +193,38 @@ def test_adam_and_average_reject_before_any_device_work():
     assert avg([A, B], [C, A + 4 * n - 16]) == F.FL_ERR_ALIAS
     assert avg([A, B], n=-5) == F.FL_ERR_ARG
     assert avg([A, B], n=0) == F.FL_OK
+
+
+def test_client_handle_validation_host_only():
+    """Client-side entry points: descriptor checks at create, id and label
+    checks on the host before anything is enqueued."""
+    lib = _lib()
+    for vocab, hidden, dt in ((100, 256, F.FL_BF16), (1000, 200, F.FL_BF16), (1000, 256, 9), (0, 256, F.FL_F32)):
+        with pytest.raises(F.FlglmError) as e:
+            F.fl_client_create(vocab, hidden, dt)
+        assert e.value.code == F.FL_ERR_SHAPE
+    h = F.fl_client_create(1000, 256, F.FL_BF16)
+    ws_n = F.fl_client_workspace_bytes(h, 10)
+    assert ws_n >= 10 * 1024 * 2  # padded logits
+    assert F.fl_client_workspace_bytes(h, 20) > ws_n
+    ids = (ctypes.c_int32 * 10)(*([5] * 9 + [1000]))
+    WS, OUT, TAB = 1 << 34, 1 << 30, 1 << 32
+    rc = lib.fl_embedding_forward(h, TAB, ids, 10, OUT, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG and "token id" in F.fl_last_error()
+    rc = lib.fl_embedding_backward(h, ids, 10, OUT, TAB, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG
+    rc = lib.fl_embedding_forward(h, TAB, ids, 10, OUT, WS, ws_n - 1, None)
+    assert rc == F.FL_ERR_WORKSPACE
+    rc = lib.fl_embedding_forward(h, TAB + 8, ids, 10, OUT, WS, ws_n, None)
+    assert rc == F.FL_ERR_ALIGN
+    labels = (ctypes.c_int32 * 10)(*([-100] * 9 + [1000]))
+    lt, ls = 1 << 31, (1 << 31) + 4096
+    rc = lib.fl_lm_head_forward(h, OUT, TAB, labels, 10, lt, ls, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG and "label" in F.fl_last_error()
+    rc = lib.fl_lm_head_forward(h, OUT, TAB, labels, 10, WS + 256, ls, WS, ws_n, None)
+    assert rc == F.FL_ERR_ALIAS
+    rc = lib.fl_lm_head_backward(h, OUT, TAB, 10, ctypes.c_float(float("inf")), lt, None, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG
+    rc = lib.fl_lm_head_backward(h, OUT, TAB, 0, ctypes.c_float(1.0), lt, None, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG
+    F.fl_client_destroy(h)
