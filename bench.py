@@ -36,8 +36,8 @@ PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix-core peaks, MI355X
 PEAK_HBM_GBS = 8000.0
 METRIC = "server-stack fwd+bwd tokens/sec and MFMA util %, ChatGLM-6B shape"
 MFMA_CLASSES = ("gemm_nt_bias", "gemm_nt_bias_res", "gemm_nt_bias_gelu", "gemm_tn_acc", "gemm_nn_gelu_bwd",
-                "gemm_nn", "attn_fwd", "attn_bwd")
-GEMM_CLASSES = MFMA_CLASSES[:6]
+                "gemm_nn", "attn_fwd", "attn_bwd", "lm_head_fwd", "lm_head_bwd")
+GEMM_CLASSES = MFMA_CLASSES[:6]   # the block GEMMs
 # Fragments of the kernel names rocprofv3 prints for each launch class of the
 # bf16 path (a class may launch several kernels), and the sources they are
 # built from (a stored counter reading is stale once these change).
@@ -209,11 +209,24 @@ def copy_calibration(mib: int) -> None:
     print(json.dumps({"copy_calibration_bytes": mib << 20, "dispatches": 3}))
 
 
+def total_layers(w: synth.Workload) -> int:
+    """Blocks a step runs: the server's, plus the client's blocks 0 and N-1
+    for the whole split model."""
+    return w.shape.num_layers + (2 if w.vocab else 0)
+
+
+def vocab_padded(w: synth.Workload) -> int:
+    return (w.vocab + 255) // 256 * 256
+
+
 def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
     """Per step: GEMM 24 H^2 per token per block forward, 48 H^2 backward
     (24 H^2 with frozen weights: input gradients only); attention 4 H per
     visible (query, key) pair forward, 8 H backward, a P-tuning v2 prefix
-    adding L_p pairs per token.  Recomputation is not counted."""
+    adding L_p pairs per token.  The whole split model adds the final
+    linear layer: 2 V H per token forward, 2 V H backward for the input
+    gradient and 2 V H for the weight gradient unless frozen.
+    Recomputation is not counted."""
     H = w.shape.hidden
     T = b.total_tokens
     pairs = float(w.num_prefix) * T
@@ -223,22 +236,25 @@ def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
         pairs += L * (L + 1) / 2 + (P * (P - 1) / 2 if P > 1 else 0.0)
     mult_g = (48 if w.frozen else 72) if w.backward else 24
     mult_a = 12 if w.backward else 4
-    g = mult_g * H * H * T * w.shape.num_layers
-    a = mult_a * H * pairs * w.shape.num_layers
-    return {"gemm": g, "attention": a, "total": g + a, "pairs": pairs}
+    g = mult_g * H * H * T * total_layers(w)
+    a = mult_a * H * pairs * total_layers(w)
+    head = (2.0 + 2.0 + (0.0 if w.frozen else 2.0)) * w.vocab * H * T if w.vocab else 0.0
+    return {"gemm": g, "attention": a, "lm_head": head, "total": g + a + head, "pairs": pairs}
 
 
 def trained_shapes(w: synth.Workload):
     """(name, shape) of every trained tensor, layer-major: the P-tuning v2
     prefixes when the weights are frozen, else every weight and bias."""
     out = []
-    for l in range(w.shape.num_layers):
+    for l in range(total_layers(w)):
         if w.frozen:
             out += [(f"{l}.{k}", (w.num_prefix, w.shape.hidden)) for k in ("prefix_k", "prefix_v")]
         else:
             out += [(f"{l}.{k}", s) for k, s in synth.param_shapes(w.shape).items()]
             out += [(f"{l}.{k}", (w.num_prefix, w.shape.hidden)) for k in ("prefix_k", "prefix_v")[
                 :2 if w.num_prefix else 0]]
+    if w.vocab and not w.frozen:
+        out += [("embedding", (w.vocab, w.shape.hidden)), ("lm_head", (w.vocab, w.shape.hidden))]
     return out
 
 
@@ -248,8 +264,11 @@ def device_inputs(w: synth.Workload, b: synth.Batch, seed: int, arena: bool = Fa
     x ~ N(0, 1), dy ~ N(0, dy_std); rounded to bf16 for bf16 workloads.
     arena: the trained tensors live in one ParamArena (fp32 masters holding
     the draws, fp32 gradients and Adam moments, bf16 compute copy); the stack
-    reads and accumulates into views of it.  Returns (params, grads, x, dy,
-    arena or None)."""
+    reads and accumulates into views of it.  The whole split model adds the
+    client's blocks (layers 0 and N-1 around the server's), an embedding
+    table ~ N(0, 1) (so block 0 sees activations of the server's scale) and
+    a final linear layer ~ N(0, 0.02).  Returns a dict: layers, grads, x, dy,
+    arena (or None), embedding, lm_head and their gradients (None: frozen)."""
     import torch
 
     from paper_2406_14898_amd import ParamArena
@@ -259,7 +278,7 @@ def device_inputs(w: synth.Workload, b: synth.Batch, seed: int, arena: bool = Fa
     ar = ParamArena(trained_shapes(w), bf16_copy=w.dtype == "bf16") if arena else None
     mv = ar.master_views() if ar else {}
     params, grads = [], []
-    for l in range(w.shape.num_layers):
+    for l in range(total_layers(w)):
         gen.manual_seed(seed * 100003 + l)
         draws = {}
         for name, shp in shapes.items():
@@ -279,18 +298,37 @@ def device_inputs(w: synth.Workload, b: synth.Batch, seed: int, arena: bool = Fa
         params.append(p)
         grads.append({k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in p.items()
                       if not w.frozen or k.startswith("prefix_")})
+    out = {"embedding": None, "lm_head": None, "g_embedding": None, "g_lm_head": None}
+    if w.vocab:
+        gen.manual_seed(seed * 100003 + 99989)
+        for name, std in (("embedding", 1.0), ("lm_head", 0.02)):
+            t = torch.randn((w.vocab, w.shape.hidden), generator=gen, device="cuda") * std
+            if name in mv:
+                mv[name].copy_(t)
+            else:
+                out[name] = t.to(dt)
+            del t
     if ar:
         ar.refresh_compute()
         cv, gv = ar.compute_views(), ar.grad_views()
         for key in ar.names:
+            if "." not in key:
+                out[key], out["g_" + key] = cv[key], gv[key]
+                continue
             l, name = key.split(".", 1)
             params[int(l)][name] = cv[key]
             grads[int(l)][name] = gv[key]
+    elif w.vocab and not w.frozen:
+        out["g_embedding"] = torch.zeros((w.vocab, w.shape.hidden), dtype=torch.float32, device="cuda")
+        out["g_lm_head"] = torch.zeros((w.vocab, w.shape.hidden), dtype=torch.float32, device="cuda")
     gen.manual_seed(seed * 100003 + 99991)
     T, H = b.total_tokens, w.shape.hidden
-    x = torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)
-    dy = (torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32) * w.dy_std).to(dt)
-    return params, grads, x, dy, ar
+    out["x"] = out["dy"] = None
+    if not w.vocab:
+        out["x"] = torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32).to(dt)
+        out["dy"] = (torch.randn((T, H), generator=gen, device="cuda", dtype=torch.float32) * w.dy_std).to(dt)
+    out.update(layers=params, grads=grads, arena=ar)
+    return out
 
 
 def average_bench(w: synth.Workload, replicas: int, launches: int) -> dict:
@@ -371,14 +409,31 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
         if spent >= budget_s:
             break
     per_block_tok_s = done_tokens / spent
+    nl = total_layers(w)
+    sec_per_tok = nl / per_block_tok_s
+    head = ""
+    if w.vocab:
+        # the final linear layer with the loss, forward and backward, on a few tokens
+        n = 32
+        g = np.random.default_rng(3)
+        wv = g.standard_normal((w.vocab, w.shape.hidden)) * 0.02
+        h = g.standard_normal((n, w.shape.hidden))
+        lab = g.integers(0, w.vocab, n)
+        t0 = time.perf_counter()
+        lg, lse, _, _ = oracle.client.lm_head_forward(h, wv, lab)
+        oracle.client.lm_head_backward(h, wv, lg, lse, lab, 1.0 / n)
+        th = time.perf_counter() - t0
+        del wv, lg
+        sec_per_tok += th / n
+        head = f"; final linear layer + loss (vocab {w.vocab}) fwd+bwd on {n} tokens in {th:.1f} s"
     return {
-        "value": per_block_tok_s / w.shape.num_layers,
+        "value": 1.0 / sec_per_tok,
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"1 of {w.shape.num_layers} blocks, {'fwd+recompute+bwd' if w.backward else 'fwd'}, float64, "
+        "sample": (f"1 of {nl} blocks, {'fwd+recompute+bwd' if w.backward else 'fwd'}, float64, "
                    f"{len(seqs)} whole sequence(s) of lengths {seqs} ({done_tokens} tokens) in {spent:.1f} s; "
-                   f"tokens/s divided by {w.shape.num_layers} blocks; host {cpu}, BLAS {blas}, "
+                   f"per-token time times {nl} blocks{head}; host {cpu}, BLAS {blas}, "
                    f"{len(os.sched_getaffinity(0))} cores visible"),
     }
 
@@ -423,7 +478,7 @@ def main() -> int:
 
     import torch
 
-    from paper_2406_14898_amd import BatchDesc, ServerStack
+    from paper_2406_14898_amd import BatchDesc, ServerStack, SplitModel
     from paper_2406_14898_amd import flglm as F
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -436,23 +491,51 @@ def main() -> int:
     if args.average_bench:
         print(json.dumps(average_bench(w, args.average_bench, max(args.steps, 1))))
         return 0
-    params, grads, x, dy, arena = device_inputs(w, b, args.seed, arena=args.update == "adam")
+    inp = device_inputs(w, b, args.seed, arena=args.update == "adam")
+    arena = inp["arena"]
     if arena is not None and not w.backward:
         raise SystemExit("--update adam needs a workload with a backward pass")
-    ss = ServerStack(w.shape.num_layers, w.shape.hidden, w.shape.num_heads, w.shape.ffn_hidden, w.shape.rotary_dim,
-                     w.dtype, w.shape.rope_base, w.shape.ln_eps, w.num_prefix)
+    params, grads = inp["layers"], inp["grads"]
+    sh = w.shape
     bd = BatchDesc.from_batch(b)
-    saved, ws = ss.buffers(bd, w.recompute, with_saved=w.backward)
-    y = torch.empty_like(x)
-    dx = torch.empty_like(x) if w.backward else None
     stream = torch.cuda.current_stream()
+    client_marks = []  # (class, start event, end event) of the client-side calls
+    if w.vocab:
+        # the whole split model: client embedding + block 0, the server's
+        # blocks, client block N-1 + final linear layer and loss
+        model = SplitModel(sh.hidden, sh.num_heads, sh.ffn_hidden, sh.rotary_dim, sh.num_layers, w.vocab, w.dtype,
+                           sh.rope_base, sh.ln_eps, w.num_prefix)
+        handles = [model.block0.handle, model.server.handle, model.block_last.handle]
+        buf = model.buffers(bd, w.recompute)
+        ids, labels = synth.token_ids(b, w.vocab, args.seed)
+        scale = 1.0 / max(1, int((labels >= 0).sum()))
+        sp = {"embedding": inp["embedding"], "lm_head": inp["lm_head"], "block0": params[0],
+              "server": params[1:-1], "block_last": params[-1]}
+        sg = {"embedding": inp["g_embedding"], "lm_head": inp["g_lm_head"], "block0": grads[0],
+              "server": grads[1:-1], "block_last": grads[-1]}
+
+        def fwd_bwd(timed):
+            model.step(bd, ids, labels, sp, sg, scale, buf, w.recompute, stream, client_marks if timed else None)
+        close = model.close
+    else:
+        ss = ServerStack(sh.num_layers, sh.hidden, sh.num_heads, sh.ffn_hidden, sh.rotary_dim, w.dtype, sh.rope_base,
+                         sh.ln_eps, w.num_prefix)
+        handles = [ss.handle]
+        saved, ws = ss.buffers(bd, w.recompute, with_saved=w.backward)
+        x, dy = inp["x"], inp["dy"]
+        y = torch.empty_like(x)
+        dx = torch.empty_like(x) if w.backward else None
+
+        def fwd_bwd(timed):
+            ss.forward(bd, params, x, y, saved, ws, w.recompute, stream)
+            if w.backward:
+                ss.backward(bd, params, grads, x, saved, dy, dx, ws, w.recompute, stream)
+        close = ss.close
 
     upd_events = []
 
-    def step():
-        ss.forward(bd, params, x, y, saved, ws, w.recompute, stream)
-        if w.backward:
-            ss.backward(bd, params, grads, x, saved, dy, dx, ws, w.recompute, stream)
+    def step(timed=True):
+        fwd_bwd(timed)
         if arena is not None:
             e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             e[0].record(stream)
@@ -461,11 +544,12 @@ def main() -> int:
             upd_events.append(e)
 
     for i in range(args.warmup):
-        step()
+        step(timed=False)
         torch.cuda.synchronize()
         print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     upd_events.clear()
-    F.fl_stack_profile(ss.handle, not args.no_profile)
+    for h in handles:
+        F.fl_stack_profile(h, not args.no_profile)
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     marks[0].record(stream)
@@ -475,8 +559,26 @@ def main() -> int:
     torch.cuda.synchronize()
     ms = marks[0].elapsed_time(marks[-1]) / args.steps
     per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
-    prof = F.profile_table(ss.handle)
-    F.fl_stack_profile(ss.handle, False)
+    prof = {}
+    for h in handles:
+        for k, r in F.profile_table(h).items():
+            e = prof.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+            for f in e:
+                e[f] += r[f]
+        F.fl_stack_profile(h, False)
+    if w.vocab and not args.no_profile:
+        # client-side calls timed with events on the same stream
+        H, Vp = sh.hidden, vocab_padded(w)
+        work = {"lm_head_fwd": (2.0 * T * Vp * H, 0.0),
+                "lm_head_bwd": ((2.0 if w.frozen else 4.0) * T * Vp * H, 0.0),
+                "embedding_fwd": (0.0, 2.0 * T * H * (2 if w.dtype == "bf16" else 4)),
+                "embedding_bwd": (0.0, T * H * ((2 if w.dtype == "bf16" else 4) + 8.0))}
+        for name, a, e in client_marks:
+            r = prof.setdefault(name, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+            r["launches"] += 1
+            r["ms"] += a.elapsed_time(e)
+            r["flops"] += work[name][0]
+            r["bytes"] += work[name][1]
     print(f"[bench] timed {args.steps} steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
 
     flops = algorithmic_flops(w, b)
@@ -526,13 +628,17 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": w.dtype,
-        "data": "synthetic (seeded device draws: weights N(0,0.02), x N(0,1), dy N(0,%g)%s)" % (
-            w.dy_std, ", prefix keys/values N(0,1)" if w.num_prefix else ""),
+        "data": ("synthetic (seeded device draws: weights N(0,0.02), %s%s)" % (
+            "embedding N(0,1), token ids uniform over the vocabulary, next-token labels" if w.vocab else
+            "x N(0,1), dy N(0,%g)" % w.dy_std, ", prefix keys/values N(0,1)" if w.num_prefix else "")),
         "config": {"workload": w.name, "clients": b.num_clients, "seqs": b.num_seqs, "total_tokens": T,
                    "max_seqlen": b.max_seqlen, "blocks": w.shape.num_layers, "hidden": w.shape.hidden,
                    "heads": w.shape.num_heads, "ffn": w.shape.ffn_hidden, "mask": w.mask,
                    "backward": w.backward, "recompute": w.recompute, "parallelism": "single GPU",
-                   "ptuning_prefix": w.num_prefix, "weights_frozen": w.frozen},
+                   "ptuning_prefix": w.num_prefix, "weights_frozen": w.frozen,
+                   "scope": ("whole split model: client embedding + block 0, %d server blocks, client block %d + "
+                             "final linear (vocab %d) + cross-entropy" % (w.shape.num_layers, w.shape.num_layers + 1,
+                                                                          w.vocab)) if w.vocab else "server stack"},
         "ms_per_step_median": round(per_step[len(per_step) // 2], 3),
         "ms_per_step_min": round(per_step[0], 3),
         "mfma_util": round(flops["total"] / (ms / 1e3) / (peak * 1e12), 4),
@@ -557,7 +663,7 @@ def main() -> int:
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, b, args.cpu_budget)
-    ss.close()
+    close()
     print(json.dumps(out))
     return 0
 

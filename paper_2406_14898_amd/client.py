@@ -61,7 +61,6 @@ class SplitModel:
         self.block_last = ServerStack(1, *args)
         self.head = ClientHead(vocab, hidden, dtype)
         self.hidden = hidden
-        self.tdt = None
 
     def close(self) -> None:
         for s in (self.block0, self.server, self.block_last, self.head):
@@ -85,25 +84,38 @@ class SplitModel:
         return b
 
     def step(self, batch: F.BatchDesc, ids, labels, params: Dict, grads: Dict, grad_scale: float, buf: Dict,
-             recompute: bool = False, stream=None) -> None:
+             recompute: bool = False, stream=None, marks: Optional[List] = None) -> None:
         """One training step.  params: "embedding" [V, H], "lm_head" [V, H],
         "block0" / "block_last" (one layer's dict), "server" (list of layer
         dicts).  grads: the same keys with fp32 accumulators (+=); a missing
         or None "embedding" / "lm_head" entry, and block dicts without weight
-        keys, mean frozen (P-tuning v2)."""
+        keys, mean frozen (P-tuning v2).  marks: when a list, each client-side
+        call is bracketed by two timing events on the stream and appended as
+        (name, start, end)."""
         T = buf["T"]
         h = self.head
-        h.embed(params["embedding"], ids, buf["e"], buf["client_ws"], stream)
+
+        def timed(name, fn, *a):
+            if marks is None:
+                return fn(*a)
+            import torch
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(*a)
+            e1.record(stream)
+            marks.append((name, e0, e1))
+
+        timed("embedding_fwd", h.embed, params["embedding"], ids, buf["e"], buf["client_ws"], stream)
         self.block0.forward(batch, [params["block0"]], buf["e"], buf["h0"], buf["b0_saved"], buf["b0_ws"],
                             recompute, stream)
         self.server.forward(batch, params["server"], buf["h0"], buf["hs"], buf["srv_saved"], buf["srv_ws"],
                             recompute, stream)
         self.block_last.forward(batch, [params["block_last"]], buf["hs"], buf["hl"], buf["bl_saved"], buf["bl_ws"],
                                 recompute, stream)
-        h.head_forward(buf["hl"], params["lm_head"], labels, buf["loss_tok"], buf["loss_sum"], buf["client_ws"],
-                       stream)
-        h.head_backward(buf["hl"], params["lm_head"], T, grad_scale, buf["d_hl"], grads.get("lm_head"),
-                        buf["client_ws"], stream)
+        timed("lm_head_fwd", h.head_forward, buf["hl"], params["lm_head"], labels, buf["loss_tok"], buf["loss_sum"],
+              buf["client_ws"], stream)
+        timed("lm_head_bwd", h.head_backward, buf["hl"], params["lm_head"], T, grad_scale, buf["d_hl"],
+              grads.get("lm_head"), buf["client_ws"], stream)
         self.block_last.backward(batch, [params["block_last"]], [grads["block_last"]], buf["hs"], buf["bl_saved"],
                                  buf["d_hl"], buf["d_hs"], buf["bl_ws"], recompute, stream)
         self.server.backward(batch, params["server"], grads["server"], buf["h0"], buf["srv_saved"], buf["d_hs"],
@@ -111,4 +123,4 @@ class SplitModel:
         self.block0.backward(batch, [params["block0"]], [grads["block0"]], buf["e"], buf["b0_saved"], buf["d_h0"],
                              buf["d_e"], buf["b0_ws"], recompute, stream)
         if grads.get("embedding") is not None:
-            h.embed_backward(ids, buf["d_e"], grads["embedding"], buf["client_ws"], stream)
+            timed("embedding_bwd", h.embed_backward, ids, buf["d_e"], grads["embedding"], buf["client_ws"], stream)

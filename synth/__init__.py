@@ -28,13 +28,13 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = [
-    "STREAM_PARAMS", "STREAM_X", "STREAM_DY", "STREAM_LENS",
+    "STREAM_PARAMS", "STREAM_X", "STREAM_DY", "STREAM_LENS", "STREAM_PREFIX", "STREAM_TOKENS",
     "PARAM_NAMES", "StackShape", "Batch", "Workload", "WORKLOADS",
     "bf16_round", "bf16_bits", "bits_to_f32", "rng", "make_batch",
-    "param_shapes", "layer_params", "activations", "upstream_grad",
+    "param_shapes", "layer_params", "prefix_params", "activations", "upstream_grad", "token_ids",
 ]
 
-STREAM_PARAMS, STREAM_X, STREAM_DY, STREAM_LENS, STREAM_PREFIX = 0, 1, 2, 3, 4
+STREAM_PARAMS, STREAM_X, STREAM_DY, STREAM_LENS, STREAM_PREFIX, STREAM_TOKENS = 0, 1, 2, 3, 4, 5
 
 PARAM_NAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
                "ln1_g", "ln1_b", "ln2_g", "ln2_b")
@@ -267,6 +267,7 @@ class Workload:
     description: str = ""
     num_prefix: int = 0            # P-tuning v2 prefix length (0: none)
     frozen: bool = False           # weights frozen: no weight gradients
+    vocab: int = 0                 # > 0: the whole split model (client blocks, embedding, final linear + loss)
 
     def batch(self, seed: int = 0) -> Batch:
         return make_batch(self.num_clients, self.per_client, self.seqlen, self.mask, 0.25, seed)
@@ -306,4 +307,24 @@ WORKLOADS: Dict[str, Workload] = {
         "the 32 x 1 U[512,2048] batch under P-tuning v2: 128 prefix keys / values per block, weights frozen "
         "(input and prefix gradients only), per-block recompute, bf16",
         num_prefix=128, frozen=True),
+    "chatglm6b_28blk_split_ptuning128_ragged_32x1_recompute": Workload(
+        "chatglm6b_28blk_split_ptuning128_ragged_32x1_recompute",
+        StackShape(num_layers=26, **CHATGLM6B),
+        32, 1, (512, 2048), "causal", "bf16", True, True, 1e-2,
+        "the whole split ChatGLM-6B-shaped model under P-tuning v2 on the 32 x 1 U[512,2048] batch: client "
+        "embedding (130528 words) and block 0, 26 server blocks, client block 27, final linear layer and "
+        "next-token cross-entropy, forward and backward; 128 prefix rows per block, weights frozen, recompute",
+        num_prefix=128, frozen=True, vocab=130528),
 }
+
+
+def token_ids(batch: Batch, vocab: int, seed: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """Synthetic client tokens for the whole split model: ids uniform over the
+    vocabulary (stream 5), and next-token labels inside each sequence (the
+    last token of a sequence has none: -100)."""
+    ids = rng(seed, STREAM_TOKENS).integers(0, vocab, batch.total_tokens).astype(np.int32)
+    labels = np.full(batch.total_tokens, -100, np.int32)
+    for s in range(batch.num_seqs):
+        r0, r1 = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+        labels[r0:r1 - 1] = ids[r0 + 1:r1]
+    return ids, labels

@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 import synth
-from tests.gpu_helpers import rel_l2
+from tests.gpu_helpers import dev, rel_l2
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -276,4 +276,103 @@ def test_average_full_stack_sampled():
     assert np.all(np.abs(out[0] - ref) <= bound)
     print(f"[fullsize] average of 4 x {n} parameters: sampled {idx.numel()} ok", flush=True)
     del reps, c16
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# The whole split model at the full block shape and ChatGLM-6B's vocabulary
+# ---------------------------------------------------------------------------
+
+WS = synth.WORKLOADS["chatglm6b_28blk_split_ptuning128_ragged_32x1_recompute"]
+
+
+def test_split_model_full_shape_ptuning(layers2):
+    """Client embedding (130528 words) + block 0, one server block, client
+    block N-1, final linear layer and cross-entropy, P-tuning v2 (128 prefix
+    rows, weights frozen), on a two-client ragged batch: loss, the tensors
+    crossing both split boundaries, every prefix gradient, against the
+    float64 oracle."""
+    from oracle import client as oc
+    from paper_2406_14898_amd import BatchDesc, SplitModel
+    b = synth.Batch(np.array([0, 100, 357], np.int32), np.array([0, 1, 2], np.int32))
+    T, H, V = b.total_tokens, ONE.hidden, WS.vocab
+    lays = [_with_prefix(layers2[l % 2], l) for l in range(3)]
+    g = np.random.default_rng(5)
+    emb = synth.bf16_round(g.standard_normal((V, H), dtype=np.float32))
+    head = synth.bf16_round(g.standard_normal((V, H), dtype=np.float32) * np.float32(0.02))
+    ids, labels = synth.token_ids(b, V, seed=5)
+    scale = 1.0 / int((labels >= 0).sum())
+    m = SplitModel(H, ONE.num_heads, ONE.ffn_hidden, ONE.rotary_dim, 1, V, "bf16", ONE.rope_base, ONE.ln_eps, NP)
+    bd = BatchDesc.from_batch(b)
+    buf = m.buffers(bd, recompute=True)
+    dl = [{k: dev(v, "bf16") for k, v in lp.items()} for lp in lays]
+    params = {"embedding": dev(emb, "bf16"), "lm_head": dev(head, "bf16"), "block0": dl[0], "server": [dl[1]],
+              "block_last": dl[2]}
+    gz = [{k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in d.items()
+           if k.startswith("prefix_")} for d in dl]
+    grads = {"block0": gz[0], "server": [gz[1]], "block_last": gz[2]}
+    m.step(bd, ids, labels, params, grads, scale, buf, recompute=True)
+    torch.cuda.synchronize()
+    got = {k: buf[k].float().cpu().numpy() for k in ("h0", "hs", "d_hs", "d_h0", "loss_tok")}
+    got["loss_sum"] = float(buf["loss_sum"].item())
+    gg = [{k: v.cpu().numpy() for k, v in d.items()} for d in gz]
+    m.close()
+    del buf, params
+    client = {"embedding": emb, "block0": lays[0], "block_last": lays[2], "lm_head": head}
+    t = time.time()
+    ref = oc.split_step(client, [lays[1]], ids, labels, b, ONE, scale, train_weights=False)
+    errs = {"h0": rel_l2(got["h0"], ref["h0"]), "h_server": rel_l2(got["hs"], ref["h_server"]),
+            "d_h_server": rel_l2(got["d_hs"], ref["d_h_server"]), "d_h0": rel_l2(got["d_h0"], ref["d_h0"]),
+            "loss_tok": rel_l2(got["loss_tok"], ref["loss_tok"]),
+            "loss_sum": abs(got["loss_sum"] - ref["loss_sum"]) / abs(ref["loss_sum"])}
+    for i, key in enumerate(("grads_block0", None, "grads_block_last")):
+        r = ref[key] if key else ref["grads_server"][0]
+        for k in ("prefix_k", "prefix_v"):
+            errs[f"{i}.{k}"] = rel_l2(gg[i][k], r[k])
+    print(f"[fullsize] split model, oracle {time.time() - t:.0f}s: {errs}", flush=True)
+    assert all(v < TOL for v in errs.values()), errs
+
+
+def test_lm_head_bench_shape_sampled():
+    """The final linear layer and loss at the benchmark's shape (41447 tokens,
+    130528 words, hidden 4096) with the weight gradient: sampled tokens'
+    losses and input-gradient rows against the oracle token by token, the
+    loss sum against the per-token losses, and the weight gradient's
+    property that each token's softmax-minus-one-hot row sums to zero, so
+    sum_v dW[v] = 0 up to the bf16 rounding of the logit gradients."""
+    from oracle import client as oc
+    from paper_2406_14898_amd import ClientHead
+    b = WS.batch()
+    T, H, V = b.total_tokens, ONE.hidden, WS.vocab
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    h = torch.randn((T, H), generator=gen, device="cuda").to(torch.bfloat16)
+    w = (torch.randn((V, H), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
+    ids, labels = synth.token_ids(b, V, seed=3)
+    n_lab = int((labels >= 0).sum())
+    ch = ClientHead(V, H, "bf16")
+    ws = ch.workspace(T)
+    lt = torch.empty(T, device="cuda")
+    ls = torch.empty(1, device="cuda")
+    ch.head_forward(h, w, labels, lt, ls, ws)
+    dh = torch.empty_like(h)
+    dw = torch.zeros((V, H), device="cuda")
+    ch.head_backward(h, w, T, 1.0 / n_lab, dh, dw, ws)
+    torch.cuda.synchronize()
+    sample = np.unique(np.concatenate([np.random.default_rng(4).integers(0, T, 12), [0, T - 1]]))
+    sample = sample[labels[sample] >= 0][:10]
+    wh = w.float().cpu().numpy()
+    hs = h[torch.from_numpy(sample).cuda()].float().cpu().numpy()
+    lg, lse, lo, _ = oc.lm_head_forward(hs, wh, labels[sample])
+    dho, _ = oc.lm_head_backward(hs, wh, lg, lse, labels[sample], 1.0 / n_lab)
+    lt_h = lt.cpu().numpy()
+    assert rel_l2(lt_h[sample], lo) < TOL
+    assert rel_l2(dh[torch.from_numpy(sample).cuda()].float().cpu().numpy(), dho) < TOL
+    assert abs(float(ls.item()) - float(lt_h.astype(np.float64).sum())) <= 1e-5 * abs(float(ls.item()))
+    col = dw.sum(dim=0, dtype=torch.float64).cpu().numpy()
+    scale_ref = float(torch.linalg.vector_norm(dw, dtype=torch.float64).item()) / np.sqrt(H)
+    print(f"[fullsize] lm head T={T} V={V}: sum_v dW rms {np.sqrt(np.mean(col ** 2)):.2e} "
+          f"vs column norm {scale_ref:.2e}", flush=True)
+    assert np.sqrt(np.mean(col ** 2)) < 2e-2 * scale_ref
+    ch.close()
+    del ws, h, w, dw
     torch.cuda.empty_cache()
