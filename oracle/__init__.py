@@ -33,7 +33,7 @@ online softmax.
 
 from .block import (  # noqa: F401
     layer_norm, layer_norm_backward, gelu, gelu_grad, positions, rope_tables,
-    rope, allowed_mask, attention_forward, attention_backward, block_forward,
+    rope, glm_positions, allowed_mask, attention_forward, attention_backward, block_forward,
     block_backward, stack_forward, stack_backward, zero_grads, zero_prefix_grads, client_token_ranges,
     pack_clients, unpack_clients,
 )

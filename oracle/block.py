@@ -92,6 +92,30 @@ def positions(cu_seqlens: np.ndarray) -> np.ndarray:
     return pos
 
 
+def glm_positions(batch):
+    """GLM 2-D positions of every packed row (ChatGLM-6B's blank infilling,
+    which the paper's base model uses; not given in the paper).  Sequence s
+    has a context of P_s tokens (the prefix-LM prefix; the whole sequence
+    when the batch is causal) ending with the [gMASK] token at M_s =
+    max(P_s - 1, 0).  The first position counts context tokens and stays at
+    M_s after the context: p1 = t for t < P_s, else M_s.  The second
+    (block) position is 0 in the context and counts the generated span from
+    1: p2 = 0 for t < P_s, else t - P_s + 1."""
+    cu = batch.cu_seqlens
+    T = int(cu[-1])
+    p1 = np.zeros(T, np.int64)
+    p2 = np.zeros(T, np.int64)
+    for s in range(len(cu) - 1):
+        r0, r1 = int(cu[s]), int(cu[s + 1])
+        L = r1 - r0
+        P = int(batch.prefix_len[s]) if getattr(batch, "mask", "causal") == "prefix" else L
+        M = max(P - 1, 0)
+        for t in range(L):
+            p1[r0 + t] = t if t < P else M
+            p2[r0 + t] = 0 if t < P else t - P + 1
+    return p1, p2
+
+
 # ----------------------------------------------------------------------------
 # LayerNorm (pre-LN reading; biased variance, eps inside the square root)
 # ----------------------------------------------------------------------------
@@ -275,12 +299,26 @@ def _cast(p: Dict[str, np.ndarray], dtype) -> Dict[str, np.ndarray]:
     return {k: np.asarray(v, dtype=dtype) for k, v in p.items()}
 
 
+def _rotate_qk(x: np.ndarray, tables, shape, inverse: bool = False) -> np.ndarray:
+    """The block's rotary encoding of q or k [T, n_h, d]: dims [0, r) by the
+    first table; with GLM 2-D positions also dims [r, 2r) by the second."""
+    r = shape.rotary_dim
+    out = rope(x, tables[0], tables[1], r, inverse)
+    if len(tables) == 4:
+        out[:, :, r:2 * r] = rope(x[:, :, r:2 * r], tables[2], tables[3], r, inverse)
+    return out
+
+
 def block_forward(p: Dict[str, np.ndarray], x: np.ndarray, batch, shape, dtype=np.float64):
     """One pre-LN block:
         u = LN1(x);  qkv = u W_qkv^T + b_qkv;  q, k rotated (first half of each head)
         h = x + attn(q, k, v) W_o^T + b_o
         w = LN2(h);  z = w W_1^T + b_1;  g = gelu(z)
         y = h + g W_2^T + b_2
+    ChatGLM-6B's variant (shape.residual_alpha = alpha > 0) feeds the
+    normalised input forward instead: h = alpha u + attn(...) W_o^T + b_o and
+    y = alpha w + g W_2^T + b_2.  With shape.rotary_2d the second half of each
+    head is rotated too, by the GLM block position (``glm_positions``).
     Returns (y, cache) with everything the backward uses."""
     p = _cast(p, dtype)
     x = np.asarray(x, dtype=dtype)
@@ -288,28 +326,33 @@ def block_forward(p: Dict[str, np.ndarray], x: np.ndarray, batch, shape, dtype=n
     nh = shape.num_heads
     d = H // nh
     eps = shape.ln_eps
-    pos = positions(batch.cu_seqlens)
-    cos, sin = rope_tables(pos, shape.rotary_dim, shape.rope_base, dtype)
+    alpha = float(getattr(shape, "residual_alpha", 0.0))
+    if getattr(shape, "rotary_2d", False):
+        p1, p2 = glm_positions(batch)
+        tables = rope_tables(p1, shape.rotary_dim, shape.rope_base, dtype) + \
+            rope_tables(p2, shape.rotary_dim, shape.rope_base, dtype)
+    else:
+        tables = rope_tables(positions(batch.cu_seqlens), shape.rotary_dim, shape.rope_base, dtype)
 
     u, xhat1, rstd1 = layer_norm(x, p["ln1_g"], p["ln1_b"], eps)
     qkv = u @ p["w_qkv"].T + p["b_qkv"]
     q = qkv[:, 0:H].reshape(T, nh, d)
     k = qkv[:, H:2 * H].reshape(T, nh, d)
     v = qkv[:, 2 * H:3 * H].reshape(T, nh, d)
-    qr = rope(q, cos, sin, shape.rotary_dim)
-    kr = rope(k, cos, sin, shape.rotary_dim)
+    qr = _rotate_qk(q, tables, shape)
+    kr = _rotate_qk(k, tables, shape)
     # P-tuning v2 prefix (Appendix A): learned keys / values [L_p, H] spliced
     # in front of every sequence's own; they carry no position, so they are
     # not rotated
     pk, pv = _prefix_kv(p, nh, d)
     o = attention_forward(qr, kr, v, batch, pk, pv).reshape(T, H)
-    h = x + o @ p["w_o"].T + p["b_o"]
+    h = (alpha * u if alpha else x) + o @ p["w_o"].T + p["b_o"]
     w, xhat2, rstd2 = layer_norm(h, p["ln2_g"], p["ln2_b"], eps)
     z = w @ p["w_1"].T + p["b_1"]
     g = gelu(z)
-    y = h + g @ p["w_2"].T + p["b_2"]
+    y = (alpha * w if alpha else h) + g @ p["w_2"].T + p["b_2"]
     cache = dict(x=x, u=u, xhat1=xhat1, rstd1=rstd1, qr=qr, kr=kr, v=v, o=o, h=h,
-                 w=w, xhat2=xhat2, rstd2=rstd2, z=z, g=g, cos=cos, sin=sin, pk=pk, pv=pv)
+                 w=w, xhat2=xhat2, rstd2=rstd2, z=z, g=g, tables=tables, pk=pk, pv=pv)
     return y, cache
 
 
@@ -347,8 +390,9 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     nh = shape.num_heads
     d = H // nh
     grads = _Sink(grads)
+    alpha = float(getattr(shape, "residual_alpha", 0.0))
 
-    # y = h + g W_2^T + b_2
+    # y = h + g W_2^T + b_2   (ChatGLM-6B: y = alpha w + g W_2^T + b_2)
     grads["w_2"] += dy.T @ c["g"]
     grads["b_2"] += dy.sum(axis=0)
     dg = dy @ p["w_2"]
@@ -357,11 +401,13 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     grads["w_1"] += dz.T @ c["w"]
     grads["b_1"] += dz.sum(axis=0)
     dw = dz @ p["w_1"]
-    # w = LN2(h); h also feeds y directly
+    if alpha:
+        dw = dw + alpha * dy
+    # w = LN2(h); h also feeds y directly (plain residual)
     dh_ln, dg2, db2 = layer_norm_backward(dw, c["xhat2"], c["rstd2"], p["ln2_g"])
     grads["ln2_g"] += dg2
     grads["ln2_b"] += db2
-    dh = dy + dh_ln
+    dh = dh_ln if alpha else dy + dh_ln
     # h = x + o W_o^T + b_o
     grads["w_o"] += dh.T @ c["o"]
     grads["b_o"] += dh.sum(axis=0)
@@ -372,18 +418,20 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
         dqr, dkr, dv, dpk, dpv = attention_backward(c["qr"], c["kr"], c["v"], do, batch, c["pk"], c["pv"])
         grads["prefix_k"] += dpk.reshape(-1, H)
         grads["prefix_v"] += dpv.reshape(-1, H)
-    dq = rope(dqr, c["cos"], c["sin"], shape.rotary_dim, inverse=True)
-    dk = rope(dkr, c["cos"], c["sin"], shape.rotary_dim, inverse=True)
+    dq = _rotate_qk(dqr, c["tables"], shape, inverse=True)
+    dk = _rotate_qk(dkr, c["tables"], shape, inverse=True)
     dqkv = np.concatenate([dq.reshape(T, H), dk.reshape(T, H), dv.reshape(T, H)], axis=1)
     # qkv = u W_qkv^T + b_qkv
     grads["w_qkv"] += dqkv.T @ c["u"]
     grads["b_qkv"] += dqkv.sum(axis=0)
     du = dqkv @ p["w_qkv"]
-    # u = LN1(x); x also feeds h directly
+    if alpha:
+        du = du + alpha * dh
+    # u = LN1(x); x also feeds h directly (plain residual)
     dx_ln, dg1, db1 = layer_norm_backward(du, c["xhat1"], c["rstd1"], p["ln1_g"])
     grads["ln1_g"] += dg1
     grads["ln1_b"] += db1
-    return dh + dx_ln
+    return dx_ln if alpha else dh + dx_ln
 
 
 class _Sink:

@@ -11,10 +11,11 @@ next-token labels y.  The backward runs the same chain in reverse: the client
 returns dL/dh_{N-2} to the server and receives dL/dh_0.
 
 Readings: the final linear layer maps hidden to vocabulary logits with no
-bias and no final normalisation (the paper's formula applies Linear directly
-to Block_{N-1}'s output); the loss is the sum over labelled tokens of
-log-sum-exp(logits) - logit[label], a negative label marking a token
-without a target; the gradient of the loss is scaled by a caller-chosen
+bias and, by default, no final normalisation (the paper's formula applies
+Linear directly to Block_{N-1}'s output; ChatGLM-6B's final LayerNorm in
+front of it is optional: "final_ln_g" / "final_ln_b" in the client dict);
+the loss is the sum over labelled tokens of log-sum-exp(logits) -
+logit[label], a negative label marking a token without a target; the gradient of the loss is scaled by a caller-chosen
 factor (1 / number of labelled tokens gives the mean).
 """
 
@@ -24,7 +25,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from .block import stack_backward, stack_forward
+from .block import layer_norm, layer_norm_backward, stack_backward, stack_forward
 
 
 def embedding_forward(table: np.ndarray, ids: np.ndarray, dtype=np.float64) -> np.ndarray:
@@ -97,8 +98,15 @@ def split_step(client: Dict, server_layers: Sequence[Dict], ids: np.ndarray, lab
     h0, xs0 = stack_forward([client["block0"]], 1, e, batch, shape, dtype=dtype)
     hs, xss = stack_forward(server_layers, n_srv, h0, batch, shape, dtype=dtype)
     hl, xsl = stack_forward([client["block_last"]], 1, hs, batch, shape, dtype=dtype)
-    logits, lse, loss_tok, loss_sum = lm_head_forward(hl, client["lm_head"], labels, dtype)
-    dhl, dw_head = lm_head_backward(hl, client["lm_head"], logits, lse, labels, grad_scale, dtype)
+    final_ln = "final_ln_g" in client
+    hn = hl
+    if final_ln:
+        hn, xhat, rstd = layer_norm(hl, np.asarray(client["final_ln_g"], dtype),
+                                    np.asarray(client["final_ln_b"], dtype), shape.ln_eps)
+    logits, lse, loss_tok, loss_sum = lm_head_forward(hn, client["lm_head"], labels, dtype)
+    dhl, dw_head = lm_head_backward(hn, client["lm_head"], logits, lse, labels, grad_scale, dtype)
+    if final_ln:
+        dhl, dg_ln, db_ln = layer_norm_backward(dhl, xhat, rstd, np.asarray(client["final_ln_g"], dtype))
     dhs, g_last = stack_backward([client["block_last"]], 1, xsl, dhl, batch, shape,
                                  grads_for([client["block_last"]]), dtype=dtype)
     dh0, g_srv = stack_backward(server_layers, n_srv, xss, dhs, batch, shape, grads_for(server_layers[:n_srv]),
@@ -110,5 +118,7 @@ def split_step(client: Dict, server_layers: Sequence[Dict], ids: np.ndarray, lab
            "grads_block_last": g_last[0], "grads_server": g_srv, "grads_block0": g_0[0]}
     if train_weights:
         out["grad_lm_head"] = dw_head
+        if final_ln:
+            out["grad_final_ln_g"], out["grad_final_ln_b"] = dg_ln, db_ln
         out["grad_embedding"] = embedding_backward(ids, de, client["embedding"].shape[0], dtype)
     return out

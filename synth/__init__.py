@@ -89,6 +89,8 @@ class StackShape:
     rotary_dim: int          # rotated leading dims of each head (half the head dim)
     rope_base: float = 10000.0
     ln_eps: float = 1e-5
+    residual_alpha: float = 0.0   # > 0: ChatGLM-6B residual alpha * LN(x) + f(LN(x)); 0: x + f(LN(x))
+    rotary_2d: bool = False       # GLM 2-D positions: second half of each head rotated by block position
 
     @property
     def head_dim(self) -> int:

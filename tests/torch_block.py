@@ -35,10 +35,26 @@ def _rotate(x: torch.Tensor, pos: torch.Tensor, r: int, base: float) -> torch.Te
     return torch.cat([z.real, z.imag, x[..., r:]], dim=-1)
 
 
+def _glm_pos(L: int, P: int):
+    """GLM 2-D positions of one sequence with a P-token context: the first
+    counter freezes at the [gMASK] position after the context, the second
+    counts the span after it (vectorised, independent of the oracle)."""
+    t = torch.arange(L)
+    m = max(P - 1, 0)
+    p1 = torch.where(t < P, t, torch.full_like(t, m))
+    p2 = torch.clamp(t - P + 1, min=0)
+    return p1, p2
+
+
 def block(p, x, cu_seqlens, prefix_len, shape):
     """One block; with "prefix_k" / "prefix_v" in p ([L_p, H], not rotated)
     the P-tuning v2 prefix is concatenated in front of every sequence's keys
-    and values and is visible to every query."""
+    and values and is visible to every query.  shape.residual_alpha > 0:
+    ChatGLM-6B's residual on the normalised input; shape.rotary_2d: the
+    second half of every head rotated by the GLM block position."""
+    alpha = float(getattr(shape, "residual_alpha", 0.0))
+    two_d = bool(getattr(shape, "rotary_2d", False))
+    r = shape.rotary_dim
     T, H = x.shape
     nh = shape.num_heads
     d = H // nh
@@ -49,11 +65,19 @@ def block(p, x, cu_seqlens, prefix_len, shape):
     for s in range(len(cu_seqlens) - 1):
         r0, r1 = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
         L = r1 - r0
-        pos = torch.arange(L)
-        qs = _rotate(q[r0:r1].reshape(L, nh, d), pos, shape.rotary_dim, shape.rope_base)
-        ks = _rotate(k[r0:r1].reshape(L, nh, d), pos, shape.rotary_dim, shape.rope_base)
-        vs = v[r0:r1].reshape(L, nh, d)
         pre = None if prefix_len is None else int(prefix_len[s])
+        qs, ks = q[r0:r1].reshape(L, nh, d), k[r0:r1].reshape(L, nh, d)
+        if two_d:
+            p1, p2 = _glm_pos(L, L if pre is None else pre)
+            qs = torch.cat([_rotate(qs[..., :r], p1, r, shape.rope_base),
+                            _rotate(qs[..., r:], p2, r, shape.rope_base)], dim=-1)
+            ks = torch.cat([_rotate(ks[..., :r], p1, r, shape.rope_base),
+                            _rotate(ks[..., r:], p2, r, shape.rope_base)], dim=-1)
+        else:
+            pos = torch.arange(L)
+            qs = _rotate(qs, pos, r, shape.rope_base)
+            ks = _rotate(ks, pos, r, shape.rope_base)
+        vs = v[r0:r1].reshape(L, nh, d)
         mask = _mask(L, pre)
         if "prefix_k" in p:
             Lp = p["prefix_k"].shape[0]
@@ -64,10 +88,10 @@ def block(p, x, cu_seqlens, prefix_len, shape):
                                            attn_mask=mask)
         outs.append(o.transpose(0, 1).reshape(L, H))
     o = torch.cat(outs, dim=0)
-    h = x + F.linear(o, p["w_o"], p["b_o"])
+    h = (alpha * u if alpha else x) + F.linear(o, p["w_o"], p["b_o"])
     w = F.layer_norm(h, (H,), p["ln2_g"], p["ln2_b"], shape.ln_eps)
     g = F.gelu(F.linear(w, p["w_1"], p["b_1"]), approximate="tanh")
-    return h + F.linear(g, p["w_2"], p["b_2"])
+    return (alpha * w if alpha else h) + F.linear(g, p["w_2"], p["b_2"])
 
 
 def stack_fwd_bwd(layers, x, dy, batch, shape):
