@@ -76,7 +76,19 @@ extern "C" {
  * v2): every block has num_prefix learned key and value rows ([L_p, H],
  * head h at columns h*d, not rotated) spliced in front of each sequence's
  * own keys and values, K' = [prefix_key; key], V' = [prefix_value; value],
- * and visible to every query of every sequence.  bf16 only; at most 4096. */
+ * and visible to every query of every sequence.  bf16 only; at most 4096.
+ *
+ * ChatGLM-6B's own block (the paper's base model; these details are
+ * ChatGLM-6B's, not the paper's), for loading its weights:
+ *   residual_alpha > 0: the residual carries the normalised input scaled by
+ *     alpha (ChatGLM-6B: sqrt(2 * 28)): h = alpha u + Attn(...) W_o^T + b_o,
+ *     y = alpha w + gelu(...) W_2^T + b_2; 0 = the plain x + f(LN(x)).
+ *   rotary_2d = 1: GLM 2-D positions (needs rotary_dim = head dim / 2).  A
+ *     sequence's context is its prefix-LM prefix (the whole sequence in a
+ *     causal batch) ending with the [gMASK] token at M = max(P - 1, 0);
+ *     dims [0, r) of each head are rotated by p1 = t in the context, M after
+ *     it, and dims [r, 2r) by the block position p2 = 0 in the context,
+ *     t - P + 1 after it. */
 typedef struct fl_stack_desc {
   int32_t num_layers;   /* N server blocks (26 for ChatGLM-6B's server part) */
   int32_t hidden;       /* H */
@@ -87,6 +99,8 @@ typedef struct fl_stack_desc {
   float ln_eps;         /* 1e-5 */
   int32_t dtype;        /* FL_BF16 or FL_F32 */
   int32_t num_prefix;   /* L_p, P-tuning v2 prefix length; 0 = no prefix */
+  float residual_alpha; /* 0: plain residual; > 0: ChatGLM-6B's alpha-scaled residual */
+  int32_t rotary_2d;    /* 0: 1-D positions; 1: GLM 2-D positions */
 } fl_stack_desc;
 
 /* A packed batch of clients (host arrays).  Sequence s covers packed rows
@@ -201,6 +215,7 @@ typedef struct {
   int64_t vocab;   /* multiple of 8, <= 2^24 (ChatGLM-6B: 130528) */
   int32_t hidden;  /* multiple of 256, <= 16384 */
   int32_t dtype;   /* FL_BF16 | FL_F32: element type of tables, weights, activations */
+  float ln_eps;    /* eps of the optional final LayerNorm (> 0 when one is used; ChatGLM-6B: 1e-5) */
 } fl_client_desc;
 
 /* FL_ERR_SHAPE for an unsupported descriptor. */
@@ -222,22 +237,30 @@ int fl_embedding_forward(fl_client* client, const void* table, const int32_t* id
 int fl_embedding_backward(fl_client* client, const int32_t* ids, int64_t T, const void* dout, float* dtable,
                           void* workspace, size_t workspace_bytes, void* stream);
 
-/* y' = h W^T and the cross-entropy: for every token t with labels[t] >= 0
- * (host [T]; a negative label marks a token without target; labels >= vocab
- * give FL_ERR_ARG), loss_tok[t] = logsumexp(y'_t) - y'_t[labels[t]], else 0;
- * loss_sum = the sum of loss_tok in a fixed order.  h [T, hidden], W
- * [vocab, hidden] device; loss_tok [T] and loss_sum [1] device fp32.  The
- * logits and log-sum-exp stay in the workspace for fl_lm_head_backward. */
-int fl_lm_head_forward(fl_client* client, const void* h, const void* w, const int32_t* labels, int64_t T,
-                       float* loss_tok, float* loss_sum, void* workspace, size_t workspace_bytes, void* stream);
+/* y' = LN(h) W^T and the cross-entropy: for every token t with labels[t]
+ * >= 0 (host [T]; a negative label marks a token without target; labels >=
+ * vocab give FL_ERR_ARG), loss_tok[t] = logsumexp(y'_t) - y'_t[labels[t]],
+ * else 0; loss_sum = the sum of loss_tok in a fixed order.  h [T, hidden],
+ * W [vocab, hidden] device; loss_tok [T] and loss_sum [1] device fp32.
+ * ln_g / ln_b [hidden] (device, both or neither): ChatGLM-6B's final
+ * LayerNorm (eps = the descriptor's ln_eps, hidden <= 4096); NULL = no
+ * normalisation, the paper's y' = Linear(Block_{N-1}(h_{N-2})).  The
+ * logits, log-sum-exp and normalised input stay in the workspace for
+ * fl_lm_head_backward. */
+int fl_lm_head_forward(fl_client* client, const void* h, const void* ln_g, const void* ln_b, const void* w,
+                       const int32_t* labels, int64_t T, float* loss_tok, float* loss_sum, void* workspace,
+                       size_t workspace_bytes, void* stream);
 /* Backward of grad_scale * loss_sum (grad_scale = 1 / labelled tokens gives
  * the mean): dlogits = grad_scale (softmax - onehot) on labelled tokens, 0
  * on the others (computed in place in the workspace, which must still hold
  * the forward's logits: same T, no other head call in between); dh [T,
- * hidden] = dlogits W; dw [vocab, hidden] fp32 += dlogits^T h, or NULL when
- * the weight is frozen (P-tuning v2). */
-int fl_lm_head_backward(fl_client* client, const void* h, const void* w, int64_t T, float grad_scale, void* dh,
-                        float* dw, void* workspace, size_t workspace_bytes, void* stream);
+ * hidden] = dlogits W, taken back through the final LayerNorm when ln_g is
+ * given (the same ln_g as the forward); dln_g / dln_b fp32 [hidden] +=
+ * its gain / shift gradients (NULL: frozen); dw [vocab, hidden] fp32 +=
+ * dlogits^T LN(h), or NULL when the weight is frozen (P-tuning v2). */
+int fl_lm_head_backward(fl_client* client, const void* h, const void* ln_g, const void* w, int64_t T,
+                        float grad_scale, void* dh, float* dln_g, float* dln_b, float* dw, void* workspace,
+                        size_t workspace_bytes, void* stream);
 
 /* Server update (Section 4.1.4, Parameter Settings: Adam, learning rate
  * 2e-2, batch size 1, no warmup, no weight decay).  One step of Algorithm 1

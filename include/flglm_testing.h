@@ -28,9 +28,11 @@ extern "C" {
 #define FL_EPI_BIAS_GELU 3 /* C = z = acc + bias[n]; C2 = gelu_tanh(z)  */
 #define FL_EPI_GELU_BWD 4  /* C = acc * gelu_tanh'(Z[m*ldz+n])          */
 #define FL_EPI_ACC_F32 5   /* C (fp32) += acc                           */
+#define FL_EPI_RES 6       /* C = acc + res_scale * R[m*ldr+n]          */
 
 /* Matrix-core GEMM as used by the linear layers.  Supported pairs: NT with
- * STORE/BIAS/BIAS_RES/BIAS_GELU, NN with STORE/GELU_BWD, TN with ACC_F32.
+ * STORE/BIAS/BIAS_RES/BIAS_GELU, NN with STORE/GELU_BWD/RES, TN with ACC_F32.
+ * res_scale multiplies R in BIAS_RES and RES (1: plain residual).
  * part / part_bytes: optional device fp32 scratch (16-byte aligned) that
  * lets the bf16 kernel split the reduction of a last, partial round of
  * tiles over more compute units (NULL / 0: never split).
@@ -42,7 +44,7 @@ extern "C" {
 int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, void* C, int M, int N, int K,
                  int64_t lda, int64_t ldb, int64_t ldc, const void* bias, const void* R, int64_t ldr, void* C2,
                  int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, int b_rows,
-                 void* stream);
+                 float res_scale, void* stream);
 
 /* LayerNorm over rows of x [T, H] (H % 256 == 0, H <= 4096). */
 int fl_test_layernorm_fwd(int dtype, const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,

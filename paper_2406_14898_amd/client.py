@@ -13,10 +13,10 @@ from .stack import ServerStack
 class ClientHead:
     """Embedding layer and final linear layer + cross-entropy of the client."""
 
-    def __init__(self, vocab: int, hidden: int, dtype: str = "bf16"):
+    def __init__(self, vocab: int, hidden: int, dtype: str = "bf16", ln_eps: float = 1e-5):
         self.vocab, self.hidden = vocab, hidden
         self.dtype = F.FL_BF16 if dtype == "bf16" else F.FL_F32
-        self.handle = F.fl_client_create(vocab, hidden, self.dtype)
+        self.handle = F.fl_client_create(vocab, hidden, self.dtype, ln_eps)
 
     def close(self) -> None:
         if self.handle:
@@ -39,11 +39,13 @@ class ClientHead:
     def embed_backward(self, ids, dout, dtable, ws, stream=None) -> None:
         F.fl_embedding_backward(self.handle, ids, dout, dtable, ws, stream)
 
-    def head_forward(self, h, w, labels, loss_tok, loss_sum, ws, stream=None) -> None:
-        F.fl_lm_head_forward(self.handle, h, w, labels, loss_tok, loss_sum, ws, stream)
+    def head_forward(self, h, w, labels, loss_tok, loss_sum, ws, stream=None, ln_g=None, ln_b=None) -> None:
+        """ln_g / ln_b: the optional final LayerNorm (ChatGLM-6B)."""
+        F.fl_lm_head_forward(self.handle, h, w, labels, loss_tok, loss_sum, ws, stream, ln_g, ln_b)
 
-    def head_backward(self, h, w, T: int, grad_scale: float, dh, dw, ws, stream=None) -> None:
-        F.fl_lm_head_backward(self.handle, h, w, T, grad_scale, dh, dw, ws, stream)
+    def head_backward(self, h, w, T: int, grad_scale: float, dh, dw, ws, stream=None, ln_g=None, dln_g=None,
+                      dln_b=None) -> None:
+        F.fl_lm_head_backward(self.handle, h, w, T, grad_scale, dh, dw, ws, stream, ln_g, dln_g, dln_b)
 
 
 class SplitModel:
@@ -54,12 +56,17 @@ class SplitModel:
     client runs on its own share of the batch)."""
 
     def __init__(self, hidden: int, num_heads: int, ffn_hidden: int, rotary_dim: int, num_server: int, vocab: int,
-                 dtype: str = "bf16", rope_base: float = 10000.0, ln_eps: float = 1e-5, num_prefix: int = 0):
-        args = (hidden, num_heads, ffn_hidden, rotary_dim, dtype, rope_base, ln_eps, num_prefix)
+                 dtype: str = "bf16", rope_base: float = 10000.0, ln_eps: float = 1e-5, num_prefix: int = 0,
+                 residual_alpha: float = 0.0, rotary_2d: bool = False):
+        """residual_alpha / rotary_2d: ChatGLM-6B's own blocks; with them a
+        step also takes the final LayerNorm ("final_ln_g" / "final_ln_b" in
+        params) when given."""
+        args = (hidden, num_heads, ffn_hidden, rotary_dim, dtype, rope_base, ln_eps, num_prefix, residual_alpha,
+                rotary_2d)
         self.block0 = ServerStack(1, *args)
         self.server = ServerStack(num_server, *args)
         self.block_last = ServerStack(1, *args)
-        self.head = ClientHead(vocab, hidden, dtype)
+        self.head = ClientHead(vocab, hidden, dtype, ln_eps)
         self.hidden = hidden
 
     def close(self) -> None:
@@ -87,7 +94,8 @@ class SplitModel:
              recompute: bool = False, stream=None, marks: Optional[List] = None) -> None:
         """One training step.  params: "embedding" [V, H], "lm_head" [V, H],
         "block0" / "block_last" (one layer's dict), "server" (list of layer
-        dicts).  grads: the same keys with fp32 accumulators (+=); a missing
+        dicts), optionally "final_ln_g" / "final_ln_b" [H] (ChatGLM-6B's final
+        LayerNorm; their gradients in grads, None when frozen).  grads: the same keys with fp32 accumulators (+=); a missing
         or None "embedding" / "lm_head" entry, and block dicts without weight
         keys, mean frozen (P-tuning v2).  marks: when a list, each client-side
         call is bracketed by two timing events on the stream and appended as
@@ -112,10 +120,11 @@ class SplitModel:
                             recompute, stream)
         self.block_last.forward(batch, [params["block_last"]], buf["hs"], buf["hl"], buf["bl_saved"], buf["bl_ws"],
                                 recompute, stream)
+        lg, lb = params.get("final_ln_g"), params.get("final_ln_b")
         timed("lm_head_fwd", h.head_forward, buf["hl"], params["lm_head"], labels, buf["loss_tok"], buf["loss_sum"],
-              buf["client_ws"], stream)
+              buf["client_ws"], stream, lg, lb)
         timed("lm_head_bwd", h.head_backward, buf["hl"], params["lm_head"], T, grad_scale, buf["d_hl"],
-              grads.get("lm_head"), buf["client_ws"], stream)
+              grads.get("lm_head"), buf["client_ws"], stream, lg, grads.get("final_ln_g"), grads.get("final_ln_b"))
         self.block_last.backward(batch, [params["block_last"]], [grads["block_last"]], buf["hs"], buf["bl_saved"],
                                  buf["d_hl"], buf["d_hs"], buf["bl_ws"], recompute, stream)
         self.server.backward(batch, params["server"], grads["server"], buf["h0"], buf["srv_saved"], buf["d_hs"],

@@ -9,6 +9,10 @@
 // the tokens by id (counting sort, ties in token order) and the device adds
 // each id's rows in that order, with no atomics.
 //
+// An optional final LayerNorm (ChatGLM-6B's, not in the paper's formula) can
+// sit in front of the linear layer; its output, statistics and the gradient
+// arriving at it live in the workspace.
+//
 // The vocabulary is padded to a multiple of the 256-wide GEMM tile inside
 // the workspace: the logits buffer is [T, V_pad]; rows of the weight past V
 // are never read (the GEMM reads them as zero), and the padded columns take
@@ -70,6 +74,12 @@ struct ClientWs {
   int32_t* labels;  // [T]
   int32_t* ids;     // [T]
   int32_t* plan;    // order [T] | segment starts [T + 1] | segment ids [T]
+  char* hn;         // final LayerNorm output [T, H]
+  char* dhn;        // gradient at the final LayerNorm output [T, H]
+  float* mean;      // final LayerNorm statistics [T]
+  float* rstd;
+  float* ln_part;   // column-sum partials of the LayerNorm gain / shift gradients
+  float* ln_part2;
   float* part;      // GEMM split-reduction scratch
   size_t part_bytes;
   size_t total;
@@ -88,6 +98,14 @@ ClientWs carve(const fl_client* c, long T, char* base) {
   w.labels = (int32_t*)take((size_t)T * 4);
   w.ids = (int32_t*)take((size_t)T * 4);
   w.plan = (int32_t*)take((size_t)(3 * T + 1) * 4);
+  const size_t th = (size_t)T * c->d.hidden * c->E;
+  w.hn = take(th);
+  w.dhn = take(th);
+  w.mean = (float*)take((size_t)T * 4);
+  w.rstd = (float*)take((size_t)T * 4);
+  const size_t cp = (size_t)colsum_blocks((int)T) * c->d.hidden * 4;
+  w.ln_part = (float*)take(cp);
+  w.ln_part2 = (float*)take(cp);
   w.part_bytes = gemm_part_bytes();
   w.part = (float*)take(w.part_bytes);
   w.total = off;
@@ -279,6 +297,7 @@ int fl_client_create(const fl_client_desc* desc, fl_client** out) {
     return set_error(FL_ERR_SHAPE, "vocab must be a multiple of 8 in [8, 2^24]");
   if (desc->hidden < 256 || desc->hidden % 256 || desc->hidden > 16384)
     return set_error(FL_ERR_SHAPE, "hidden must be a multiple of 256 in [256, 16384]");
+  if (!(desc->ln_eps >= 0.f) || !std::isfinite(desc->ln_eps)) return set_error(FL_ERR_SHAPE, "ln_eps must be >= 0");
   fl_client* c = new fl_client;
   c->d = *desc;
   c->E = desc->dtype == FL_BF16 ? 2 : 4;
@@ -370,10 +389,22 @@ int fl_embedding_backward(fl_client* c, const int32_t* ids, int64_t T, const voi
   return herr(hipGetLastError());
 }
 
-int fl_lm_head_forward(fl_client* c, const void* h, const void* w_vocab, const int32_t* labels, int64_t T,
-                       float* loss_tok, float* loss_sum, void* workspace, size_t workspace_bytes, void* stream) {
+// The final LayerNorm's arguments: both or neither, hidden <= 4096, eps > 0.
+int check_final_ln(const fl_client* c, const void* g, const void* b) {
+  if (!g && !b) return FL_OK;
+  if (!g || !b) return set_error(FL_ERR_NULL, "final LayerNorm gain / shift: both or neither");
+  if (!al16(g) || !al16(b)) return set_error(FL_ERR_ALIGN, "final LayerNorm parameters not 16-byte aligned");
+  if (c->d.hidden > 4096) return set_error(FL_ERR_SHAPE, "the final LayerNorm supports hidden <= 4096");
+  if (!(c->d.ln_eps > 0.f)) return set_error(FL_ERR_SHAPE, "the final LayerNorm needs ln_eps > 0");
+  return FL_OK;
+}
+
+int fl_lm_head_forward(fl_client* c, const void* h, const void* ln_g, const void* ln_b, const void* w_vocab,
+                       const int32_t* labels, int64_t T, float* loss_tok, float* loss_sum, void* workspace,
+                       size_t workspace_bytes, void* stream) {
   if (int rc = check_common(c, T, workspace, workspace_bytes)) return rc;
   if (!h || !w_vocab || !labels || !loss_tok || !loss_sum) return set_error(FL_ERR_NULL, "NULL argument");
+  if (int rc = check_final_ln(c, ln_g, ln_b)) return rc;
   if (!al16(h) || !al16(w_vocab) || !al16(loss_tok) || ((uintptr_t)loss_sum & 3))
     return set_error(FL_ERR_ALIGN, "h / w / loss_tok not 16-byte aligned");
   if (overlap(loss_tok, T * 4, workspace, workspace_bytes) || overlap(loss_sum, 4, workspace, workspace_bytes) ||
@@ -385,8 +416,13 @@ int fl_lm_head_forward(fl_client* c, const void* h, const void* w_vocab, const i
   hipStream_t s = (hipStream_t)stream;
   if (int rc = upload(c, labels, (size_t)T * 4, w.labels, s)) return rc;
   const int H = c->d.hidden;
+  const void* hin = h;
+  if (ln_g) {
+    CK(layernorm_fwd(dt_of(c), h, ln_g, ln_b, w.hn, w.mean, w.rstd, (int)T, H, c->d.ln_eps, s));
+    hin = w.hn;
+  }
   GemmDesc g;
-  g.A = h; g.B = w_vocab; g.C = w.logits;
+  g.A = hin; g.B = w_vocab; g.C = w.logits;
   g.M = (int)T; g.N = (int)c->vpad; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = c->vpad;
   g.b_rows = (int)c->d.vocab;
@@ -403,10 +439,16 @@ int fl_lm_head_forward(fl_client* c, const void* h, const void* w_vocab, const i
   return herr(hipGetLastError());
 }
 
-int fl_lm_head_backward(fl_client* c, const void* h, const void* w_vocab, int64_t T, float grad_scale, void* dh,
-                        float* dw_vocab, void* workspace, size_t workspace_bytes, void* stream) {
+int fl_lm_head_backward(fl_client* c, const void* h, const void* ln_g, const void* w_vocab, int64_t T,
+                        float grad_scale, void* dh, float* dln_g, float* dln_b, float* dw_vocab, void* workspace,
+                        size_t workspace_bytes, void* stream) {
   if (int rc = check_common(c, T, workspace, workspace_bytes)) return rc;
   if (!h || !w_vocab || !dh) return set_error(FL_ERR_NULL, "h / w / dh is NULL");
+  if (ln_g && (!al16(ln_g) || c->d.hidden > 4096 || !(c->d.ln_eps > 0.f)))
+    return set_error(FL_ERR_ARG, "final LayerNorm gain misaligned, or hidden / ln_eps unsupported");
+  if (!ln_g && (dln_g || dln_b)) return set_error(FL_ERR_ARG, "LayerNorm gradients without a final LayerNorm");
+  if ((dln_g == nullptr) != (dln_b == nullptr)) return set_error(FL_ERR_NULL, "dln_g / dln_b: both or neither");
+  if ((dln_g && !al16(dln_g)) || (dln_b && !al16(dln_b))) return set_error(FL_ERR_ALIGN, "dln not aligned");
   if (!al16(h) || !al16(w_vocab) || !al16(dh) || (dw_vocab && !al16(dw_vocab)))
     return set_error(FL_ERR_ALIGN, "h / w / dh / dw not 16-byte aligned");
   if (!std::isfinite(grad_scale)) return set_error(FL_ERR_ARG, "grad_scale is not finite");
@@ -425,18 +467,29 @@ int fl_lm_head_backward(fl_client* c, const void* h, const void* w_vocab, int64_
     hipLaunchKernelGGL(ce_bwd_kernel<float>, dim3((unsigned)T), dim3(kThreads), 0, s, (float*)w.logits, c->vpad,
                        (int)V, w.labels, w.lse, grad_scale);
   CK(hipGetLastError());
-  // dh = dlogits W   (reduction over the padded vocabulary; W's rows past V read as zero)
+  // dh = dlogits W   (reduction over the padded vocabulary; W's rows past V
+  // read as zero); with the final LayerNorm this is the gradient at its output
   GemmDesc g;
-  g.A = w.logits; g.B = w_vocab; g.C = dh;
+  g.A = w.logits; g.B = w_vocab; g.C = ln_g ? (void*)w.dhn : dh;
   g.M = (int)T; g.N = (int)H; g.K = (int)c->vpad;
   g.lda = c->vpad; g.ldb = H; g.ldc = H;
   g.b_rows = (int)V;
   g.part = w.part; g.part_bytes = w.part_bytes;
   CK(gemm(dt_of(c), GEMM_NN, EPI_STORE, g, s));
+  if (ln_g) {
+    CK(layernorm_bwd_dx(dt_of(c), w.dhn, h, w.mean, w.rstd, ln_g, nullptr, dh, (int)T, (int)H, s));
+    if (dln_g) {
+      const int nb = colsum_blocks((int)T);
+      CK(colsum_partial(dt_of(c), 1, w.dhn, H, h, w.mean, w.rstd, (int)T, (int)H, w.ln_part, w.ln_part2, s));
+      CK(colsum_finish(w.ln_part, nb, (int)H, dln_g, s));
+      CK(colsum_finish(w.ln_part2, nb, (int)H, dln_b, s));
+    }
+  }
   if (!dw_vocab) return FL_OK;
-  // dW += dlogits^T h   (rows m < V of the padded logits' columns)
+  // dW += dlogits^T hn   (rows m < V of the padded logits' columns; hn = h
+  // without the final LayerNorm)
   GemmDesc gw;
-  gw.A = w.logits; gw.B = h; gw.C = dw_vocab;
+  gw.A = w.logits; gw.B = ln_g ? (const void*)w.hn : h; gw.C = dw_vocab;
   gw.M = (int)V; gw.N = (int)H; gw.K = (int)T;
   gw.lda = c->vpad; gw.ldb = H; gw.ldc = H;
   gw.part = w.part; gw.part_bytes = w.part_bytes;

@@ -22,6 +22,27 @@ hipError_t seq_positions(const int32_t* cu, int S, int32_t* pos, hipStream_t st)
   return hipGetLastError();
 }
 
+// GLM 2-D positions: with a context of P tokens (ctx[s], or the whole
+// sequence), p1 = t inside the context and the [gMASK] position max(P-1, 0)
+// after it; p2 = 0 inside the context and t - P + 1 after it.
+__global__ void seq_positions_2d_kernel(const int32_t* cu, const int32_t* ctx, int32_t* p1, int32_t* p2) {
+  const int s = blockIdx.x;
+  const int r0 = cu[s], r1 = cu[s + 1];
+  const int P = ctx ? ctx[s] : r1 - r0;
+  const int m = P > 0 ? P - 1 : 0;
+  for (int r = r0 + (int)threadIdx.x; r < r1; r += blockDim.x) {
+    const int t = r - r0;
+    p1[r] = t < P ? t : m;
+    p2[r] = t < P ? 0 : t - P + 1;
+  }
+}
+
+hipError_t seq_positions_2d(const int32_t* cu, const int32_t* ctx, int S, int32_t* p1, int32_t* p2, hipStream_t st) {
+  if (S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(seq_positions_2d_kernel, dim3(S), dim3(256), 0, st, cu, ctx, p1, p2);
+  return hipGetLastError();
+}
+
 __global__ void rope_table_kernel(float* ct, float* stbl, int max_pos, int r, double base) {
   const int half = r / 2;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -44,7 +65,7 @@ hipError_t rope_table(float* ct, float* stbl, int max_pos, int r, float base, hi
 // One thread rotates 4 pairs (i, i + r/2), i..i+3, of one head of q or k.
 template <typename T>
 __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
-                               int H, int d, int r) {
+                               int H, int d, int r, float sign) {
   const int half = r / 2, groups = half / 4;
   const int nh = H / d;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -65,9 +86,9 @@ __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float*
   float ya[4], yb[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const float x1 = a.get(e), x2 = b.get(e);
-    ya[e] = x1 * c[e] - x2 * s[e];
-    yb[e] = x2 * c[e] + x1 * s[e];
+    const float x1 = a.get(e), x2 = b.get(e), sn = sign * s[e];
+    ya[e] = x1 * c[e] - x2 * sn;
+    yb[e] = x2 * c[e] + x1 * sn;
   }
   a.set(ya);
   b.set(yb);
@@ -76,14 +97,15 @@ __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float*
 }
 
 hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
-                   int H, int d, int r, hipStream_t st) {
+                   int H, int d, int r, hipStream_t st, float sign) {
   const long n = (long)T_ * 2 * (H / d) * (r / 8);
   if (n <= 0) return hipSuccess;
   dim3 g((unsigned)((n + 255) / 256));
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, ct, stbl, T_, H, d, r);
+    hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, ct, stbl, T_, H, d, r, sign);
   else
-    hipLaunchKernelGGL(rope_qk_kernel<float>, g, dim3(256), 0, st, (float*)qkv, ld, pos, ct, stbl, T_, H, d, r);
+    hipLaunchKernelGGL(rope_qk_kernel<float>, g, dim3(256), 0, st, (float*)qkv, ld, pos, ct, stbl, T_, H, d, r,
+                       sign);
   return hipGetLastError();
 }
 
@@ -175,7 +197,10 @@ __global__ void __launch_bounds__(256) ln_bwd_dx_kernel(const T* dy, const T* x,
     const int idx = lane + 64 * c;
     if (idx < nch) {
       Vec8<T> r, o;
-      r.load(dres + off + idx * 8);
+      if (dres)
+        r.load(dres + off + idx * 8);
+      else
+        r.zero();
       float out[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) out[e] = r.get(e) + rs * (dxh[c][e] - m1 - xh[c][e] * m2);

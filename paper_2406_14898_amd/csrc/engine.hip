@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -199,6 +200,11 @@ int validate_desc(const fl_stack_desc* d) {
     return fail(FL_ERR_SHAPE, "num_prefix %d must be in [0, 4096]", d->num_prefix);
   if (d->num_prefix > 0 && d->dtype != FL_BF16)
     return fail(FL_ERR_SHAPE, "the P-tuning v2 prefix (num_prefix > 0) needs dtype FL_BF16");
+  if (!(d->residual_alpha >= 0.f) || !std::isfinite(d->residual_alpha))
+    return fail(FL_ERR_SHAPE, "residual_alpha must be finite and >= 0");
+  if (d->rotary_2d != 0 && d->rotary_2d != 1) return fail(FL_ERR_SHAPE, "rotary_2d must be 0 or 1");
+  if (d->rotary_2d && 2 * d->rotary_dim != hd)
+    return fail(FL_ERR_SHAPE, "GLM 2-D positions need rotary_dim = head dim / 2");
   return FL_OK;
 }
 
@@ -209,6 +215,7 @@ struct Plan {
   int32_t* cu;
   int32_t* prefix;
   int32_t* pos;
+  int32_t* pos2;  // GLM block positions (2-D mode)
   float* cos_t;
   float* sin_t;
   float* gemm_part;  // split-reduction scratch of the bf16 GEMMs (null for fp32)
@@ -219,7 +226,9 @@ void carve_plan(Carver& cv, const BatchInfo& bi, int rotary_dim, Plan* p) {
   p->cu = (int32_t*)cv.take(sizeof(int32_t) * (bi.S + 1));
   p->prefix = (int32_t*)cv.take(sizeof(int32_t) * bi.S);
   p->pos = (int32_t*)cv.take(sizeof(int32_t) * bi.T);
-  const size_t tab = sizeof(float) * (size_t)bi.maxL * std::max(rotary_dim / 2, 1);
+  p->pos2 = (int32_t*)cv.take(sizeof(int32_t) * bi.T);
+  // positions 0..maxL (a GLM block position reaches L when the context is empty)
+  const size_t tab = sizeof(float) * (size_t)(bi.maxL + 1) * std::max(rotary_dim / 2, 1);
   p->cos_t = (float*)cv.take(tab);
   p->sin_t = (float*)cv.take(tab);
 }
@@ -376,8 +385,10 @@ int upload_plan(fl_stack* st, const fl_batch_desc* b, const BatchInfo& bi, const
   st->ev_used[k] = true;
   hipStream_t s = stream;
   LAUNCH(FL_PROF_PLAN, 0, 4.0 * bi.T, [&]() {
-    hipError_t e = seq_positions(p.cu, bi.S, p.pos, stream);
-    return e != hipSuccess ? e : rope_table(p.cos_t, p.sin_t, bi.maxL, st->d.rotary_dim, st->d.rope_base, stream);
+    hipError_t e = st->d.rotary_2d ? seq_positions_2d(p.cu, bi.prefix ? p.prefix : nullptr, bi.S, p.pos, p.pos2, stream)
+                                   : seq_positions(p.cu, bi.S, p.pos, stream);
+    return e != hipSuccess ? e
+                           : rope_table(p.cos_t, p.sin_t, bi.maxL + 1, st->d.rotary_dim, st->d.rope_base, stream);
   }());
   return FL_OK;
 }
@@ -415,6 +426,11 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   // at T = 41447 than this 0.14 ms kernel, the epilogue being latency-bound.
   LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
          rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
+  if (st->d.rotary_2d)  // GLM 2-D positions: the second half by the block position
+    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
+           rope_qk(dt, (char*)a.qkv + (size_t)st->d.rotary_dim * st->E, 3 * H, plan.pos2, plan.cos_t, plan.sin_t, T, H,
+                   st->hd, st->d.rotary_dim, s));
+  const float alpha = st->d.residual_alpha;
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
   ad.cu_seqlens = plan.cu; ad.prefix_len = bi.prefix ? plan.prefix : nullptr;
@@ -425,7 +441,9 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   LAUNCH(FL_PROF_ATTN_FWD, 4.0 * H * pairs, 4 * TH * E + 4.0 * T * st->d.num_heads, attn_fwd(dt, ad, s));
   g = GemmDesc();
   g.A = a.o; g.B = p.w_o; g.C = a.h; g.M = T; g.N = H; g.K = H;
-  g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.R = x; g.ldr = H;
+  g.lda = H; g.ldb = H; g.ldc = H; g.bias = p.b_o; g.ldr = H;
+  g.R = alpha > 0.f ? a.u : x;  // ChatGLM-6B: h = alpha u + ...
+  g.res_scale = alpha > 0.f ? alpha : 1.f;
   LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, H), gemm_bytes(T, H, H, E, E) + TH * E,
          gemm(dt, GEMM_NT, EPI_BIAS_RES, with_part(g, plan), s));
   LAUNCH(FL_PROF_LAYERNORM_FWD, 0, 2 * TH * E + 8.0 * T,
@@ -438,7 +456,9 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   if (out) {
     g = GemmDesc();
     g.A = a.g; g.B = p.w_2; g.C = out; g.M = T; g.N = H; g.K = F;
-    g.lda = F; g.ldb = F; g.ldc = H; g.bias = p.b_2; g.R = a.h; g.ldr = H;
+    g.lda = F; g.ldb = F; g.ldc = H; g.bias = p.b_2; g.ldr = H;
+    g.R = alpha > 0.f ? a.w : a.h;  // ChatGLM-6B: y = alpha w + ...
+    g.res_scale = alpha > 0.f ? alpha : 1.f;
     LAUNCH(FL_PROF_GEMM_NT_BIAS_RES, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E) + TH * E,
            gemm(dt, GEMM_NT, EPI_BIAS_RES, with_part(g, plan), s));
   }
@@ -479,6 +499,10 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   const double E = st->E;
   // frozen weights (P-tuning v2): input gradients and prefix gradients only
   const bool train_w = gr.w_qkv != nullptr;
+  // ChatGLM-6B's residual: the normalised inputs w and u, scaled by alpha,
+  // feed y and h, so dy and dh join the LayerNorm inputs' gradients (in the
+  // input-gradient GEMMs' epilogues) instead of passing straight through
+  const float alpha = st->d.residual_alpha;
   int rc;
   // y = h + g W_2^T + b_2
   GemmDesc g;
@@ -503,9 +527,14 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   }
   g = GemmDesc();
   g.A = w.dz; g.B = p.w_1; g.C = w.tmp; g.M = T; g.N = H; g.K = F; g.lda = F; g.ldb = H; g.ldc = H;
-  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E), gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
-  // w = LN2(h); h also feeds y directly
-  if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, dy, w.dh, gr.ln2_g, gr.ln2_b, T, H, w, s)))
+  if (alpha > 0.f) {
+    g.R = dy; g.ldr = H; g.res_scale = alpha;
+  }
+  LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E),
+         gemm(dt, GEMM_NN, alpha > 0.f ? EPI_RES : EPI_STORE, with_part(g, plan), s));
+  // w = LN2(h); h also feeds y directly (plain residual)
+  if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, alpha > 0.f ? nullptr : dy, w.dh, gr.ln2_g,
+                        gr.ln2_b, T, H, w, s)))
     return rc;
   // h = x + o W_o^T + b_o
   if (train_w) {
@@ -525,10 +554,21 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.num_seqs = bi.S; ad.max_seqlen = bi.maxL; ad.num_heads = st->d.num_heads; ad.head_dim = st->hd;
   ad.hidden = H; ad.total_tokens = T;
   ad.dout = w.tmp; ad.ld_dout = H; ad.delta = w.delta; ad.dqkv = w.dqkv; ad.ld_dqkv = 3 * H;
-  ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t; ad.rotary_dim = st->d.rotary_dim;
+  // The attention kernels fuse the inverse rotation with the row's index
+  // inside its sequence as the position; GLM 2-D positions differ from it
+  // after the context, so in that mode both halves are rotated back below.
+  ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t;
+  ad.rotary_dim = st->d.rotary_2d ? 0 : st->d.rotary_dim;
   ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix; ad.dprefix_part = w.dprefix;
   const double pairs = bi.pairs + (double)st->d.num_prefix * T;
   LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
+  if (st->d.rotary_2d) {  // dq and dk rotated back: first half by p1, second by the block position
+    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
+           rope_qk(dt, w.dqkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s, -1.f));
+    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
+           rope_qk(dt, (char*)w.dqkv + (size_t)st->d.rotary_dim * st->E, 3 * H, plan.pos2, plan.cos_t, plan.sin_t, T, H,
+                   st->hd, st->d.rotary_dim, s, -1.f));
+  }
   if (st->d.num_prefix) {
     // sum of the per-sequence prefix gradients, in sequence order
     const long n = (long)st->d.num_prefix * H;
@@ -545,10 +585,14 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   }
   g = GemmDesc();
   g.A = w.dqkv; g.B = p.w_qkv; g.C = w.tmp; g.M = T; g.N = H; g.K = 3 * H; g.lda = 3 * H; g.ldb = H; g.ldc = H;
+  if (alpha > 0.f) {
+    g.R = w.dh; g.ldr = H; g.res_scale = alpha;
+  }
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, 3 * H), gemm_bytes(T, H, 3 * H, E, E),
-         gemm(dt, GEMM_NN, EPI_STORE, with_part(g, plan), s));
-  // u = LN1(x); x also feeds h directly
-  return ln_backward(st, dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, w.dh, dx, gr.ln1_g, gr.ln1_b, T, H, w, s);
+         gemm(dt, GEMM_NN, alpha > 0.f ? EPI_RES : EPI_STORE, with_part(g, plan), s));
+  // u = LN1(x); x also feeds h directly (plain residual)
+  return ln_backward(st, dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, alpha > 0.f ? nullptr : w.dh, dx, gr.ln1_g,
+                     gr.ln1_b, T, H, w, s);
 }
 
 }  // namespace

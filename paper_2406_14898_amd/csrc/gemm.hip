@@ -39,6 +39,7 @@ struct GemmArgs {
   const void* Z;
   long ldz;
   int nb;  // rows of B that exist (see GemmDesc::b_rows)
+  float res_scale;
 };
 
 __device__ __forceinline__ float gelu_f(float z) {
@@ -244,11 +245,11 @@ gemm_kernel(GemmArgs p) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) v[r] += b.get(r);
         }
-        if constexpr (EPI == EPI_BIAS_RES) {
+        if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) {
           Vec4<T> rr;
           rr.load(static_cast<const T*>(p.R) + (long)m * p.ldr + n);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] += rr.get(r);
+          for (int r = 0; r < 4; ++r) v[r] += p.res_scale * rr.get(r);
         }
         if constexpr (EPI == EPI_GELU_BWD) {
           Vec4<T> z;
@@ -309,6 +310,7 @@ static hipError_t dispatch_layout(int epi, const GemmArgs& a, hipStream_t st) {
     switch (epi) {
       case EPI_STORE: return launch_layout<T, true, false, EPI_STORE>(a, st);
       case EPI_GELU_BWD: return launch_layout<T, true, false, EPI_GELU_BWD>(a, st);
+      case EPI_RES: return launch_layout<T, true, false, EPI_RES>(a, st);
     }
   } else {
     if (epi == EPI_ACC_F32) return launch_layout<T, false, false, EPI_ACC_F32>(a, st);
@@ -348,6 +350,7 @@ hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStre
   a.lda = d.lda; a.ldb = d.ldb; a.ldc = d.ldc;
   a.bias = d.bias; a.R = d.R; a.ldr = d.ldr; a.C2 = d.C2; a.ldc2 = d.ldc2; a.Z = d.Z; a.ldz = d.ldz;
   a.nb = gemm_b_rows(layout == GEMM_NT, d);
+  a.res_scale = d.res_scale;
   if (dt == DT_BF16) {
     switch (layout) {
       case GEMM_NT: return dispatch_layout<bf16, GEMM_NT>(epi, a, st);

@@ -60,6 +60,7 @@ struct G2Args {
   float* part;
   int tail, splits, fixup;
   int nb;  // rows of B that exist (see GemmDesc::b_rows)
+  float res_scale;
 };
 
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
@@ -394,7 +395,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
       for (int u = 0; u < kBatch; ++u) {
         const long m = mbase + (q0 + u) * kWaves;
         if (m < p.M) {
-          if constexpr (EPI == EPI_BIAS_RES) ext[u].load(p.R + m * p.ldr + n);
+          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) ext[u].load(p.R + m * p.ldr + n);
           if constexpr (EPI == EPI_GELU_BWD) ext[u].load(p.Z + m * p.ldz + n);
           if constexpr (EPI == EPI_ACC_F32) cacc[u].load(static_cast<float*>(p.C) + m * p.ldc + n);
         }
@@ -413,9 +414,9 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
           cacc[u].set(o);
           cacc[u].store(static_cast<float*>(p.C) + m * p.ldc + n);
         } else {
-          if constexpr (EPI == EPI_BIAS_RES) {
+          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += ext[u].get(e);
+            for (int e = 0; e < 4; ++e) v[e] += p.res_scale * ext[u].get(e);
           }
           if constexpr (EPI == EPI_GELU_BWD) {
 #pragma unroll
@@ -468,6 +469,7 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.C2 = (bf16*)d.C2; a.ldc2 = d.ldc2; a.Z = (const bf16*)d.Z; a.ldz = d.ldz;
   a.part = d.part; a.tail = 0; a.splits = 1; a.fixup = 0;
   a.nb = gemm_b_rows(BKc, d);
+  a.res_scale = d.res_scale;
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
   const int cus = num_cus();
@@ -527,6 +529,7 @@ hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStrea
       switch (epi) {
         case EPI_STORE: return launch2<true, false, EPI_STORE>(d, st);
         case EPI_GELU_BWD: return launch2<true, false, EPI_GELU_BWD>(d, st);
+        case EPI_RES: return launch2<true, false, EPI_RES>(d, st);
       }
       break;
     case GEMM_TN:

@@ -30,6 +30,8 @@ struct GemmDesc {
   // Rows B really has (the N index for NT, the reduction index for NN / TN);
   // rows at or past it read as zero.  0 = as many as the shape implies.
   int b_rows = 0;
+  // Scale of R in EPI_BIAS_RES and EPI_RES (1: plain residual add).
+  float res_scale = 1.f;
 };
 // Rows of B a kernel may read for a layout and shape.
 inline int gemm_b_rows(bool b_kcontig, const GemmDesc& d) {
@@ -46,6 +48,7 @@ enum GemmEpi : int {
   EPI_BIAS_GELU = 3,  // C = z = acc + bias; C2 = gelu(z)
   EPI_GELU_BWD = 4,   // C = acc * gelu'(Z)
   EPI_ACC_F32 = 5,    // Cf += acc (fp32 output)
+  EPI_RES = 6,        // C = acc + res_scale * R
 };
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
 // bf16 LDS-DMA kernel (gemm_bf16.hip), used by gemm() for the shapes it takes.
@@ -54,11 +57,15 @@ hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStrea
 
 // Batch bookkeeping: position of every packed row inside its own sequence.
 hipError_t seq_positions(const int32_t* cu_seqlens, int num_seqs, int32_t* pos, hipStream_t st);
+// GLM 2-D positions (context length ctx[s], or the whole sequence when ctx is null).
+hipError_t seq_positions_2d(const int32_t* cu_seqlens, const int32_t* ctx, int num_seqs, int32_t* p1, int32_t* p2,
+                            hipStream_t st);
 // cos / sin (p * theta_i), theta_i = base^(-2i/r), p < max_pos, i < r/2 (computed in double).
 hipError_t rope_table(float* cos_t, float* sin_t, int max_pos, int rotary_dim, float base, hipStream_t st);
-// In-place rotation of the q and k parts of qkv [T, 3H] (row stride ld).
+// In-place rotation of the q and k parts of qkv [T, 3H] (row stride ld):
+// dims [0, rotary_dim) of every head starting at qkv; sign -1 rotates back.
 hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* cos_t, const float* sin_t,
-                   int T, int H, int head_dim, int rotary_dim, hipStream_t st);
+                   int T, int H, int head_dim, int rotary_dim, hipStream_t st, float sign = 1.f);
 
 // LayerNorm forward: y = (x - mean) * rstd * g + b, saving mean and rstd.
 hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
@@ -101,7 +108,10 @@ struct AttnDesc {
   float* delta = nullptr;  // [T, nh] scratch: rowsum(dO * O)
   void* dqkv = nullptr;    // [T, 3H]
   long ld_dqkv = 0;
-  const int32_t* pos = nullptr;  // per-row position (inverse rotary of dq, dk)
+  // Inverse rotary of dq, dk fused into the kernels' epilogues, over dims
+  // [0, rotary_dim) with the row's index inside its sequence as the
+  // position (0 = no rotation).
+  const int32_t* pos = nullptr;
   const float* cos_t = nullptr;
   const float* sin_t = nullptr;
   int rotary_dim = 0;

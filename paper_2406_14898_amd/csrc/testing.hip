@@ -2,6 +2,7 @@
 // Each validates the shape constraints its kernel relies on before any launch.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 
@@ -29,7 +30,7 @@ extern "C" {
 int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, void* C, int M, int N, int K,
                  int64_t lda, int64_t ldb, int64_t ldc, const void* bias, const void* R, int64_t ldr, void* C2,
                  int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, int b_rows,
-                 void* stream) {
+                 float res_scale, void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!A || !B || !C) return set_error(FL_ERR_NULL, "A / B / C is NULL");
   if (!al16(A) || !al16(B) || !al16(C)) return set_error(FL_ERR_ALIGN, "A / B / C not 16-byte aligned");
@@ -43,7 +44,8 @@ int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, v
            K % 64 == 0 && lda >= K && ldb >= K && ldc >= N;
       break;
     case FL_GEMM_NN:
-      ok = (epi == FL_EPI_STORE || epi == FL_EPI_GELU_BWD) && K % 64 == 0 && lda >= K && ldb >= N && ldc >= N;
+      ok = (epi == FL_EPI_STORE || epi == FL_EPI_GELU_BWD || epi == FL_EPI_RES) && K % 64 == 0 && lda >= K &&
+           ldb >= N && ldc >= N;
       break;
     case FL_GEMM_TN:
       ok = epi == FL_EPI_ACC_F32 && M % 8 == 0 && lda >= M && ldb >= N && ldc >= N;
@@ -54,7 +56,9 @@ int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, v
   if (!ok) return set_error(FL_ERR_ARG, "unsupported layout / epilogue / shape combination");
   if ((epi == FL_EPI_BIAS || epi == FL_EPI_BIAS_RES || epi == FL_EPI_BIAS_GELU) && (!bias || !al16(bias)))
     return set_error(FL_ERR_NULL, "bias missing or misaligned");
-  if (epi == FL_EPI_BIAS_RES && (!R || !al16(R) || ldr % 8 || ldr < N)) return set_error(FL_ERR_NULL, "R missing");
+  if ((epi == FL_EPI_BIAS_RES || epi == FL_EPI_RES) && (!R || !al16(R) || ldr % 8 || ldr < N))
+    return set_error(FL_ERR_NULL, "R missing");
+  if (!std::isfinite(res_scale)) return set_error(FL_ERR_ARG, "res_scale not finite");
   if (epi == FL_EPI_BIAS_GELU && (!C2 || !al16(C2) || ldc2 % 8 || ldc2 < N))
     return set_error(FL_ERR_NULL, "C2 missing");
   if (epi == FL_EPI_GELU_BWD && (!Z || !al16(Z) || ldz % 8 || ldz < N)) return set_error(FL_ERR_NULL, "Z missing");
@@ -65,6 +69,7 @@ int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, v
   d.bias = bias; d.R = R; d.ldr = ldr; d.C2 = C2; d.ldc2 = ldc2; d.Z = Z; d.ldz = ldz;
   d.part = part; d.part_bytes = part ? (size_t)part_bytes : 0;
   d.b_rows = b_rows;
+  d.res_scale = res_scale;
   return herr(gemm((DType)dtype, (GemmLayout)layout, epi, d, (hipStream_t)stream));
 }
 

@@ -23,7 +23,7 @@ FL_ERR_WORKSPACE, FL_ERR_ALIAS, FL_ERR_ALIGN, FL_ERR_HIP, FL_ERR_ARG = -6, -7, -
 FL_BF16, FL_F32 = 0, 1
 FL_MASK_CAUSAL, FL_MASK_PREFIX = 0, 1
 FL_GEMM_NT, FL_GEMM_NN, FL_GEMM_TN = 0, 1, 2
-FL_EPI_STORE, FL_EPI_BIAS, FL_EPI_BIAS_RES, FL_EPI_BIAS_GELU, FL_EPI_GELU_BWD, FL_EPI_ACC_F32 = range(6)
+FL_EPI_STORE, FL_EPI_BIAS, FL_EPI_BIAS_RES, FL_EPI_BIAS_GELU, FL_EPI_GELU_BWD, FL_EPI_ACC_F32, FL_EPI_RES = range(7)
 FL_PROF_NUM_CLASSES = 14
 
 PARAM_FIELDS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
@@ -53,7 +53,8 @@ class FlglmError(RuntimeError):
 class fl_stack_desc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("ffn_hidden", ctypes.c_int32), ("rotary_dim", ctypes.c_int32), ("rope_base", ctypes.c_float),
-                ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32), ("num_prefix", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32), ("num_prefix", ctypes.c_int32),
+                ("residual_alpha", ctypes.c_float), ("rotary_2d", ctypes.c_int32)]
 
 
 class fl_batch_desc(ctypes.Structure):
@@ -64,7 +65,8 @@ class fl_batch_desc(ctypes.Structure):
 
 
 class fl_client_desc(ctypes.Structure):
-    _fields_ = [("vocab", ctypes.c_int64), ("hidden", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+    _fields_ = [("vocab", ctypes.c_int64), ("hidden", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float)]
 
 
 class fl_layer_params(ctypes.Structure):
@@ -109,14 +111,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_client_workspace_bytes": [vp, i64, P(sz)],
         "fl_embedding_forward": [vp, vp, P(i32), i64, vp, vp, sz, vp],
         "fl_embedding_backward": [vp, P(i32), i64, vp, vp, vp, sz, vp],
-        "fl_lm_head_forward": [vp, vp, vp, P(i32), i64, vp, vp, vp, sz, vp],
-        "fl_lm_head_backward": [vp, vp, vp, i64, ctypes.c_float, vp, vp, vp, sz, vp],
+        "fl_lm_head_forward": [vp, vp, vp, vp, vp, P(i32), i64, vp, vp, vp, sz, vp],
+        "fl_lm_head_backward": [vp, vp, vp, vp, i64, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp],
         "fl_stack_profile": [vp, ctypes.c_int],
         "fl_stack_profile_read": [vp, ctypes.c_int, P(i64), P(ctypes.c_double), P(ctypes.c_double),
                                   P(ctypes.c_double)],
         "fl_test_gemm": [ctypes.c_int] * 3 + [vp] * 3 + [ctypes.c_int] * 3 + [i64] * 3 + [vp, vp, i64, vp, i64, vp,
                                                                                           i64, vp, i64, ctypes.c_int,
-                                                                                          vp],
+                                                                                          ctypes.c_float, vp],
         "fl_test_layernorm_fwd": [ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                   vp],
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
@@ -174,8 +176,9 @@ def _stream(s) -> Optional[int]:
 
 def stack_desc(num_layers: int, hidden: int, num_heads: int, ffn_hidden: int, rotary_dim: int,
                dtype: int = FL_BF16, rope_base: float = 10000.0, ln_eps: float = 1e-5,
-               num_prefix: int = 0) -> fl_stack_desc:
-    return fl_stack_desc(num_layers, hidden, num_heads, ffn_hidden, rotary_dim, rope_base, ln_eps, dtype, num_prefix)
+               num_prefix: int = 0, residual_alpha: float = 0.0, rotary_2d: bool = False) -> fl_stack_desc:
+    return fl_stack_desc(num_layers, hidden, num_heads, ffn_hidden, rotary_dim, rope_base, ln_eps, dtype, num_prefix,
+                         residual_alpha, int(rotary_2d))
 
 
 class BatchDesc:
@@ -298,9 +301,9 @@ def _host_i32(a):
     return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
 
 
-def fl_client_create(vocab: int, hidden: int, dtype: int = FL_BF16) -> int:
+def fl_client_create(vocab: int, hidden: int, dtype: int = FL_BF16, ln_eps: float = 1e-5) -> int:
     h = ctypes.c_void_p()
-    _check(load().fl_client_create(ctypes.byref(fl_client_desc(vocab, hidden, dtype)), ctypes.byref(h)))
+    _check(load().fl_client_create(ctypes.byref(fl_client_desc(vocab, hidden, dtype, ln_eps)), ctypes.byref(h)))
     return h.value
 
 
@@ -326,17 +329,19 @@ def fl_embedding_backward(handle: int, ids, dout, dtable, workspace, stream=None
                                         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
-def fl_lm_head_forward(handle: int, h, w, labels, loss_tok, loss_sum, workspace, stream=None) -> None:
+def fl_lm_head_forward(handle: int, h, w, labels, loss_tok, loss_sum, workspace, stream=None, ln_g=None,
+                       ln_b=None) -> None:
     arr, p = _host_i32(labels)
-    _check(load().fl_lm_head_forward(handle, _ptr(h), _ptr(w), p, len(arr), _ptr(loss_tok), _ptr(loss_sum),
-                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+    _check(load().fl_lm_head_forward(handle, _ptr(h), _ptr(ln_g), _ptr(ln_b), _ptr(w), p, len(arr), _ptr(loss_tok),
+                                     _ptr(loss_sum), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                      _stream(stream)))
 
 
-def fl_lm_head_backward(handle: int, h, w, T: int, grad_scale: float, dh, dw, workspace, stream=None) -> None:
-    _check(load().fl_lm_head_backward(handle, _ptr(h), _ptr(w), T, grad_scale, _ptr(dh), _ptr(dw),
-                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                      _stream(stream)))
+def fl_lm_head_backward(handle: int, h, w, T: int, grad_scale: float, dh, dw, workspace, stream=None, ln_g=None,
+                        dln_g=None, dln_b=None) -> None:
+    _check(load().fl_lm_head_backward(handle, _ptr(h), _ptr(ln_g), _ptr(w), T, grad_scale, _ptr(dh), _ptr(dln_g),
+                                      _ptr(dln_b), _ptr(dw), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def fl_stack_profile(handle: int, enable: bool) -> None:
@@ -370,13 +375,13 @@ def profile_table(handle: int):
 # ---------------------------------------------------------------------------
 
 def fl_test_gemm(dtype, layout, epi, A, B, C, M, N, K, lda, ldb, ldc, bias=None, R=None, ldr=0, C2=None, ldc2=0,
-                 Z=None, ldz=0, part=None, b_rows=0, stream=None) -> None:
+                 Z=None, ldz=0, part=None, b_rows=0, res_scale=1.0, stream=None) -> None:
     """part: optional fp32 device tensor, split-reduction scratch; b_rows:
     rows B really has (0 = all)."""
     nbytes = part.numel() * part.element_size() if part is not None else 0
     _check(load().fl_test_gemm(dtype, layout, epi, _ptr(A), _ptr(B), _ptr(C), M, N, K, lda, ldb, ldc, _ptr(bias),
                                _ptr(R), ldr, _ptr(C2), ldc2, _ptr(Z), ldz, _ptr(part), nbytes, b_rows,
-                               _stream(stream)))
+                               res_scale, _stream(stream)))
 
 
 def fl_test_layernorm_fwd(dtype, x, g, b, y, mean, rstd, T, H, eps, stream=None) -> None:

@@ -12,15 +12,19 @@ class ServerStack:
     """FL-GLM server stack (blocks 1..N-2 of the split model) on one GPU."""
 
     def __init__(self, num_layers: int, hidden: int, num_heads: int, ffn_hidden: int, rotary_dim: int,
-                 dtype: str = "bf16", rope_base: float = 10000.0, ln_eps: float = 1e-5, num_prefix: int = 0):
+                 dtype: str = "bf16", rope_base: float = 10000.0, ln_eps: float = 1e-5, num_prefix: int = 0,
+                 residual_alpha: float = 0.0, rotary_2d: bool = False):
         """num_prefix > 0: P-tuning v2 prefix of that many key / value rows per
-        block (params then carry "prefix_k" / "prefix_v" [num_prefix, hidden])."""
+        block (params then carry "prefix_k" / "prefix_v" [num_prefix, hidden]).
+        residual_alpha > 0 / rotary_2d: ChatGLM-6B's own block (alpha-scaled
+        residual on the normalised input, GLM 2-D positions)."""
         self.dtype = F.FL_BF16 if dtype == "bf16" else F.FL_F32
         self.num_layers = num_layers
         self.hidden = hidden
         self.num_prefix = num_prefix
         self.handle = F.fl_stack_create(F.stack_desc(num_layers, hidden, num_heads, ffn_hidden, rotary_dim,
-                                                     self.dtype, rope_base, ln_eps, num_prefix))
+                                                     self.dtype, rope_base, ln_eps, num_prefix, residual_alpha,
+                                                     rotary_2d))
 
     def close(self) -> None:
         if self.handle:

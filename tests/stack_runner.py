@@ -20,7 +20,7 @@ class GpuStack:
         [num_prefix, hidden] (P-tuning v2)."""
         self.shape, self.dt = shape, dt
         self.ss = ServerStack(shape.num_layers, shape.hidden, shape.num_heads, shape.ffn_hidden, shape.rotary_dim,
-                              dt, shape.rope_base, shape.ln_eps, num_prefix)
+                              dt, shape.rope_base, shape.ln_eps, num_prefix, shape.residual_alpha, shape.rotary_2d)
         cache = {}  # layers given as the same dict share one device copy
         self.params = []
         for lp in layers:

@@ -219,12 +219,19 @@ def test_client_handle_validation_host_only():
     assert rc == F.FL_ERR_ALIGN
     labels = (ctypes.c_int32 * 10)(*([-100] * 9 + [1000]))
     lt, ls = 1 << 31, (1 << 31) + 4096
-    rc = lib.fl_lm_head_forward(h, OUT, TAB, labels, 10, lt, ls, WS, ws_n, None)
+    rc = lib.fl_lm_head_forward(h, OUT, None, None, TAB, labels, 10, lt, ls, WS, ws_n, None)
     assert rc == F.FL_ERR_ARG and "label" in F.fl_last_error()
-    rc = lib.fl_lm_head_forward(h, OUT, TAB, labels, 10, WS + 256, ls, WS, ws_n, None)
+    rc = lib.fl_lm_head_forward(h, OUT, None, None, TAB, labels, 10, WS + 256, ls, WS, ws_n, None)
     assert rc == F.FL_ERR_ALIAS
-    rc = lib.fl_lm_head_backward(h, OUT, TAB, 10, ctypes.c_float(float("inf")), lt, None, WS, ws_n, None)
+    ok_labels = (ctypes.c_int32 * 10)(*([-100] * 10))
+    rc = lib.fl_lm_head_forward(h, OUT, TAB + (1 << 20), None, TAB, ok_labels, 10, lt, ls, WS, ws_n, None)
+    assert rc == F.FL_ERR_NULL and "both or neither" in F.fl_last_error()
+    rc = lib.fl_lm_head_backward(h, OUT, None, TAB, 10, ctypes.c_float(float("inf")), lt, None, None, None, WS,
+                                 ws_n, None)
     assert rc == F.FL_ERR_ARG
-    rc = lib.fl_lm_head_backward(h, OUT, TAB, 0, ctypes.c_float(1.0), lt, None, WS, ws_n, None)
+    rc = lib.fl_lm_head_backward(h, OUT, None, TAB, 0, ctypes.c_float(1.0), lt, None, None, None, WS, ws_n, None)
     assert rc == F.FL_ERR_ARG
+    rc = lib.fl_lm_head_backward(h, OUT, None, TAB, 10, ctypes.c_float(1.0), lt, lt + (1 << 20), lt + (1 << 21),
+                                 None, WS, ws_n, None)
+    assert rc == F.FL_ERR_ARG and "without a final LayerNorm" in F.fl_last_error()
     F.fl_client_destroy(h)
