@@ -504,7 +504,7 @@ def main() -> int:
         # the whole split model: client embedding + block 0, the server's
         # blocks, client block N-1 + final linear layer and loss
         model = SplitModel(sh.hidden, sh.num_heads, sh.ffn_hidden, sh.rotary_dim, sh.num_layers, w.vocab, w.dtype,
-                           sh.rope_base, sh.ln_eps, w.num_prefix)
+                           sh.rope_base, sh.ln_eps, w.num_prefix, sh.residual_alpha, sh.rotary_2d)
         handles = [model.block0.handle, model.server.handle, model.block_last.handle]
         buf = model.buffers(bd, w.recompute)
         ids, labels = synth.token_ids(b, w.vocab, args.seed)
@@ -513,6 +513,14 @@ def main() -> int:
               "server": params[1:-1], "block_last": params[-1]}
         sg = {"embedding": inp["g_embedding"], "lm_head": inp["g_lm_head"], "block0": grads[0],
               "server": grads[1:-1], "block_last": grads[-1]}
+        if sh.residual_alpha > 0:  # ChatGLM-6B's final LayerNorm: 1 + N(0, 0.02), N(0, 0.02)
+            gen = torch.Generator(device="cuda").manual_seed(args.seed * 100003 + 99983)
+            tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+            sp["final_ln_g"] = (1 + 0.02 * torch.randn(sh.hidden, generator=gen, device="cuda")).to(tdt)
+            sp["final_ln_b"] = (0.02 * torch.randn(sh.hidden, generator=gen, device="cuda")).to(tdt)
+            if not w.frozen:
+                sg["final_ln_g"] = torch.zeros(sh.hidden, device="cuda")
+                sg["final_ln_b"] = torch.zeros(sh.hidden, device="cuda")
 
         def fwd_bwd(timed):
             model.step(bd, ids, labels, sp, sg, scale, buf, w.recompute, stream, client_marks if timed else None)
@@ -636,6 +644,9 @@ def main() -> int:
                    "heads": w.shape.num_heads, "ffn": w.shape.ffn_hidden, "mask": w.mask,
                    "backward": w.backward, "recompute": w.recompute, "parallelism": "single GPU",
                    "ptuning_prefix": w.num_prefix, "weights_frozen": w.frozen,
+                   "block": ("ChatGLM-6B (alpha %.3f residual, 2-D positions%s)" % (
+                       w.shape.residual_alpha, ", final LayerNorm" if w.vocab else "")
+                             if w.shape.residual_alpha else "pre-LN, x + f(LN(x)), 1-D positions"),
                    "scope": ("whole split model: client embedding + block 0, %d server blocks, client block %d + "
                              "final linear (vocab %d) + cross-entropy" % (w.shape.num_layers, w.shape.num_layers + 1,
                                                                           w.vocab)) if w.vocab else "server stack"},

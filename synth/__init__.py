@@ -23,6 +23,7 @@ W_qkv, b_qkv, W_o, b_o, W_1, b_1, W_2, b_2, ln1_g, ln1_b, ln2_g, ln2_b.
 from __future__ import annotations
 
 from dataclasses import dataclass, field
+import math
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -316,6 +317,14 @@ WORKLOADS: Dict[str, Workload] = {
         "the whole split ChatGLM-6B-shaped model under P-tuning v2 on the 32 x 1 U[512,2048] batch: client "
         "embedding (130528 words) and block 0, 26 server blocks, client block 27, final linear layer and "
         "next-token cross-entropy, forward and backward; 128 prefix rows per block, weights frozen, recompute",
+        num_prefix=128, frozen=True, vocab=130528),
+    "chatglm6b_28blk_split_glm_ptuning128_prefix_32x1_recompute": Workload(
+        "chatglm6b_28blk_split_glm_ptuning128_prefix_32x1_recompute",
+        StackShape(num_layers=26, residual_alpha=math.sqrt(2 * 28), rotary_2d=True, **CHATGLM6B),
+        32, 1, (512, 2048), "prefix", "bf16", True, True, 1e-2,
+        "the whole split model with ChatGLM-6B's own blocks (alpha = sqrt(56) residual, GLM 2-D positions, final "
+        "LayerNorm) on GLM blank-infilling batches (32 x 1 U[512,2048], the first 25 % of each sequence the "
+        "bidirectional context), P-tuning v2 (128 prefix rows, weights frozen), recompute, bf16",
         num_prefix=128, frozen=True, vocab=130528),
 }
 

@@ -376,3 +376,33 @@ def test_lm_head_bench_shape_sampled():
     ch.close()
     del ws, h, w, dw
     torch.cuda.empty_cache()
+
+
+def test_glm_26_blocks_sampled(layers2):
+    """The ChatGLM-6B-exact server stack of the GLM benchmark workload (26
+    blocks, alpha residual, 2-D positions, prefix-LM batches of 32 x 1
+    U[512,2048] with 25 % context, P-tuning v2 with frozen weights,
+    recompute): the shortest sequence's y and dx against the float32 oracle.
+    The blocks' weights are the plain layers' (the variant changes the
+    arithmetic, not the parameters)."""
+    w = synth.WORKLOADS["chatglm6b_28blk_split_glm_ptuning128_prefix_32x1_recompute"]
+    b = w.batch()
+    n = w.shape.num_layers
+    pl = [_with_prefix(layers2[l], l) for l in range(2)]
+    layers = [pl[l % 2] for l in range(n)]
+    x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=w.dy_std)
+    g = GpuStack(w.shape, layers, "bf16", NP)
+    res = g.run(b, x, dy, recompute=True, frozen=True)
+    host = {"y": res["y"].float().cpu().numpy(), "dx": res["dx"].float().cpu().numpy()}
+    del res
+    g.close()
+    s = int(np.argmin(b.seqlens))
+    sb, r0, r1 = _seq_batch(b, s)
+    yo, xs = oracle.stack_forward(layers, n, x[r0:r1], sb, w.shape, dtype=np.float32)
+    grads = [oracle.zero_prefix_grads(NP, ONE.hidden, np.float32) for _ in range(n)]
+    dxo, _ = oracle.stack_backward(layers, n, xs, dy[r0:r1], sb, w.shape, grads, dtype=np.float32)
+    ey, edx = rel_l2(host["y"][r0:r1], yo), rel_l2(host["dx"][r0:r1], dxo)
+    print(f"[fullsize] GLM 26 blocks seq {s} (L={r1 - r0}, P={int(sb.prefix_len[0])}): y {ey:.2e} dx {edx:.2e}",
+          flush=True)
+    assert ey < TOL and edx < TOL
