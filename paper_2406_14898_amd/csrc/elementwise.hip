@@ -279,23 +279,38 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* X, long ld
   float a1[8], a2[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) { a1[e] = 0.f; a2[e] = 0.f; }
-  if (col < N) {
-    for (int r = r0 + w; r < r1; r += 4) {
-      Vec8<T> xv;
-      xv.load(X + (long)r * ldx + col);
-      if constexpr (MODE == 0) {
+  // rows r0 + w, r0 + w + 4, ... in order; four of them loaded before any is
+  // added, so each wave keeps four loads in flight (same summation order)
+  auto add = [&](const Vec8<T>& xv, const Vec8<T>& yv, int r) {
+    if constexpr (MODE == 0) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) a1[e] += xv.get(e);
-      } else {
-        Vec8<T> yv;
-        yv.load(Y + (long)r * ldx + col);
-        const float mu = mean[r], rs = rstd[r];
+      for (int e = 0; e < 8; ++e) a1[e] += xv.get(e);
+    } else {
+      const float mu = mean[r], rs = rstd[r];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          a1[e] += xv.get(e) * ((yv.get(e) - mu) * rs);
-          a2[e] += xv.get(e);
-        }
+      for (int e = 0; e < 8; ++e) {
+        a1[e] += xv.get(e) * ((yv.get(e) - mu) * rs);
+        a2[e] += xv.get(e);
       }
+    }
+  };
+  if (col < N) {
+    int r = r0 + w;
+    for (; r + 12 < r1; r += 16) {
+      Vec8<T> xv[4], yv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        xv[u].load(X + (long)(r + 4 * u) * ldx + col);
+        if constexpr (MODE == 1) yv[u].load(Y + (long)(r + 4 * u) * ldx + col);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(xv[u], yv[u], r + 4 * u);
+    }
+    for (; r < r1; r += 4) {
+      Vec8<T> xv, yv;
+      xv.load(X + (long)r * ldx + col);
+      if constexpr (MODE == 1) yv.load(Y + (long)r * ldx + col);
+      add(xv, yv, r);
     }
   }
 #pragma unroll
@@ -336,17 +351,36 @@ hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const voi
   return hipGetLastError();
 }
 
-__global__ void colsum_finish_kernel(const float* part, int nblk, int N, float* out) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
+// out[n] += sum over the nblk partial rows.  A workgroup takes 64 columns;
+// its four waves sum contiguous quarters of the rows (eight loads in flight
+// per lane), and the quarters are added in order through LDS: a fixed order,
+// so the result is deterministic.
+__global__ void __launch_bounds__(256) colsum_finish_kernel(const float* part, int nblk, int N, float* out) {
+  __shared__ float q[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + lane;
+  const int per = (nblk + 3) / 4;
+  const int b0 = min(nblk, w * per), b1 = min(nblk, b0 + per);
   float s = 0.f;
-  for (int b = 0; b < nblk; ++b) s += part[(long)b * N + n];
-  out[n] += s;
+  if (n < N) {
+    int b = b0;
+    for (; b + 8 <= b1; b += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(long)(b + u) * N + n];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; b < b1; ++b) s += part[(long)b * N + n];
+  }
+  q[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && n < N) out[n] += ((q[0][lane] + q[1][lane]) + q[2][lane]) + q[3][lane];
 }
 
 hipError_t colsum_finish(const float* part, int nblk, int N, float* out, hipStream_t st) {
   if (N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 255) / 256), dim3(256), 0, st, part, nblk, N, out);
+  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 63) / 64), dim3(256), 0, st, part, nblk, N, out);
   return hipGetLastError();
 }
 

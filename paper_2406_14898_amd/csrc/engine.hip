@@ -408,8 +408,10 @@ GemmDesc& with_part(GemmDesc& g, const Plan& plan) {
   return g;
 }
 
+// keep_z = false: the FFN's pre-activation z is not stored (nothing reads it
+// when the block's intermediates are not kept for a backward).
 int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_layer_params& p, const void* x,
-                  const Acts& a, void* out, hipStream_t s) {
+                  const Acts& a, void* out, hipStream_t s, bool keep_z = true) {
   const DType dt = (DType)st->d.dtype;
   const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
   const double E = st->E, TH = (double)T * H;
@@ -449,9 +451,9 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   LAUNCH(FL_PROF_LAYERNORM_FWD, 0, 2 * TH * E + 8.0 * T,
          layernorm_fwd(dt, a.h, p.ln2_g, p.ln2_b, a.w, a.mean2, a.rstd2, T, H, st->d.ln_eps, s));
   g = GemmDesc();
-  g.A = a.w; g.B = p.w_1; g.C = a.z; g.C2 = a.g; g.M = T; g.N = F; g.K = H;
+  g.A = a.w; g.B = p.w_1; g.C = keep_z ? a.z : nullptr; g.C2 = a.g; g.M = T; g.N = F; g.K = H;
   g.lda = H; g.ldb = H; g.ldc = F; g.ldc2 = F; g.bias = p.b_1;
-  LAUNCH(FL_PROF_GEMM_NT_BIAS_GELU, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
+  LAUNCH(FL_PROF_GEMM_NT_BIAS_GELU, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, keep_z ? 2 * E : E),
          gemm(dt, GEMM_NT, EPI_BIAS_GELU, with_part(g, plan), s));
   if (out) {
     g = GemmDesc();
@@ -738,9 +740,10 @@ int fl_server_stack_forward(fl_stack* st, const fl_batch_desc* b, const fl_layer
   const int N = st->d.num_layers;
   const void* cur = x;
   for (int l = 0; l < N; ++l) {
-    const Acts& a = (saved && !recompute) ? sv.acts[l] : w.acts;
+    const bool keep = saved && !recompute;  // intermediates kept for the backward
+    const Acts& a = keep ? sv.acts[l] : w.acts;
     void* out = (l == N - 1) ? y : (saved ? sv.xin[l + 1] : w.ping[l & 1]);
-    if ((rc = block_forward(st, bi, w.plan, layers[l], cur, a, out, s))) return rc;
+    if ((rc = block_forward(st, bi, w.plan, layers[l], cur, a, out, s, keep))) return rc;
     cur = out;
   }
   return FL_OK;

@@ -259,7 +259,7 @@ gemm_kernel(GemmArgs p) {
         }
         Vec4<T> o;
         o.set(v);
-        o.store(static_cast<T*>(p.C) + (long)m * p.ldc + n);
+        if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<T*>(p.C) + (long)m * p.ldc + n);
         if constexpr (EPI == EPI_BIAS_GELU) {
           float g[4];
 #pragma unroll

@@ -424,7 +424,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
           }
         Vec4<bf16> o;
           o.set(v);
-          o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
+          if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
           if constexpr (EPI == EPI_BIAS_GELU) {
             float g[4];
 #pragma unroll

@@ -45,7 +45,7 @@ enum GemmEpi : int {
   EPI_STORE = 0,      // C = acc
   EPI_BIAS = 1,       // C = acc + bias
   EPI_BIAS_RES = 2,   // C = acc + bias + R
-  EPI_BIAS_GELU = 3,  // C = z = acc + bias; C2 = gelu(z)
+  EPI_BIAS_GELU = 3,  // C = z = acc + bias (skipped when C is null); C2 = gelu(z)
   EPI_GELU_BWD = 4,   // C = acc * gelu'(Z)
   EPI_ACC_F32 = 5,    // Cf += acc (fp32 output)
   EPI_RES = 6,        // C = acc + res_scale * R
