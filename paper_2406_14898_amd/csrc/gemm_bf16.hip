@@ -310,8 +310,10 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
       fa1[j] = rd_a(slot, 1, j);
       if (j < kWTN) fb1[j] = rd_b(slot, 1, j);
       __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);  // the matrix group wins issue over the other wave's memory ops
 #pragma unroll
       for (int i = 0; i < kWTN; ++i) acc[i][j] = mma16(fb0[i], fa0[j], acc[i][j]);
+      __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);
     }
     // stage kt+1 landed (own loads) and every wave has finished reading
@@ -326,8 +328,10 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
       fa0[j] = rd_a(slot ^ 1, 0, j);
       if (j < kWTN) fb0[j] = rd_b(slot ^ 1, 0, j);
       __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int i = 0; i < kWTN; ++i) acc[i][j] = mma16(fb1[i], fa1[j], acc[i][j]);
+      __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
