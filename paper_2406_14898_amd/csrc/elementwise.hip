@@ -64,8 +64,10 @@ hipError_t rope_table(float* ct, float* stbl, int max_pos, int r, float base, hi
 
 // One thread rotates 4 pairs (i, i + r/2), i..i+3, of one head of q or k.
 template <typename T>
-__global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
-                               int H, int d, int r, float sign) {
+// pos2 (GLM 2-D positions): the same thread also rotates the matching pairs
+// of dims [r, 2r) by pos2, so both halves take one pass over q and k.
+__global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const int32_t* pos2, const float* ct,
+                               const float* stbl, int T_, int H, int d, int r, float sign) {
   const int half = r / 2, groups = half / 4;
   const int nh = H / d;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -94,18 +96,36 @@ __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const float*
   b.set(yb);
   a.store(base + i);
   b.store(base + half + i);
+  if (pos2) {
+    const int p2 = pos2[t];
+    a.load(base + r + i);
+    b.load(base + r + half + i);
+    const float* c2 = ct + (long)p2 * half + i;
+    const float* s2 = stbl + (long)p2 * half + i;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x1 = a.get(e), x2 = b.get(e), sn = sign * s2[e];
+      ya[e] = x1 * c2[e] - x2 * sn;
+      yb[e] = x2 * c2[e] + x1 * sn;
+    }
+    a.set(ya);
+    b.set(yb);
+    a.store(base + r + i);
+    b.store(base + r + half + i);
+  }
 }
 
 hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
-                   int H, int d, int r, hipStream_t st, float sign) {
+                   int H, int d, int r, hipStream_t st, float sign, const int32_t* pos2) {
   const long n = (long)T_ * 2 * (H / d) * (r / 8);
   if (n <= 0) return hipSuccess;
   dim3 g((unsigned)((n + 255) / 256));
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, ct, stbl, T_, H, d, r, sign);
-  else
-    hipLaunchKernelGGL(rope_qk_kernel<float>, g, dim3(256), 0, st, (float*)qkv, ld, pos, ct, stbl, T_, H, d, r,
+    hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, pos2, ct, stbl, T_, H, d, r,
                        sign);
+  else
+    hipLaunchKernelGGL(rope_qk_kernel<float>, g, dim3(256), 0, st, (float*)qkv, ld, pos, pos2, ct, stbl, T_, H, d,
+                       r, sign);
   return hipGetLastError();
 }
 

@@ -426,12 +426,10 @@ int block_forward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const fl_
   // A separate pass on purpose: folded into the QKV epilogue (a lane-pair
   // exchange plus table loads per row) it measured 0.5 ms slower per call
   // at T = 41447 than this 0.14 ms kernel, the epilogue being latency-bound.
-  LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
-         rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s));
-  if (st->d.rotary_2d)  // GLM 2-D positions: the second half by the block position
-    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
-           rope_qk(dt, (char*)a.qkv + (size_t)st->d.rotary_dim * st->E, 3 * H, plan.pos2, plan.cos_t, plan.sin_t, T, H,
-                   st->hd, st->d.rotary_dim, s));
+  // (GLM 2-D positions: the second half by the block position, same pass)
+  const int32_t* pos2 = st->d.rotary_2d ? plan.pos2 : nullptr;
+  LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E * (pos2 ? 2 : 1),
+         rope_qk(dt, a.qkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s, 1.f, pos2));
   const float alpha = st->d.residual_alpha;
   AttnDesc ad;
   ad.qkv = a.qkv; ad.ld_qkv = 3 * H; ad.o = a.o; ad.ld_o = H; ad.lse = a.lse;
@@ -564,13 +562,10 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix; ad.dprefix_part = w.dprefix;
   const double pairs = bi.pairs + (double)st->d.num_prefix * T;
   LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
-  if (st->d.rotary_2d) {  // dq and dk rotated back: first half by p1, second by the block position
-    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
-           rope_qk(dt, w.dqkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s, -1.f));
-    LAUNCH(FL_PROF_ROPE, 0, 4.0 * T * st->d.num_heads * st->d.rotary_dim * E,
-           rope_qk(dt, (char*)w.dqkv + (size_t)st->d.rotary_dim * st->E, 3 * H, plan.pos2, plan.cos_t, plan.sin_t, T, H,
-                   st->hd, st->d.rotary_dim, s, -1.f));
-  }
+  if (st->d.rotary_2d)  // dq and dk rotated back: first half by p1, second by the block position
+    LAUNCH(FL_PROF_ROPE, 0, 8.0 * T * st->d.num_heads * st->d.rotary_dim * E,
+           rope_qk(dt, w.dqkv, 3 * H, plan.pos, plan.cos_t, plan.sin_t, T, H, st->hd, st->d.rotary_dim, s, -1.f,
+                   plan.pos2));
   if (st->d.num_prefix) {
     // sum of the per-sequence prefix gradients, in sequence order
     const long n = (long)st->d.num_prefix * H;

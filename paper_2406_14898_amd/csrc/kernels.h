@@ -63,9 +63,11 @@ hipError_t seq_positions_2d(const int32_t* cu_seqlens, const int32_t* ctx, int n
 // cos / sin (p * theta_i), theta_i = base^(-2i/r), p < max_pos, i < r/2 (computed in double).
 hipError_t rope_table(float* cos_t, float* sin_t, int max_pos, int rotary_dim, float base, hipStream_t st);
 // In-place rotation of the q and k parts of qkv [T, 3H] (row stride ld):
-// dims [0, rotary_dim) of every head starting at qkv; sign -1 rotates back.
+// dims [0, rotary_dim) of every head by pos; with pos2 (GLM 2-D positions)
+// also dims [rotary_dim, 2 rotary_dim) by pos2.  sign -1 rotates back.
 hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* cos_t, const float* sin_t,
-                   int T, int H, int head_dim, int rotary_dim, hipStream_t st, float sign = 1.f);
+                   int T, int H, int head_dim, int rotary_dim, hipStream_t st, float sign = 1.f,
+                   const int32_t* pos2 = nullptr);
 
 // LayerNorm forward: y = (x - mean) * rstd * g + b, saving mean and rstd.
 hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
