@@ -204,10 +204,22 @@ def test_colsum_many_blocks(dt):
 # Rotary and attention
 # ---------------------------------------------------------------------------
 
+def _many_tiny():
+    """600 sequences of 1 to 4 tokens, three per client: many (sequence, head)
+    groups, every tile ragged."""
+    lens = np.random.default_rng(9).integers(1, 5, 600)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    return synth.Batch(cu, np.arange(0, 601, 3, dtype=np.int32))
+
+
 BATCHES = {
     "ragged_causal": synth.Batch(np.array([0, 1, 6, 70, 135, 335], np.int32), np.array([0, 2, 5], np.int32)),
     "ragged_prefix": synth.Batch(np.array([0, 1, 6, 70, 135, 335], np.int32), np.array([0, 2, 5], np.int32),
                                  "prefix", np.array([0, 3, 16, 65, 150], np.int32)),
+    # contexts covering the whole sequence (bidirectional) or all but its last token
+    "full_context": synth.Batch(np.array([0, 1, 65, 130, 260], np.int32), np.array([0, 1, 4], np.int32),
+                                "prefix", np.array([1, 64, 64, 130], np.int32)),
+    "many_tiny": _many_tiny(),
 }
 
 
@@ -307,6 +319,45 @@ def test_attention_fwd_bwd(dt, heads, bname):
         assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
         assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
         assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
+
+
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+def test_attention_long_sequence(mask):
+    """One 8192-token sequence (bf16, 2 heads of 128; prefix-LM with a
+    2048-token context), forward and backward with the inverse rotation."""
+    nh, d = 2, 128
+    H, T = nh * d, 8192
+    b = synth.Batch(np.array([0, T], np.int32), np.array([0, 1], np.int32), mask,
+                    np.array([2048], np.int32) if mask == "prefix" else None)
+    qkv = _qkv(T, H, 23, "bf16")
+    q = qkv[:, :H].astype(np.float64).reshape(T, nh, d)
+    k = qkv[:, H:2 * H].astype(np.float64).reshape(T, nh, d)
+    v = qkv[:, 2 * H:].astype(np.float64).reshape(T, nh, d)
+    cu = dev_i32(b.cu_seqlens)
+    pre = dev_i32(b.prefix_len) if mask == "prefix" else None
+    t = dev(qkv, "bf16")
+    o = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_fwd(F.FL_BF16, t, o, lse, cu, pre, T, 1, T, H, nh)
+    r = d // 2
+    pos = torch.empty(T, dtype=torch.int32, device="cuda")
+    ct = torch.empty(T * r // 2, dtype=torch.float32, device="cuda")
+    st = torch.empty_like(ct)
+    F.fl_test_rope(F.FL_BF16, torch.zeros((T, 3 * H), dtype=torch.bfloat16, device="cuda"), cu, 1, T, T, H, nh, r,
+                   10000.0, pos, ct, st)
+    do = rnd((T, H), 24, dt="bf16")
+    dqkv = torch.empty((T, 3 * H), dtype=torch.bfloat16, device="cuda")
+    delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, dev(do, "bf16"), dqkv, delta, cu, pre, pos, ct, st, r, T, 1, T,
+                            H, nh)
+    sync()
+    assert rel_l2(host(o), oracle.attention_forward(q, k, v, b).reshape(T, H)) < TOL["bf16"] / 2
+    dq, dk, dv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b)
+    cos, sin = oracle.rope_tables(oracle.positions(b.cu_seqlens), r, 10000.0)
+    g = host(dqkv)
+    assert rel_l2(g[:, :H], oracle.rope(dq, cos, sin, r, inverse=True).reshape(T, H)) < TOL["bf16"] / 2
+    assert rel_l2(g[:, H:2 * H], oracle.rope(dk, cos, sin, r, inverse=True).reshape(T, H)) < TOL["bf16"] / 2
+    assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < TOL["bf16"] / 2
 
 
 # ---------------------------------------------------------------------------
