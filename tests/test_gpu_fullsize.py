@@ -20,11 +20,11 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 from tests.stack_runner import GpuStack  # noqa: E402
 
-W2 = synth.WORKLOADS["chatglm6b_1blk_fwd_4x4x512"]
-W3 = synth.WORKLOADS["chatglm6b_1blk_ragged_8x4"]
-W4 = synth.WORKLOADS["chatglm6b_26blk_prefix_16x2x512"]
-W5 = synth.WORKLOADS["chatglm6b_26blk_ragged_32x1_recompute"]
-ONE = W2.shape
+W_FWD = synth.WORKLOADS["chatglm6b_1blk_fwd_4x4x512"]
+W_RAGGED = synth.WORKLOADS["chatglm6b_1blk_ragged_8x4"]
+W_PREFIX = synth.WORKLOADS["chatglm6b_26blk_prefix_16x2x512"]
+W_LONG = synth.WORKLOADS["chatglm6b_26blk_ragged_32x1_recompute"]
+ONE = W_FWD.shape
 TOL = 2e-2
 
 
@@ -47,9 +47,9 @@ def _shape(n):
     return synth.StackShape(n, ONE.hidden, ONE.num_heads, ONE.ffn_hidden, ONE.rotary_dim)
 
 
-def test_cfg2_forward_sampled_sequences(layers2):
+def test_1blk_fwd_4x4x512_sampled_sequences(layers2):
     """1 block, forward, 4 clients x 4 x 512 tokens, causal."""
-    b = W2.batch()
+    b = W_FWD.batch()
     x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
     g = GpuStack(ONE, [layers2[0]], "bf16")
     y = g.to_host(g.run(b, x, None))["y"]
@@ -58,15 +58,15 @@ def test_cfg2_forward_sampled_sequences(layers2):
         sb, r0, r1 = _seq_batch(b, s)
         yo, _ = oracle.stack_forward([layers2[0]], 1, x[r0:r1], sb, ONE, keep="none")
         err = rel_l2(y[r0:r1], yo)
-        print(f"[fullsize] cfg2 seq {s}: rel-L2 {err:.2e}", flush=True)
+        print(f"[fullsize] 1 block fwd 4x4x512 seq {s}: rel-L2 {err:.2e}", flush=True)
         assert err < TOL
 
 
-def test_cfg3_fwd_bwd_sampled_sequences(layers2):
+def test_1blk_ragged_8x4_fwd_bwd_sampled_sequences(layers2):
     """1 block, fwd+bwd, 8 clients x 4 ragged sequences U[128,1024]."""
-    b = W3.batch()
+    b = W_RAGGED.batch()
     x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
-    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W3.dy_std)
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W_RAGGED.dy_std)
     g = GpuStack(ONE, [layers2[0]], "bf16")
     res = g.to_host(g.run(b, x, dy))
     g.close()
@@ -76,7 +76,7 @@ def test_cfg3_fwd_bwd_sampled_sequences(layers2):
         yo, xs = oracle.stack_forward([layers2[0]], 1, x[r0:r1], sb, ONE)
         dxo, _ = oracle.stack_backward([layers2[0]], 1, xs, dy[r0:r1], sb, ONE)
         ey, edx = rel_l2(res["y"][r0:r1], yo), rel_l2(res["dx"][r0:r1], dxo)
-        print(f"[fullsize] cfg3 seq {s} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e}", flush=True)
+        print(f"[fullsize] 1 block ragged 8x4 seq {s} (L={r1 - r0}): y {ey:.2e} dx {edx:.2e}", flush=True)
         assert ey < TOL and edx < TOL
 
 
@@ -123,26 +123,26 @@ def _stack_sample(w, layers2, sample_seq, recompute):
     assert ey < TOL and edx < TOL
 
 
-def test_cfg4_26_blocks_prefix_sampled(layers2):
+def test_26blk_prefix_16x2x512_sampled(layers2):
     """26 blocks, fwd+bwd, 16 clients x 2 x 512 tokens, prefix-LM (25%)."""
-    _stack_sample(W4, layers2, 0, recompute=False)
+    _stack_sample(W_PREFIX, layers2, 0, recompute=False)
 
 
-def test_cfg5_26_blocks_ragged_recompute_sampled(layers2):
+def test_26blk_ragged_32x1_recompute_sampled(layers2):
     """26 blocks, fwd+bwd with per-block recompute, 32 clients x 1 sequence
     U[512,2048]; the shortest sequence is recomputed by the oracle."""
-    _stack_sample(W5, layers2, int(np.argmin(W5.batch().seqlens)), recompute=True)
+    _stack_sample(W_LONG, layers2, int(np.argmin(W_LONG.batch().seqlens)), recompute=True)
 
 
-def test_cfg4_recompute_is_bitwise_identical(layers2):
+def test_26blk_prefix_recompute_is_bitwise_identical(layers2):
     """Per-block recomputation changes no bit of y, dx or any weight gradient
     at the full 26-block shape."""
-    b = W4.batch()
-    n = W4.shape.num_layers
+    b = W_PREFIX.batch()
+    n = W_PREFIX.shape.num_layers
     layers = [layers2[l % 2] for l in range(n)]
     x = synth.activations(b.total_tokens, ONE.hidden, seed=0)
-    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W4.dy_std)
-    g = GpuStack(W4.shape, layers, "bf16")
+    dy = synth.upstream_grad(b.total_tokens, ONE.hidden, seed=0, std=W_PREFIX.dy_std)
+    g = GpuStack(W_PREFIX.shape, layers, "bf16")
     a = g.run(b, x, dy, recompute=False)
     ya, dxa = a["y"].clone(), a["dx"].clone()
     ga = [{k: v.clone() for k, v in gg.items()} for gg in a["grads"]]
@@ -233,7 +233,7 @@ def test_adam_full_stack_sampled():
     shaped stack in one launch (indices past 2^32), with the bf16 copy and
     the gradient clear: 200k sampled elements against the oracle."""
     from tests.test_gpu_optim import check_adam
-    n = W5.shape.num_layers * W5.shape.params_per_layer()
+    n = W_LONG.shape.num_layers * W_LONG.shape.params_per_layer()
     assert n > (1 << 32)
     gen = torch.Generator(device="cuda").manual_seed(0)
     p = torch.randn(n, generator=gen, device="cuda")
@@ -258,7 +258,7 @@ def test_adam_full_stack_sampled():
 def test_average_full_stack_sampled():
     """Averaging four replicas of every parameter of the 26-block stack (with
     bf16 copies): sampled elements against the oracle, replicas equal."""
-    n = W5.shape.num_layers * W5.shape.params_per_layer()
+    n = W_LONG.shape.num_layers * W_LONG.shape.params_per_layer()
     gen = torch.Generator(device="cuda").manual_seed(1)
     reps = [torch.randn(n, generator=gen, device="cuda") for _ in range(4)]
     c16 = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(4)]
