@@ -406,3 +406,41 @@ def test_glm_26_blocks_sampled(layers2):
     print(f"[fullsize] GLM 26 blocks seq {s} (L={r1 - r0}, P={int(sb.prefix_len[0])}): y {ey:.2e} dx {edx:.2e}",
           flush=True)
     assert ey < TOL and edx < TOL
+
+
+def test_long_batch_grads_add_over_client_parts(layers2):
+    """A 70000-token batch (35 clients x 2000 tokens, one ChatGLM-6B-shaped
+    block): the FFN weight-gradient GEMMs span more than 2^31 bytes along the
+    tokens and run cut into pieces.  Client batching mixes nothing across
+    clients and the weight gradients are sums over tokens, so the batch's
+    gradients equal the sum of three client groups' runs, and its y / dx rows
+    equal theirs, up to rounding: a GEMM splits the reduction of its partial
+    last round of tiles, which tiles that is depends on the token count, and
+    a changed fp32 summation order can move a bf16 intermediate by one unit
+    in the last place (2^-8 relative).  The gradients then agree to well
+    under 2^-9; a dropped, repeated or misplaced piece of the cut reduction
+    (at least 4464 of the 70000 rows) would be off by more than 0.2."""
+    b = synth.make_batch(35, 1, 2000, seed=7)
+    T = b.total_tokens
+    x = synth.activations(T, ONE.hidden, seed=7)
+    dy = synth.upstream_grad(T, ONE.hidden, seed=7, std=1e-2)
+    g = GpuStack(ONE, [layers2[0]], "bf16")
+    full = g.run(b, x, dy, recompute=True)
+    y_all, dx_all = full["y"].float().cpu().numpy(), full["dx"].float().cpu().numpy()
+    grads_all = {k: v.double().cpu().numpy() for k, v in full["grads"][0].items()}
+    del full
+    acc = {k: np.zeros_like(v) for k, v in grads_all.items()}
+    for part in (range(0, 12), range(12, 24), range(24, 35)):
+        sub, rows = b.subset_clients(list(part))
+        r = g.run(sub, x[rows], dy[rows], recompute=True)
+        assert rel_l2(r["y"].float().cpu().numpy(), y_all[rows]) < 5e-3
+        assert rel_l2(r["dx"].float().cpu().numpy(), dx_all[rows]) < 5e-3
+        for k, v in r["grads"][0].items():
+            acc[k] += v.double().cpu().numpy()
+        del r
+    g.close()
+    errs = {k: rel_l2(grads_all[k], acc[k]) for k in acc}
+    print(f"[fullsize] T={T}: batch vs sum of parts: "
+          + " ".join(f"{k}={v:.1e}" for k, v in sorted(errs.items())), flush=True)
+    assert all(e < 2e-3 for e in errs.values()), errs
+    torch.cuda.empty_cache()
