@@ -222,8 +222,10 @@ typedef struct {
 int fl_client_create(const fl_client_desc* desc, fl_client** out);
 int fl_client_destroy(fl_client* client);
 /* Workspace for T tokens (1 <= T <= 2^26): the logits [T, vocab rounded up
- * to 256] in the element type, per-token log-sum-exp, labels, ids and the
- * embedding-gradient plan.  Caller-allocated device memory. */
+ * to 256] in the element type, per-token log-sum-exp, labels, ids, the
+ * embedding-gradient plan, the final LayerNorm's output, statistics and
+ * gradient partials, and the GEMM's split-reduction scratch.
+ * Caller-allocated device memory, 16-byte aligned. */
 int fl_client_workspace_bytes(const fl_client* client, int64_t T, size_t* bytes);
 
 /* Embedding(x): out [T, hidden] (device) = rows ids[t] (host [T], each in
