@@ -46,7 +46,7 @@ CLASS_KERNELS = {
     "gemm_nt_bias_res": ("gemm_bf16_kernel<true, true, 2>",),
     "gemm_nt_bias_gelu": ("gemm_bf16_kernel<true, true, 3>",),
     "gemm_nn_gelu_bwd": ("gemm_bf16_kernel<true, false, 4>",),
-    "gemm_nn": ("gemm_bf16_kernel<true, false, 0>",),
+    "gemm_nn": ("gemm_bf16_kernel<true, false, 0>", "gemm_bf16_kernel<true, false, 6>"),
     "gemm_tn_acc": ("gemm_bf16_kernel<false, false",),
     "attn_fwd": ("::fwd_kernel<",),
     "attn_bwd": ("attn_delta_kernel", "::dkdv_kernel<", "::dq_kernel<"),
@@ -110,31 +110,49 @@ def _short_kernel(name: str) -> str:
     return name
 
 
-def _pmc_per_kernel(d: str, counter: str) -> dict:
-    """{kernel name: [dispatches, counter sum]} from a rocprofv3 --pmc CSV run."""
+def _pmc_dispatches(d: str, counter: str) -> list:
+    """[(queue, dispatch id, kernel name, counter value)] in dispatch order
+    from a rocprofv3 --pmc CSV run."""
     import csv
     import glob
-    out = {}
+    out = []
     for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
-            if r["Counter_Name"] != counter:
-                continue
-            e = out.setdefault(r["Kernel_Name"], [0, 0.0])
-            e[0] += 1
-            e[1] += float(r["Counter_Value"])
+            if r["Counter_Name"] == counter:
+                out.append((r["Queue_Id"], int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    out.sort(key=lambda x: (x[0], x[1]))
     return out
 
 
-def _class_totals(per_kernel: dict, cls: str):
-    pats = CLASS_KERNELS[cls]
-    launches, total = 0, 0.0
-    for name, (n, v) in per_kernel.items():
+def _class_of(name: str):
+    """(class, starts a launch) of a kernel name, or (None, False).  A class's
+    first pattern starts an engine launch; its other patterns are later parts
+    of the same launch (the attention backward's three kernels, a column sum's
+    finish)."""
+    for cls, pats in CLASS_KERNELS.items():
         hit = [p for p in pats if p in name]
         if hit:
-            total += v
-            if hit[0] == pats[0]:
-                launches += n
-    return launches, total
+            return cls, hit[0] == pats[0]
+    return None, False
+
+
+def _class_launches(dispatches) -> dict:
+    """{class: [engine launches, value total]} from (queue, id, name, value)
+    dispatches in order.  A dispatch of the same kernel as the one right
+    before it on its queue belongs to the same engine launch: a GEMM's
+    split-reduction fix-up, or the next piece of a GEMM cut along its
+    reduction."""
+    out = {}
+    prev = {}
+    for q, _, name, v in dispatches:
+        cls, first = _class_of(name)
+        if cls is not None:
+            e = out.setdefault(cls, [0, 0.0])
+            e[1] += v
+            if first and prev.get(q) != name:
+                e[0] += 1
+        prev[q] = name
+    return out
 
 
 def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
@@ -146,18 +164,17 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
     lines = []
     scale = {}
     for c, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
-        pk = _pmc_per_kernel(os.path.join(root, "copy_" + sub), c)
-        hits = [(n, v) for k, (n, v) in pk.items() if COPY_KERNEL in k]
-        n, v = sum(h[0] for h in hits), sum(h[1] for h in hits)
+        hits = [v for _, _, k, v in _pmc_dispatches(os.path.join(root, "copy_" + sub), c) if COPY_KERNEL in k]
+        n, v = len(hits), sum(hits)
         per = v / max(n, 1) * 1024.0
         scale[c] = copy_bytes / per
         lines.append(f"calibration {c} copy_bytes {copy_bytes} dispatches {n} counter_bytes_per_dispatch "
                      f"{per:.0f} factor {scale[c]:.4f}")
-    fetch = _pmc_per_kernel(os.path.join(root, "fetch"), "FETCH_SIZE")
-    write = _pmc_per_kernel(os.path.join(root, "write"), "WRITE_SIZE")
+    fetch = _class_launches(_pmc_dispatches(os.path.join(root, "fetch"), "FETCH_SIZE"))
+    write = _class_launches(_pmc_dispatches(os.path.join(root, "write"), "WRITE_SIZE"))
     for cls in CLASS_KERNELS:
-        n, fv = _class_totals(fetch, cls)
-        n2, wv = _class_totals(write, cls)
+        n, fv = fetch.get(cls, (0, 0.0))
+        n2, wv = write.get(cls, (0, 0.0))
         if n == 0:
             continue
         fb = fv / n * 1024.0 * scale["FETCH_SIZE"]
@@ -168,7 +185,9 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
 
 
 def summarize_trace(root: str) -> str:
-    """Per-kernel table from a rocprofv3 --kernel-trace --stats CSV run."""
+    """Per-kernel table from a rocprofv3 --kernel-trace --stats CSV run, then
+    per class the engine launches (grouped as in _class_launches) and their
+    average duration."""
     import csv
     import glob
     rows = []
@@ -179,16 +198,13 @@ def summarize_trace(root: str) -> str:
     for r in rows:
         out.append(f"{_short_kernel(r['Name'])[:72]:<72} {int(r['Calls']):>6} {float(r['AverageNs']) / 1e3:>10.1f} "
                    f"{float(r['TotalDurationNs']) / 1e6:>10.2f} {float(r['Percentage']):>6.2f}")
-    by_cls = {}
-    for r in rows:
-        for cls, pats in CLASS_KERNELS.items():
-            hit = [p for p in pats if p in r["Name"]]
-            if hit:
-                e = by_cls.setdefault(cls, [0, 0.0])
-                e[1] += float(r["TotalDurationNs"])
-                if hit[0] == pats[0]:
-                    e[0] += int(r["Calls"])
-                break
+    disp = []
+    for f in glob.glob(os.path.join(root, "**", "*kernel_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            disp.append((r["Queue_Id"], int(r["Dispatch_Id"]), r["Kernel_Name"],
+                         float(r["End_Timestamp"]) - float(r["Start_Timestamp"])))
+    disp.sort(key=lambda x: (x[0], x[1]))
+    by_cls = _class_launches(disp)
     out.append("")
     out.append(f"{'class':<20} {'launches':>8} {'avg_us_per_launch':>18}")
     for cls, (n, t) in sorted(by_cls.items(), key=lambda kv: -kv[1][1]):
