@@ -97,6 +97,65 @@ def committed_traffic(cls: str, workload: str):
     return None
 
 
+PUBLISHED_SCLK_MHZ = 2400.0   # the clock the published matrix-core peaks assume
+
+
+def sclk_path():
+    """The amdgpu driver's shader-clock readout (pp_dpm_sclk) of device 0, or
+    None where it is not readable."""
+    import glob
+    paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+    if len(paths) == 1:
+        return paths[0]
+    try:
+        import torch
+        pr = torch.cuda.get_device_properties(0)
+        bus = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
+        for q in paths:
+            if os.path.basename(os.path.realpath(os.path.dirname(q))) == bus:
+                return q
+    except Exception:
+        pass
+    return None
+
+
+class ClockSampler:
+    """Mean shader clock over a window: the current level of pp_dpm_sclk (the
+    line marked '*'), read every 20 ms from a thread while the GPU runs."""
+
+    def __init__(self, path):
+        import threading
+        self.path, self.samples, self._stop = path, [], threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True) if path else None
+
+    def _read(self):
+        import re
+        try:
+            with open(self.path) as fh:
+                m = re.search(r"(\d+)\s*Mhz\s*\*", fh.read(), re.IGNORECASE)
+            return float(m.group(1)) if m else None
+        except OSError:
+            return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(0.02)
+
+    def start(self):
+        if self._t:
+            self._t.start()
+        return self
+
+    def stop(self):
+        if self._t:
+            self._stop.set()
+            self._t.join()
+        return (sum(self.samples) / len(self.samples)) if self.samples else None
+
+
 def _short_kernel(name: str) -> str:
     name = name[5:] if name.startswith("void ") else name
     depth = 0
@@ -236,8 +295,9 @@ def vocab_padded(w: synth.Workload) -> int:
 
 
 def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
-    """Per step: GEMM 24 H^2 per token per block forward, 48 H^2 backward
-    (24 H^2 with frozen weights: input gradients only); attention 4 H per
+    """Per step: GEMM 8 H^2 + 4 H F per token per block forward (24 H^2 at
+    F = 4 H), twice that backward (once with frozen weights: input gradients
+    only); attention 4 H per
     visible (query, key) pair forward, 8 H backward, a P-tuning v2 prefix
     adding L_p pairs per token.  The whole split model adds the final
     linear layer: 2 V H per token forward, 2 V H backward for the input
@@ -250,9 +310,11 @@ def algorithmic_flops(w: synth.Workload, b: synth.Batch) -> dict:
         L = float(b.seqlens[s])
         P = float(b.prefix_len[s]) if b.mask == "prefix" else 0.0
         pairs += L * (L + 1) / 2 + (P * (P - 1) / 2 if P > 1 else 0.0)
-    mult_g = (48 if w.frozen else 72) if w.backward else 24
+    F = w.shape.ffn_hidden
+    fwd_g = 8.0 * H * H + 4.0 * H * F   # QKV 6 H^2, out-projection 2 H^2, FFN 4 H F
+    mult_g = ((2 if w.frozen else 3) if w.backward else 1) * fwd_g
     mult_a = 12 if w.backward else 4
-    g = mult_g * H * H * T * total_layers(w)
+    g = mult_g * T * total_layers(w)
     a = mult_a * H * pairs * total_layers(w)
     head = (2.0 + 2.0 + (0.0 if w.frozen else 2.0)) * w.vocab * H * T if w.vocab else 0.0
     return {"gemm": g, "attention": a, "lm_head": head, "total": g + a + head, "pairs": pairs}
@@ -576,11 +638,13 @@ def main() -> int:
         F.fl_stack_profile(h, not args.no_profile)
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
+    clock = ClockSampler(sclk_path()).start()
     marks[0].record(stream)
     for i in range(args.steps):
         step()
         marks[i + 1].record(stream)
     torch.cuda.synchronize()
+    sclk = clock.stop()
     ms = marks[0].elapsed_time(marks[-1]) / args.steps
     per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     prof = {}
@@ -673,6 +737,13 @@ def main() -> int:
         "hardware_tflop_per_step": round(hw_flops / 1e12, 3) if hw_flops else None,
         "gemm_mfma_util": round(gemm_fl / (gemm_ms / 1e3) / (peak * 1e12), 4) if gemm_ms else None,
         "algorithmic_tflop_per_step": round(flops["total"] / 1e12, 3),
+        # the same utilisations against the peak at the shader clock measured
+        # during the timed steps (the published peak assumes 2400 MHz)
+        "sclk_mhz_mean": round(sclk, 1) if sclk else None,
+        "mfma_util_at_clock": (round(flops["total"] / (ms / 1e3) / (peak * 1e12) * PUBLISHED_SCLK_MHZ / sclk, 4)
+                               if sclk else None),
+        "gemm_mfma_util_at_clock": (round(gemm_fl / (gemm_ms / 1e3) / (peak * 1e12) * PUBLISHED_SCLK_MHZ / sclk, 4)
+                                    if sclk and gemm_ms else None),
         "roofline": roofline,
         "kernels": kernels,
         "cpu_baseline": None,

@@ -1,0 +1,136 @@
+"""Host logic of bench.py: the algorithmic work it divides by, the grouping of
+profiler dispatches into engine launches, the stale-counter rule and the
+shader-clock readout.  CPU only."""
+
+import csv
+import os
+
+import numpy as np
+import pytest
+
+import bench
+import synth
+
+
+def _allowed_pairs_brute(b):
+    """Visible (query, key) pairs by enumeration: causal j <= i; prefix-LM
+    j <= max(i, P - 1) (Section 3.3 batches; GLM's bidirectional context)."""
+    n = 0
+    for s in range(b.num_seqs):
+        L = int(b.seqlens[s])
+        P = int(b.prefix_len[s]) if b.mask == "prefix" else 0
+        for i in range(L):
+            n += sum(1 for j in range(L) if j <= max(i, P - 1))
+    return n
+
+
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+def test_attention_pairs_match_enumeration(mask):
+    b = synth.make_batch(3, 2, (5, 40), mask=mask, seed=4)
+    w = synth.WORKLOADS["tiny_2blk_fp32"]
+    fl = bench.algorithmic_flops(w, b)
+    assert fl["pairs"] == _allowed_pairs_brute(b)
+
+
+def test_gemm_flops_are_the_sum_of_the_block_products():
+    """2 m n k per product: forward QKV (T x 3H x H), out-projection (T x H x
+    H), FFN1 (T x F x H), FFN2 (T x H x F); the backward repeats each as an
+    input-gradient and a weight-gradient product (input gradients only when
+    the weights are frozen)."""
+    b = synth.make_batch(2, 2, (9, 30), seed=1)
+    for name in ("tiny_2blk_fp32", "chatglm6b_26blk_ragged_32x1_recompute",
+                 "chatglm6b_26blk_ptuning128_ragged_32x1_recompute"):
+        w = synth.WORKLOADS[name]
+        H, F, T = w.shape.hidden, w.shape.ffn_hidden, b.total_tokens
+        fwd = 2 * T * (3 * H * H + H * H + F * H + H * F)
+        per_block = fwd * (1 + (1 if w.frozen else 2) if w.backward else 1)
+        assert bench.algorithmic_flops(w, b)["gemm"] == pytest.approx(per_block * bench.total_layers(w), rel=1e-12)
+
+
+def test_gemm_flops_follow_the_ffn_width():
+    b = synth.make_batch(1, 1, (16, 16), seed=0)
+    w = synth.WORKLOADS["tiny_2blk_fp32"]
+    import dataclasses
+    w2 = dataclasses.replace(w, shape=dataclasses.replace(w.shape, ffn_hidden=3 * w.shape.hidden))
+    H, T = w.shape.hidden, b.total_tokens
+    d = bench.algorithmic_flops(w, b)["gemm"] - bench.algorithmic_flops(w2, b)["gemm"]
+    # one H-wide slice of FFN width less: 4 H^2 per token forward, x3 with the backward
+    assert d == pytest.approx(3 * 4 * H * H * T * bench.total_layers(w), rel=1e-12)
+
+
+def _disp(*names):
+    return [("1", i, n, 1.0) for i, n in enumerate(names)]
+
+
+GEMM_RES = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, true, 2>(G2Args)"
+GEMM_TN = "flglm::(anonymous namespace)::gemm_bf16_kernel<false, false, 5>(G2Args)"
+LN = "void flglm::ln_fwd_kernel<bf16, 8>(...)"
+DELTA, DKDV, DQ = "attn_delta_kernel<bf16, 128>", "flglm::(anonymous namespace)::dkdv_kernel<128>", \
+    "flglm::(anonymous namespace)::dq_kernel<128>"
+
+
+def test_fixup_dispatch_joins_its_launch():
+    """A GEMM whose last round is split runs the same kernel twice in a row
+    (main, then fix-up): one engine launch; the same GEMM again after another
+    kernel is a new launch."""
+    r = bench._class_launches(_disp(GEMM_RES, GEMM_RES, LN, GEMM_RES, LN, GEMM_TN, GEMM_TN, GEMM_TN))
+    assert r["gemm_nt_bias_res"] == [2, 3.0]
+    assert r["gemm_tn_acc"] == [1, 3.0]   # a reduction cut into three pieces
+    assert r["layernorm_fwd"] == [2, 2.0]
+
+
+def test_multi_kernel_class_counts_once():
+    r = bench._class_launches(_disp(DELTA, DKDV, DQ, LN, DELTA, DKDV, DQ))
+    assert r["attn_bwd"] == [2, 6.0]
+
+
+def test_queues_are_grouped_separately():
+    d = [("1", 0, GEMM_RES, 1.0), ("2", 1, GEMM_RES, 1.0)]
+    assert bench._class_launches(d)["gemm_nt_bias_res"] == [2, 2.0]
+
+
+def test_summarize_trace_on_a_synthetic_run(tmp_path):
+    rows = [(GEMM_RES, 0, 100), (GEMM_RES, 100, 130), (LN, 130, 140), (GEMM_RES, 140, 240)]
+    with open(tmp_path / "run_kernel_trace.csv", "w", newline="") as fh:
+        wr = csv.writer(fh)
+        wr.writerow(["Queue_Id", "Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        for i, (n, a, e) in enumerate(rows):
+            wr.writerow(["1", i, n, a * 1000, e * 1000])
+    with open(tmp_path / "run_kernel_stats.csv", "w", newline="") as fh:
+        wr = csv.writer(fh)
+        wr.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage"])
+        wr.writerow([GEMM_RES, 3, 230000, 76666.7, 95.8])
+        wr.writerow([LN, 1, 10000, 10000, 4.2])
+    out = bench.summarize_trace(str(tmp_path))
+    line = [l for l in out.splitlines() if l.startswith("gemm_nt_bias_res")][0].split()
+    assert int(line[1]) == 2 and float(line[2]) == pytest.approx(115.0)   # (130 + 100) us over 2 launches
+
+
+def test_committed_traffic_goes_stale_with_the_sources(tmp_path, monkeypatch):
+    h = bench.class_source_hash("gemm_tn_acc")
+    f = tmp_path / "server_stack_kernels_w_hbm_traffic.txt"
+    f.write_text(f"class gemm_tn_acc launches 4 hbm_bytes_per_launch 1234 src {h}\n"
+                 f"class attn_fwd launches 4 hbm_bytes_per_launch 99 src 0000000000000000\n")
+    monkeypatch.setattr(bench, "traffic_file", lambda w: str(f))
+    assert bench.committed_traffic("gemm_tn_acc", "w") == 1234
+    assert bench.committed_traffic("attn_fwd", "w") is None      # hash of other sources
+    assert bench.committed_traffic("layernorm_fwd", "w") is None  # not measured
+
+
+@pytest.mark.parametrize("text,mhz", [("0: 500Mhz\n1: 1938Mhz *\n2: 2400Mhz\n", 1938.0),
+                                      ("S: 112Mhz *\n0: 500Mhz\n1: 2400Mhz\n", 112.0),
+                                      ("0: 500Mhz\n1: 2400Mhz\n", None)])
+def test_clock_readout(tmp_path, text, mhz):
+    f = tmp_path / "pp_dpm_sclk"
+    f.write_text(text)
+    assert bench.ClockSampler(str(f))._read() == mhz
+
+
+def test_clock_sampler_mean_and_absent_source(tmp_path):
+    import time
+    f = tmp_path / "pp_dpm_sclk"
+    f.write_text("0: 500Mhz\n1: 2000Mhz *\n")
+    c = bench.ClockSampler(str(f)).start()
+    time.sleep(0.08)
+    assert c.stop() == 2000.0 and len(c.samples) >= 2
+    assert bench.ClockSampler(None).start().stop() is None
