@@ -60,6 +60,8 @@ def test_stack_desc_validation(desc, code):
 
 
 @pytest.mark.parametrize("cu,csp,pre,code", [
+    ([0], [0], None, F.FL_ERR_SEQLENS),                      # empty batch: no sequences, no tokens
+    ([0, 3], [0], None, F.FL_ERR_CLIENTS),                   # no clients
     ([0, 3, 3, 7], [0, 1, 3], None, F.FL_ERR_SEQLENS),      # empty sequence
     ([1, 3, 7], [0, 1, 2], None, F.FL_ERR_SEQLENS),         # cu[0] != 0
     ([0, 3, 7], [0, 2, 2], None, F.FL_ERR_CLIENTS),         # client without sequences
