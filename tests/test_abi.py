@@ -237,3 +237,27 @@ def test_client_handle_validation_host_only():
                                  None, WS, ws_n, None)
     assert rc == F.FL_ERR_ARG and "without a final LayerNorm" in F.fl_last_error()
     F.fl_client_destroy(h)
+
+
+def test_missing_library_raises_instead_of_falling_back():
+    """Without the built HIP library every entry point raises: there is no
+    CPU path to fall back on (fresh interpreter, library path pointed at a
+    file that does not exist)."""
+    import subprocess
+    import sys
+    import textwrap
+    code = textwrap.dedent('''
+        import sys
+        from paper_2406_14898_amd import flglm as F, ServerStack
+        F.load.__defaults__ = ("/nonexistent/libflglm.so",)
+        try:
+            ServerStack(2, 256, 4, 1024, 32, dtype="f32")
+        except F.FlglmError as e:
+            print("RAISED", e)
+            sys.exit(0)
+        sys.exit(3)
+    ''')
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "HIP library not built" in r.stdout
