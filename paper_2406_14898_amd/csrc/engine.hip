@@ -111,8 +111,15 @@ hipError_t timed(fl_stack* st, hipStream_t s, int cls, double flops, double byte
   fl_stack::Rec r{cls, nullptr, nullptr, flops, bytes};
   hipError_t e = take_event(st, &r.a);
   if (e != hipSuccess) return e;
-  if ((e = take_event(st, &r.b)) != hipSuccess) return e;
-  if ((e = hipEventRecord(r.a, s)) != hipSuccess) return e;
+  if ((e = take_event(st, &r.b)) != hipSuccess) {
+    st->pool.push_back(r.a);
+    return e;
+  }
+  if ((e = hipEventRecord(r.a, s)) != hipSuccess) {
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+    return e;
+  }
   e = launch();
   hipError_t e2 = hipEventRecord(r.b, s);
   st->recs.push_back(r);
