@@ -218,3 +218,35 @@ def test_ptuning_stack_matches_oracle(frozen, mask, num_prefix):
     dx, grads = oracle.stack_backward(layers, shape.num_layers, xs, dy, b, shape, want)
     assert all(set(r) == set(w) for r, w in zip(res["grads"], grads))
     _check(res, (y, dx, grads), b, TOL["bf16"])
+
+
+SHAPES = {
+    # widths that are not powers of two, an FFN width other than 4 H, both
+    # head dims, and the rotary widths at their ends and in between
+    "h768_d128_f2304_r96": synth.StackShape(num_layers=2, hidden=768, num_heads=6, ffn_hidden=2304, rotary_dim=96),
+    "h1280_d64_f3328_r64full": synth.StackShape(num_layers=2, hidden=1280, num_heads=20, ffn_hidden=3328,
+                                                rotary_dim=64),
+    "h512_d128_f1536_r0": synth.StackShape(num_layers=2, hidden=512, num_heads=4, ffn_hidden=1536, rotary_dim=0),
+    "h256_d128_f768_r128full": synth.StackShape(num_layers=2, hidden=256, num_heads=2, ffn_hidden=768,
+                                                rotary_dim=128),
+}
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("name", sorted(SHAPES))
+def test_other_block_shapes_match_oracle(name, dt):
+    """The stack at block shapes other than the two workload shapes: every
+    GEMM width a multiple of 256 but not of 512 somewhere, 9- and 13-tile
+    column counts, no rotary at all and rotary over the whole head; a ragged
+    prefix-LM batch with a one-token sequence, across three clients."""
+    shape = SHAPES[name]
+    cu = np.array([0, 1, 70, 203, 260, 389], np.int32)
+    csp = np.array([0, 2, 3, 5], np.int32)
+    pre = np.array([1, 17, 0, 57, 129], np.int32)
+    b = synth.Batch(cu, csp, "prefix", pre)
+    layers, x, dy = _inputs(b, dt, seed=11, shape=shape)
+    g = GpuStack(shape, layers, dt)
+    res = g.to_host(g.run(b, x, dy))
+    g.close()
+    worst = _check(res, _oracle(layers, x, dy, b, shape), b, TOL[dt])
+    print(f"[shapes] {name} {dt}: worst rel-L2 {worst:.2e}", flush=True)
