@@ -550,7 +550,7 @@ def main() -> int:
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs the server stack on one GPU only; "
+        print(json.dumps({"error": "bench.py runs the server stack on one GPU only; "
                                    f"--gpus {args.gpus} is not supported (multi-GPU sharding is design-only)"}))
         return 2
 
