@@ -169,16 +169,19 @@ def _short_kernel(name: str) -> str:
     return name
 
 
-def _pmc_dispatches(d: str, counter: str) -> list:
-    """[(queue, dispatch id, kernel name, counter value)] in dispatch order
-    from a rocprofv3 --pmc CSV run."""
+def _pmc_dispatches(d: str, counter: str, with_duration: bool = False) -> list:
+    """[(queue, dispatch id, kernel name, counter value[, duration ns])] in
+    dispatch order from a rocprofv3 --pmc CSV run."""
     import csv
     import glob
     out = []
     for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
             if r["Counter_Name"] == counter:
-                out.append((r["Queue_Id"], int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+                row = (r["Queue_Id"], int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
+                if with_duration:
+                    row += (float(r["End_Timestamp"]) - float(r["Start_Timestamp"]),)
+                out.append(row)
     out.sort(key=lambda x: (x[0], x[1]))
     return out
 
@@ -241,6 +244,40 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
         lines.append(f"class {cls} launches {n} fetch_bytes_per_launch {fb:.0f} write_bytes_per_launch {wb:.0f} "
                      f"hbm_bytes_per_launch {fb + wb:.0f} src {class_source_hash(cls)}")
     return "\n".join(lines)
+
+
+def summarize_mfma(root: str, bench_json: str = "") -> str:
+    """Per class from one rocprofv3 --pmc "MfmaFlopsBF16 MfmaUtil" run under
+    root: MFMA flops per engine launch as the hardware counts them (bf16 MFMA
+    ops x 512), the same per launch from the engine's algorithmic count (the
+    bench line in bench_json, when given), and the matrix cores' busy share
+    while the class ran (MfmaUtil, weighted by dispatch duration)."""
+    fl = _class_launches(_pmc_dispatches(root, "MfmaFlopsBF16"))
+    util = {}
+    for _, _, name, v, dur in _pmc_dispatches(root, "MfmaUtil", with_duration=True):
+        cls, _ = _class_of(name)
+        if cls is not None:
+            e = util.setdefault(cls, [0.0, 0.0])
+            e[0] += v * dur
+            e[1] += dur
+    alg = {}
+    if bench_json:
+        d = json.loads([l for l in open(bench_json) if l.startswith("{")][-1])
+        for k, v in d["kernels"].items():
+            if "tflops" in v:
+                alg[k] = v["tflops"] * 1e12 * v["avg_launch_us"] * 1e-6
+    out = [f"{'class':<20} {'launches':>8} {'counter_flop_per_launch':>24} {'algorithmic_flop_per_launch':>28} "
+           f"{'ratio':>7} {'mfma_busy_pct':>14}"]
+    for cls in CLASS_KERNELS:
+        if cls not in fl or fl[cls][1] == 0:
+            continue
+        n, v = fl[cls]
+        per = v / max(n, 1)
+        a = alg.get(cls)
+        u = util.get(cls)
+        out.append(f"{cls:<20} {n:>8} {per:>24.4e} " + (f"{a:>28.4e} {per / a:>7.4f}" if a else f"{'-':>28} {'-':>7}") +
+                   (f" {u[0] / u[1]:>14.1f}" if u and u[1] > 0 else f" {'-':>14}"))
+    return "\n".join(out)
 
 
 def summarize_trace(root: str) -> str:
@@ -530,6 +567,9 @@ def main() -> int:
                     help="only run the counter-calibration copy kernel over MIB MiB")
     ap.add_argument("--summarize-traffic", metavar="DIR",
                     help="print the HBM traffic summary of rocprofv3 --pmc runs under DIR (no GPU)")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="print MFMA counter summary of a rocprofv3 --pmc 'MfmaFlopsBF16 MfmaUtil' run")
+    ap.add_argument("--bench-json", default="", help="bench line to compare --summarize-mfma with")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print the per-kernel table of a rocprofv3 --kernel-trace --stats run (no GPU)")
     ap.add_argument("--copy-mib", type=int, default=1024, help="size the calibration run used")
@@ -541,6 +581,9 @@ def main() -> int:
     args = ap.parse_args()
     if args.summarize_traffic:
         print(summarize_traffic(args.summarize_traffic, args.copy_mib, args.workload))
+        return 0
+    if args.summarize_mfma:
+        print(summarize_mfma(args.summarize_mfma, args.bench_json))
         return 0
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))

@@ -134,3 +134,23 @@ def test_clock_sampler_mean_and_absent_source(tmp_path):
     time.sleep(0.08)
     assert c.stop() == 2000.0 and len(c.samples) >= 2
     assert bench.ClockSampler(None).start().stop() is None
+
+
+def test_summarize_mfma_on_a_synthetic_run(tmp_path):
+    rows = [(GEMM_RES, "MfmaFlopsBF16", 1000.0, 0, 100), (GEMM_RES, "MfmaUtil", 50.0, 0, 100),
+            (GEMM_RES, "MfmaFlopsBF16", 24.0, 100, 110), (GEMM_RES, "MfmaUtil", 10.0, 100, 110),
+            (LN, "MfmaFlopsBF16", 0.0, 110, 120), (LN, "MfmaUtil", 0.0, 110, 120)]
+    with open(tmp_path / "run_counter_collection.csv", "w", newline="") as fh:
+        wr = csv.writer(fh)
+        wr.writerow(["Queue_Id", "Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+                     "End_Timestamp"])
+        for i, (n, c, v, a, e) in enumerate(rows):
+            wr.writerow(["1", i // 2, n, c, v, a, e])
+    bj = tmp_path / "b.json"
+    bj.write_text('{"kernels": {"gemm_nt_bias_res": {"tflops": 1e-6, "avg_launch_us": 1024.0}}}\n')
+    out = bench.summarize_mfma(str(tmp_path), str(bj))
+    line = [l for l in out.splitlines() if l.startswith("gemm_nt_bias_res")][0].split()
+    # main + fix-up dispatch: one launch of 1024 flops; busy share weighted by duration
+    assert int(line[1]) == 1 and float(line[2]) == 1024.0 and float(line[4]) == pytest.approx(1.0)
+    assert float(line[5]) == pytest.approx((50.0 * 100 + 10.0 * 10) / 110, abs=0.05)
+    assert not any(l.startswith("layernorm_fwd") for l in out.splitlines())
