@@ -203,17 +203,20 @@ def _class_launches(dispatches) -> dict:
     dispatches in order.  A dispatch of the same kernel as the one right
     before it on its queue belongs to the same engine launch: a GEMM's
     split-reduction fix-up, or the next piece of a GEMM cut along its
-    reduction."""
+    reduction.  A class's later kernel continues the launch its first kernel
+    began, unless another class ran in between (a column-sum finish whose
+    partial sums a GEMM epilogue produced is a launch of its own)."""
     out = {}
-    prev = {}
-    for q, _, name, v in dispatches:
+    prev, prev_cls = {}, {}
+    for d in dispatches:
+        q, name, v = d[0], d[2], d[3]
         cls, first = _class_of(name)
         if cls is not None:
             e = out.setdefault(cls, [0, 0.0])
             e[1] += v
-            if first and prev.get(q) != name:
+            if prev.get(q) != name and (first or prev_cls.get(q) != cls):
                 e[0] += 1
-        prev[q] = name
+        prev[q], prev_cls[q] = name, cls
     return out
 
 

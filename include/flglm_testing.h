@@ -39,12 +39,16 @@ extern "C" {
  * b_rows > 0: B holds only that many rows (its N index for NT, its
  * reduction index for NN and TN); the rest read as zero and are never
  * touched (0: B is complete).
+ * colsum (NULL: none): for bf16 NN GELU_BWD on the LDS-DMA kernel only
+ * (FL_ERR_ARG otherwise), device fp32 [ceil(M/256)][N] that receives, per
+ * 256-row block, the column sums of the stored C (the partial layout of the
+ * bias-gradient column sums).
  * Requirements: N % 128 == 0 (bf16) or N % 64 == 0 (fp32); K % 64 == 0 for
  * NT and NN; M % 8 == 0 for TN. */
 int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, void* C, int M, int N, int K,
                  int64_t lda, int64_t ldb, int64_t ldc, const void* bias, const void* R, int64_t ldr, void* C2,
                  int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, int b_rows,
-                 float res_scale, void* stream);
+                 float res_scale, float* colsum, void* stream);
 
 /* LayerNorm over rows of x [T, H] (H % 256 == 0, H <= 4096). */
 int fl_test_layernorm_fwd(int dtype, const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,

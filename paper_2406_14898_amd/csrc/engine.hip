@@ -522,11 +522,19 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   g = GemmDesc();
   g.A = dy; g.B = p.w_2; g.C = w.dz; g.M = T; g.N = F; g.K = H; g.lda = H; g.ldb = F; g.ldc = F;
   g.Z = a.z; g.ldz = F;
+  // db_1 = column sums of dz: formed per 256-row tile in the GEMM's epilogue
+  // where the kernel supports it (no second pass over dz), else below
+  const bool b1_fused = train_w && gemm_fuses_colsum(dt, GEMM_NN, EPI_GELU_BWD, g);
+  if (b1_fused) g.colsum = w.part;
   LAUNCH(FL_PROF_GEMM_NN_GELU_BWD, gemm_flops(T, F, H), gemm_bytes(T, F, H, E, 2 * E),
          gemm(dt, GEMM_NN, EPI_GELU_BWD, with_part(g, plan), s));
   // z = w W_1^T + b_1
   if (train_w) {
-    if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) return rc;
+    if (b1_fused) {
+      LAUNCH(FL_PROF_COLSUM, 0, 4.0 * colsum_blocks(T) * F, colsum_finish(w.part, colsum_blocks(T), F, gr.b_1, s));
+    } else if ((rc = colsum_into(st, dt, w.dz, F, T, F, gr.b_1, w, s))) {
+      return rc;
+    }
     g = GemmDesc();
     g.A = w.dz; g.B = a.w; g.C = gr.w_1; g.M = F; g.N = H; g.K = T; g.lda = F; g.ldb = H; g.ldc = H;
     LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(F, H, T), gemm_bytes(F, H, T, E, 8),

@@ -61,6 +61,9 @@ struct G2Args {
   int tail, splits, fixup;
   int nb;  // rows of B that exist (see GemmDesc::b_rows)
   float res_scale;
+  // EPI_GELU_BWD: per 256-row tile, the column sums of the stored C (fp32
+  // [tiles_m][N]), or null
+  float* colsum;
 };
 
 // K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
@@ -365,6 +368,9 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   barrier();  // every wave is done with the operand tiles
   const int n = n0 + 4 * lane;
   float bias[4] = {0.f, 0.f, 0.f, 0.f};
+  // EPI_GELU_BWD with colsum: this lane's four columns summed over its rows
+  // (the stored, rounded values), in row order
+  float csum[4] = {0.f, 0.f, 0.f, 0.f};
   if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
     Vec4<bf16> b;
     b.load(p.bias + n);
@@ -429,6 +435,10 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
         Vec4<bf16> o;
           o.set(v);
           if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
+          if constexpr (EPI == EPI_GELU_BWD) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) csum[e] += o.get(e);
+          }
           if constexpr (EPI == EPI_BIAS_GELU) {
             float g[4];
 #pragma unroll
@@ -443,6 +453,24 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     // the second half, or the next tile's loads, overwrite the staging area
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     barrier();
+  }
+  if constexpr (EPI == EPI_GELU_BWD) {
+    if (p.colsum) {
+      // the eight waves' partial column sums, added in wave order (the
+      // operand tiles are free: every wave has passed the barrier above)
+      float* cs = reinterpret_cast<float*>(&smem[0][0][0]);
+      st16(cs + wave * kBN + 4 * lane, __builtin_bit_cast(u32x4, f32x4{csum[0], csum[1], csum[2], csum[3]}));
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();
+      if (tid < kBN) {
+        float t = 0.f;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) t += cs[w2 * kBN + tid];
+        p.colsum[(long)tm * p.N + n0 + tid] = t;
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();  // the next tile's loads overwrite cs
+    }
   }
   }
 }
@@ -474,6 +502,7 @@ hipError_t launch2(const GemmDesc& d, hipStream_t st) {
   a.part = d.part; a.tail = 0; a.splits = 1; a.fixup = 0;
   a.nb = gemm_b_rows(BKc, d);
   a.res_scale = d.res_scale;
+  a.colsum = EPI == EPI_GELU_BWD ? d.colsum : nullptr;
   const int tiles = ((d.M + kBM - 1) / kBM) * (d.N / kBN);
   if (tiles == 0) return hipSuccess;
   const int cus = num_cus();
@@ -517,6 +546,11 @@ bool gemm_bf16_dma_ok(GemmLayout layout, const GemmDesc& d) {
   if (ak && (long)kBM * d.lda * 2 >= lim) return false;
   if (bk && (long)kBN * d.ldb * 2 >= lim) return false;
   return true;
+}
+
+bool gemm_fuses_colsum(DType dt, GemmLayout layout, int epi, const GemmDesc& d) {
+  return dt == DT_BF16 && layout == GEMM_NN && epi == EPI_GELU_BWD && kBM == kColsumRows &&
+         gemm_bf16_dma_ok(layout, d);
 }
 
 hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st) {

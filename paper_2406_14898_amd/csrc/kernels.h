@@ -32,6 +32,10 @@ struct GemmDesc {
   int b_rows = 0;
   // Scale of R in EPI_BIAS_RES and EPI_RES (1: plain residual add).
   float res_scale = 1.f;
+  // EPI_GELU_BWD where gemm_fuses_colsum() holds: fp32 [ceil(M / 256)][N]
+  // receives, per 256-row block, the column sums of the stored C (the
+  // layout colsum_partial writes, so colsum_finish completes them).
+  float* colsum = nullptr;
 };
 // Rows of B a kernel may read for a layout and shape.
 inline int gemm_b_rows(bool b_kcontig, const GemmDesc& d) {
@@ -53,6 +57,9 @@ enum GemmEpi : int {
 hipError_t gemm(DType dt, GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
 // bf16 LDS-DMA kernel (gemm_bf16.hip), used by gemm() for the shapes it takes.
 bool gemm_bf16_dma_ok(GemmLayout layout, const GemmDesc& d);
+// Whether gemm() fills d.colsum for this call (bf16 GeLU' input-gradient
+// GEMMs on the LDS-DMA kernel); otherwise the caller sums the columns itself.
+bool gemm_fuses_colsum(DType dt, GemmLayout layout, int epi, const GemmDesc& d);
 hipError_t gemm_bf16_dma(GemmLayout layout, int epi, const GemmDesc& d, hipStream_t st);
 
 // Batch bookkeeping: position of every packed row inside its own sequence.

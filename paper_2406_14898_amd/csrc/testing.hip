@@ -30,7 +30,7 @@ extern "C" {
 int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, void* C, int M, int N, int K,
                  int64_t lda, int64_t ldb, int64_t ldc, const void* bias, const void* R, int64_t ldr, void* C2,
                  int64_t ldc2, const void* Z, int64_t ldz, float* part, int64_t part_bytes, int b_rows,
-                 float res_scale, void* stream) {
+                 float res_scale, float* colsum, void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!A || !B || !C) return set_error(FL_ERR_NULL, "A / B / C is NULL");
   if (!al16(A) || !al16(B) || !al16(C)) return set_error(FL_ERR_ALIGN, "A / B / C not 16-byte aligned");
@@ -70,6 +70,12 @@ int fl_test_gemm(int dtype, int layout, int epi, const void* A, const void* B, v
   d.part = part; d.part_bytes = part ? (size_t)part_bytes : 0;
   d.b_rows = b_rows;
   d.res_scale = res_scale;
+  if (colsum) {
+    if (!al16(colsum)) return set_error(FL_ERR_ALIGN, "colsum misaligned");
+    if (!gemm_fuses_colsum((DType)dtype, (GemmLayout)layout, epi, d))
+      return set_error(FL_ERR_ARG, "this GEMM does not produce column sums");
+    d.colsum = colsum;
+  }
   return herr(gemm((DType)dtype, (GemmLayout)layout, epi, d, (hipStream_t)stream));
 }
 

@@ -118,7 +118,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                   P(ctypes.c_double)],
         "fl_test_gemm": [ctypes.c_int] * 3 + [vp] * 3 + [ctypes.c_int] * 3 + [i64] * 3 + [vp, vp, i64, vp, i64, vp,
                                                                                           i64, vp, i64, ctypes.c_int,
-                                                                                          ctypes.c_float, vp],
+                                                                                          ctypes.c_float, vp, vp],
         "fl_test_layernorm_fwd": [ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                   vp],
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
@@ -375,13 +375,14 @@ def profile_table(handle: int):
 # ---------------------------------------------------------------------------
 
 def fl_test_gemm(dtype, layout, epi, A, B, C, M, N, K, lda, ldb, ldc, bias=None, R=None, ldr=0, C2=None, ldc2=0,
-                 Z=None, ldz=0, part=None, b_rows=0, res_scale=1.0, stream=None) -> None:
+                 Z=None, ldz=0, part=None, b_rows=0, res_scale=1.0, colsum=None, stream=None) -> None:
     """part: optional fp32 device tensor, split-reduction scratch; b_rows:
-    rows B really has (0 = all)."""
+    rows B really has (0 = all); colsum: fp32 [ceil(M/256), N] per-block
+    column sums of C (bf16 NN GELU_BWD only)."""
     nbytes = part.numel() * part.element_size() if part is not None else 0
     _check(load().fl_test_gemm(dtype, layout, epi, _ptr(A), _ptr(B), _ptr(C), M, N, K, lda, ldb, ldc, _ptr(bias),
                                _ptr(R), ldr, _ptr(C2), ldc2, _ptr(Z), ldz, _ptr(part), nbytes, b_rows,
-                               res_scale, _stream(stream)))
+                               res_scale, _ptr(colsum), _stream(stream)))
 
 
 def fl_test_layernorm_fwd(dtype, x, g, b, y, mean, rstd, T, H, eps, stream=None) -> None:

@@ -84,6 +84,18 @@ def test_multi_kernel_class_counts_once():
     assert r["attn_bwd"] == [2, 6.0]
 
 
+PART, FIN = "void flglm::colsum_partial_kernel<bf16, 0>(...)", "flglm::colsum_finish_kernel(...)"
+GELU_BWD = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, false, 4>(G2Args)"
+
+
+def test_finish_after_a_gemm_is_a_column_sum_launch():
+    """partial + finish, partial + finish + finish (LayerNorm gain and shift)
+    and a finish of sums a GEMM epilogue formed: three column-sum launches."""
+    r = bench._class_launches(_disp(PART, FIN, LN, PART, FIN, FIN, GELU_BWD, FIN))
+    assert r["colsum"] == [3, 6.0]
+    assert r["gemm_nn_gelu_bwd"] == [1, 1.0]
+
+
 def test_queues_are_grouped_separately():
     d = [("1", 0, GEMM_RES, 1.0), ("2", 1, GEMM_RES, 1.0)]
     assert bench._class_launches(d)["gemm_nt_bias_res"] == [2, 2.0]

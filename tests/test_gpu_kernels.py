@@ -69,6 +69,46 @@ def test_gemm_nn(dt, epi, N):
     assert rel_l2(host(C), ref) < TOL[dt] / 4
 
 
+@pytest.mark.parametrize("M", [700, 256, 1])
+def test_gemm_gelu_bwd_column_sums(M):
+    """The GeLU' input-gradient GEMM also writes, per 256-row block, the
+    column sums of what it stores (the bias gradient's partial sums): equal
+    to the sums of the stored bf16 values over each block's rows, up to fp32
+    summation order.  M = 700 ends a block inside its second 128-row half."""
+    N, K = 768, 448
+    A, B, Z = rnd((M, K), 21, dt="bf16"), rnd((K, N), 22, 0.1, dt="bf16"), rnd((M, N), 23, dt="bf16")
+    C = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    nb = (M + 255) // 256
+    cs = torch.full((nb, N), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_gemm(F.FL_BF16, F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, dev(A, "bf16"), dev(B, "bf16"), C, M, N, K, K, N, N,
+                   Z=dev(Z, "bf16"), ldz=N, colsum=cs)
+    sync()
+    c = host(C).astype(np.float64)
+    ref = A.astype(np.float64) @ B.astype(np.float64) * oracle.gelu_grad(Z.astype(np.float64))
+    assert rel_l2(c, ref) < TOL["bf16"] / 4
+    got = host(cs)
+    for b in range(nb):
+        want = c[256 * b:256 * (b + 1)].sum(axis=0)
+        scale = np.abs(c[256 * b:256 * (b + 1)]).sum(axis=0) + 1e-30
+        assert np.all(np.abs(got[b] - want) <= 1e-6 * scale), b
+
+
+def test_gemm_column_sums_only_where_supported():
+    """Column sums come only from the bf16 GeLU' input-gradient GEMM on the
+    LDS-DMA kernel; elsewhere the call is refused before any work."""
+    M, N, K = 300, 512, 256
+    cs = torch.zeros((2, N), dtype=torch.float32, device="cuda")
+    for dt, lay, epi, n in (("f32", F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, N), ("bf16", F.FL_GEMM_NN, F.FL_EPI_STORE, N),
+                            ("bf16", F.FL_GEMM_NN, F.FL_EPI_GELU_BWD, 384)):
+        code, tdt = DTYPES[dt]
+        A = torch.zeros((M, K), dtype=tdt, device="cuda")
+        B = torch.zeros((K, n), dtype=tdt, device="cuda")
+        C = torch.zeros((M, n), dtype=tdt, device="cuda")
+        with pytest.raises(F.FlglmError) as e:
+            F.fl_test_gemm(code, lay, epi, A, B, C, M, n, K, K, n, n, Z=C, ldz=n, colsum=cs)
+        assert e.value.code == F.FL_ERR_ARG
+
+
 @pytest.mark.parametrize("dt", DT)
 def test_gemm_tn_accumulates(dt):
     code, tdt = DTYPES[dt]
