@@ -38,6 +38,13 @@ def test_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_stack_desc_accepts_the_glm_block():
+    _lib()
+    h = F.fl_stack_create(F.stack_desc(2, 256, 4, 1024, 32, F.FL_BF16, residual_alpha=7.48, rotary_2d=True,
+                                       num_prefix=16))
+    F.fl_stack_destroy(h)
+
+
 def _tiny_handle(dtype=F.FL_BF16):
     _lib()
     return F.fl_stack_create(F.stack_desc(2, 256, 4, 1024, 32, dtype))
@@ -49,6 +56,11 @@ def _tiny_handle(dtype=F.FL_BF16):
     (dict(ffn_hidden=1000), F.FL_ERR_SHAPE), (dict(rotary_dim=48), F.FL_ERR_SHAPE),
     (dict(rotary_dim=96), F.FL_ERR_SHAPE), (dict(num_layers=0), F.FL_ERR_SHAPE),
     (dict(dtype=7), F.FL_ERR_SHAPE), (dict(ln_eps=0.0), F.FL_ERR_SHAPE),
+    (dict(rope_base=0.0), F.FL_ERR_SHAPE), (dict(hidden=4352, num_heads=34), F.FL_ERR_SHAPE),
+    (dict(num_prefix=-1), F.FL_ERR_SHAPE), (dict(num_prefix=4097), F.FL_ERR_SHAPE),
+    (dict(num_prefix=16, dtype=F.FL_F32), F.FL_ERR_SHAPE),       # the prefix path is bf16 only
+    (dict(residual_alpha=-1.0), F.FL_ERR_SHAPE), (dict(residual_alpha=float("inf")), F.FL_ERR_SHAPE),
+    (dict(rotary_2d=True, rotary_dim=64), F.FL_ERR_SHAPE),       # 2-D positions need rotary = head dim / 2
 ])
 def test_stack_desc_validation(desc, code):
     _lib()
