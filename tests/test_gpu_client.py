@@ -220,3 +220,46 @@ def test_split_step_matches_oracle(dt, frozen, num_prefix, mask):
     assert not bad, bad
     if frozen:
         assert set(grads["block0"]) == {"prefix_k", "prefix_v"}
+
+
+def test_split_step_is_deterministic_and_recompute_exact():
+    """The whole bf16 split step twice, and once with per-block recompute:
+    every boundary tensor, the loss and every gradient agree bit for bit (no
+    atomics anywhere: segmented embedding sums, fixed-order reductions)."""
+    dt = "bf16"
+    b = synth.make_batch(3, 2, (20, 130), mask="prefix", seed=9)
+    T = b.total_tokens
+    layers = [synth.layer_params(TINY, l, seed=9, bf16=True) for l in range(4)]
+    m = SplitModel(TINY.hidden, TINY.num_heads, TINY.ffn_hidden, TINY.rotary_dim, 2, VT, dt, TINY.rope_base,
+                   TINY.ln_eps)
+    bd = BatchDesc.from_batch(b)
+    dlayers = [{k: dev(v, dt) for k, v in lp.items()} for lp in layers]
+    params = {"embedding": dev(rnd((VT, TINY.hidden), 91, 1.0, dt), dt),
+              "lm_head": dev(rnd((VT, TINY.hidden), 92, 0.05, dt), dt),
+              "block0": dlayers[0], "block_last": dlayers[3], "server": dlayers[1:3]}
+    ids = _ids(T, VT, 93)
+    labels = _labels(ids, 94)
+    scale = 1.0 / int((labels >= 0).sum())
+
+    def run(recompute):
+        buf = m.buffers(bd, recompute=recompute)
+        gz = lambda lp: {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in lp.items()}
+        grads = {"block0": gz(dlayers[0]), "block_last": gz(dlayers[3]), "server": [gz(d) for d in dlayers[1:3]],
+                 "embedding": torch.zeros((VT, TINY.hidden), device="cuda"),
+                 "lm_head": torch.zeros((VT, TINY.hidden), device="cuda")}
+        m.step(bd, ids, labels, params, grads, scale, buf, recompute=recompute)
+        torch.cuda.synchronize()
+        out = {k: host(buf[k]) for k in ("h0", "hs", "hl", "d_hl", "d_hs", "d_h0", "d_e", "loss_tok", "loss_sum")}
+        for name in ("block0", "block_last"):
+            out.update({f"{name}.{k}": host(v) for k, v in grads[name].items()})
+        for l in range(2):
+            out.update({f"server{l}.{k}": host(v) for k, v in grads["server"][l].items()})
+        out["embedding"], out["lm_head"] = host(grads["embedding"]), host(grads["lm_head"])
+        return out
+
+    a, a2, r = run(False), run(False), run(True)
+    m.close()
+    for other in (a2, r):
+        for k in a:
+            assert np.array_equal(a[k], other[k]), k
+    assert np.abs(a["embedding"]).sum() > 0 and np.abs(a["lm_head"]).sum() > 0
