@@ -65,6 +65,20 @@ CLASS_SOURCES = {"gemm": ("gemm_bf16.hip", "common.h", "kernels.h"),
                  "average": ("optim.hip", "common.h"),
                  "": ("elementwise.hip", "common.h", "kernels.h")}
 COPY_KERNEL = "neg_kernel"   # calibration: y = -x over float32, reads and writes the same bytes
+# The paper's own efficiency figures (Section 4.1, the table comparing the
+# training strategies' training time), quoted beside the measurement as
+# context: end-to-end wall times of whole training runs on other hardware,
+# with no token rate, so nothing here converts to this metric.
+PAPER_CONTEXT = {
+    "source": "Section 4.1, training time of the training strategies",
+    "hardware": "NVIDIA A100 40 GB for the server and for each client",
+    "workload": "1000 ReCoRD training points, P-tuning v2, batch 1 per client; sequence lengths not stated",
+    "unit": "s (end-to-end wall time: client and server compute plus messaging)",
+    "training_time_s": {"centralized": 166.4, "serial_2_clients": 175.2, "client_batch_2": 85.3,
+                        "client_batch_4": 43.0, "client_batch_8": 22.5, "server_hierarchical_2": 87.3,
+                        "server_hierarchical_3": 65.5, "server_hierarchical_5": 34.5,
+                        "server_hierarchical_10": 17.3},
+}
 
 
 def class_source_hash(cls: str) -> str:
@@ -793,6 +807,7 @@ def main() -> int:
         "roofline": roofline,
         "kernels": kernels,
         "cpu_baseline": None,
+        "paper_context": PAPER_CONTEXT,
     }
     if arena is not None:
         # read p, g, m, v; write p, m, v, the bf16 copy and the cleared g
