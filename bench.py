@@ -238,7 +238,9 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
     """Text summary of four rocprofv3 --pmc runs under root: fetch/ and write/
     (FETCH_SIZE, WRITE_SIZE of the benchmark), copy_fetch/ and copy_write/ (the
     same counters for --copy-calibration).  Counter KiB are scaled by the
-    ratio of the copy's known bytes to what the counter reads for it."""
+    ratio of the copy's known bytes to what the counter reads for it; per
+    class also the average launch duration in the FETCH_SIZE run (dispatch
+    timestamps) and the HBM rate the counters give over it."""
     copy_bytes = copy_mib << 20
     lines = []
     scale = {}
@@ -249,8 +251,11 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
         scale[c] = copy_bytes / per
         lines.append(f"calibration {c} copy_bytes {copy_bytes} dispatches {n} counter_bytes_per_dispatch "
                      f"{per:.0f} factor {scale[c]:.4f}")
-    fetch = _class_launches(_pmc_dispatches(os.path.join(root, "fetch"), "FETCH_SIZE"))
+    fdisp = _pmc_dispatches(os.path.join(root, "fetch"), "FETCH_SIZE", with_duration=True)
+    fetch = _class_launches(fdisp)
     write = _class_launches(_pmc_dispatches(os.path.join(root, "write"), "WRITE_SIZE"))
+    # duration of each class's launches in the FETCH_SIZE run (dispatch timestamps)
+    dur = _class_launches([(q, i, name, d) for q, i, name, _, d in fdisp])
     for cls in CLASS_KERNELS:
         n, fv = fetch.get(cls, (0, 0.0))
         n2, wv = write.get(cls, (0, 0.0))
@@ -258,8 +263,11 @@ def summarize_traffic(root: str, copy_mib: int, workload: str) -> str:
             continue
         fb = fv / n * 1024.0 * scale["FETCH_SIZE"]
         wb = wv / max(n2, 1) * 1024.0 * scale["WRITE_SIZE"]
+        us = dur.get(cls, (n, 0.0))[1] / n / 1e3
+        gbs = (fb + wb) / (us * 1e-6) / 1e9 if us > 0 else 0.0
         lines.append(f"class {cls} launches {n} fetch_bytes_per_launch {fb:.0f} write_bytes_per_launch {wb:.0f} "
-                     f"hbm_bytes_per_launch {fb + wb:.0f} src {class_source_hash(cls)}")
+                     f"hbm_bytes_per_launch {fb + wb:.0f} avg_us {us:.1f} counter_gbs {gbs:.0f} "
+                     f"src {class_source_hash(cls)}")
     return "\n".join(lines)
 
 
