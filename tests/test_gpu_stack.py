@@ -250,3 +250,18 @@ def test_other_block_shapes_match_oracle(name, dt):
     g.close()
     worst = _check(res, _oracle(layers, x, dy, b, shape), b, TOL[dt])
     print(f"[shapes] {name} {dt}: worst rel-L2 {worst:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+def test_single_token_batch_matches_oracle(dt, mask):
+    """The smallest batch: one client sending one 1-token sequence (T = 1).
+    Attention reduces to o = v (the token sees only itself), every GEMM is a
+    single ragged row, LayerNorm and the column sums see one row."""
+    b = synth.Batch(np.array([0, 1], np.int32), np.array([0, 1], np.int32), mask,
+                    np.array([1], np.int32) if mask == "prefix" else None)
+    layers, x, dy = _inputs(b, dt, seed=12)
+    g = GpuStack(SHAPE, layers, dt)
+    res = g.to_host(g.run(b, x, dy))
+    g.close()
+    _check(res, _oracle(layers, x, dy, b), b, TOL[dt])
