@@ -265,3 +265,25 @@ def test_single_token_batch_matches_oracle(dt, mask):
     res = g.to_host(g.run(b, x, dy))
     g.close()
     _check(res, _oracle(layers, x, dy, b), b, TOL[dt])
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", ["257_one_token_clients", "one_4096_token_sequence"])
+def test_extreme_batches_match_oracle(case, dt):
+    """257 clients of one token each (T one past a 256-row tile, every
+    sequence its own client) and a single 4096-token sequence (rotary angles
+    up to position 4095), prefix-LM with a quarter-length context."""
+    if case == "257_one_token_clients":
+        cu = np.arange(258, dtype=np.int32)
+        csp = np.arange(258, dtype=np.int32)
+    else:
+        cu = np.array([0, 4096], np.int32)
+        csp = np.array([0, 1], np.int32)
+    pre = (np.diff(cu) // 4).astype(np.int32)
+    b = synth.Batch(cu, csp, "prefix", pre)
+    layers, x, dy = _inputs(b, dt, seed=13)
+    g = GpuStack(SHAPE, layers, dt)
+    res = g.to_host(g.run(b, x, dy))
+    g.close()
+    worst = _check(res, _oracle(layers, x, dy, b), b, TOL[dt])
+    print(f"[extreme] {case} {dt}: worst rel-L2 {worst:.2e}", flush=True)
