@@ -21,7 +21,7 @@ factor (1 / number of labelled tokens gives the mean).
 
 from __future__ import annotations
 
-from typing import Dict, List, Optional, Sequence, Tuple
+from typing import Dict, Optional, Sequence, Tuple
 
 import numpy as np
 

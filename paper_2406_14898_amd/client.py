@@ -4,7 +4,7 @@ and the stream only; every step runs in the library's kernels."""
 
 from __future__ import annotations
 
-from typing import Dict, List, Optional, Sequence
+from typing import Dict, List, Optional
 
 from . import flglm as F
 from .stack import ServerStack

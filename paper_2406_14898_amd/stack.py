@@ -3,7 +3,7 @@ saved-activation and workspace buffers with torch (device memory only)."""
 
 from __future__ import annotations
 
-from typing import Dict, List, Optional, Sequence
+from typing import Dict, Sequence
 
 from . import flglm as F
 

@@ -6,7 +6,6 @@ import ctypes
 import os
 import re
 
-import numpy as np
 import pytest
 
 from paper_2406_14898_amd import flglm as F

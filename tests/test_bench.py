@@ -3,9 +3,7 @@ profiler dispatches into engine launches, the stale-counter rule and the
 shader-clock readout.  CPU only."""
 
 import csv
-import os
 
-import numpy as np
 import pytest
 
 import bench

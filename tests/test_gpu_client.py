@@ -8,7 +8,6 @@ training steps against the oracle."""
 import numpy as np
 import pytest
 
-import oracle
 import synth
 from oracle import client as oc
 from paper_2406_14898_amd import BatchDesc, ClientHead, SplitModel

@@ -13,7 +13,7 @@ import pytest
 import oracle
 import synth
 from oracle import client as oc
-from paper_2406_14898_amd import BatchDesc, ClientHead, SplitModel
+from paper_2406_14898_amd import BatchDesc, SplitModel
 from paper_2406_14898_amd import flglm as F
 
 pytestmark = pytest.mark.gpu

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from tests.gpu_helpers import TOL, dev, dev_i32, host, rel_l2
+from tests.gpu_helpers import TOL, dev, host, rel_l2
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")

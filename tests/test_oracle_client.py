@@ -11,7 +11,6 @@ import pytest
 import torch
 import torch.nn.functional as F
 
-import oracle
 from oracle import client as oc
 from tests import torch_block
 from tests.test_oracle_pins import TINY, _tiny_batch, _tiny_layers, rel_l2

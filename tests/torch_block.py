@@ -7,8 +7,6 @@ every gradient comes from autograd."""
 
 from __future__ import annotations
 
-import math
-
 import numpy as np
 import torch
 import torch.nn.functional as F
