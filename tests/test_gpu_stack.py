@@ -287,3 +287,32 @@ def test_extreme_batches_match_oracle(case, dt):
     g.close()
     worst = _check(res, _oracle(layers, x, dy, b), b, TOL[dt])
     print(f"[extreme] {case} {dt}: worst rel-L2 {worst:.2e}", flush=True)
+
+
+def test_launch_profile_accounts_every_launch():
+    """The opt-in launch timing the benchmark reads: one forward (keeping
+    intermediates) and one backward of the 2-block stack record every engine
+    launch by class, with the algorithmic work of each, and a duration."""
+    import bench
+    b = synth.make_batch(2, 2, (30, 170), "prefix", seed=14)
+    layers, x, dy = _inputs(b, "bf16", seed=14)
+    g = GpuStack(SHAPE, layers, "bf16")
+    F.fl_stack_profile(g.ss.handle, True)
+    g.run(b, x, dy)
+    prof = F.profile_table(g.ss.handle)
+    F.fl_stack_profile(g.ss.handle, False)
+    g.close()
+    N = SHAPE.num_layers
+    per_block = {"layernorm_fwd": 2, "gemm_nt_bias": 1, "rope_qk": 1, "attn_fwd": 1, "gemm_nt_bias_res": 2,
+                 "gemm_nt_bias_gelu": 1, "gemm_tn_acc": 4, "gemm_nn_gelu_bwd": 1, "gemm_nn": 3,
+                 "layernorm_bwd": 2, "colsum": 6, "attn_bwd": 1}
+    want = {k: v * N for k, v in per_block.items()}
+    want["plan"] = 2
+    assert {k: r["launches"] for k, r in prof.items()} == want
+    assert all(r["ms"] > 0 for r in prof.values())
+    w = synth.WORKLOADS["tiny_2blk_fp32"]
+    alg = bench.algorithmic_flops(w, b)
+    gemm = sum(r["flops"] for k, r in prof.items() if k.startswith("gemm"))
+    attn = sum(r["flops"] for k, r in prof.items() if k.startswith("attn"))
+    assert gemm == pytest.approx(alg["gemm"], rel=1e-9)
+    assert attn == pytest.approx(alg["attention"], rel=1e-9)
