@@ -62,3 +62,16 @@ def test_block_zero_weights_example():
     x = np.arange(T, dtype=np.float64)[:, None] - 0.5 * np.arange(c["hidden"])[None, :]
     y, _ = oracle.block_forward(p, x, b, shape)
     np.testing.assert_allclose(y - x, np.broadcast_to(ev(c["y_minus_x"]), x.shape), rtol=0, atol=1e-14)
+
+
+def test_pack_two_clients_example():
+    c = CASES["pack_two_clients"]
+    per = [np.array(t, np.float64) for t in c["client_tensors"]]
+    cu = np.array(c["cu_seqlens"], np.int32)
+    csp = np.array(c["client_seq_ptr"], np.int32)
+    packed = oracle.pack_clients(per, cu, csp)
+    np.testing.assert_array_equal(packed[:, 0], np.array(c["packed"], np.float64))
+    back = oracle.unpack_clients(packed, cu, csp)
+    for got, want in zip(back, c["unpacked"]):
+        np.testing.assert_array_equal(got, np.array(want, np.float64))
+    np.testing.assert_array_equal(oracle.client_token_ranges(cu, csp), np.array(c["client_rows"]))
