@@ -148,14 +148,14 @@ def layer_norm_backward(dy: np.ndarray, xhat: np.ndarray, rstd: np.ndarray, g: n
 # ----------------------------------------------------------------------------
 
 def gelu(z: np.ndarray) -> np.ndarray:
-    """0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3)))."""
-    return 0.5 * z * (1.0 + np.tanh(GELU_C * (z + GELU_A * z ** 3)))
+    """0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3)))  (z^3 as z z z)."""
+    return 0.5 * z * (1.0 + np.tanh(GELU_C * (z + GELU_A * (z * z * z))))
 
 
 def gelu_grad(z: np.ndarray) -> np.ndarray:
     """d gelu / dz = 0.5 (1 + t) + 0.5 z (1 - t^2) sqrt(2/pi) (1 + 3 * 0.044715 z^2),
     t = tanh(sqrt(2/pi) (z + 0.044715 z^3))."""
-    t = np.tanh(GELU_C * (z + GELU_A * z ** 3))
+    t = np.tanh(GELU_C * (z + GELU_A * (z * z * z)))
     return 0.5 * (1.0 + t) + 0.5 * z * (1.0 - t * t) * GELU_C * (1.0 + 3.0 * GELU_A * z * z)
 
 
@@ -382,7 +382,8 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     The server returns dx to the client in split learning (Section 3.1).
     With P-tuning v2 the block weights are frozen and only the prefix is
     trained (Section 3.1, Appendix A): pass grads holding just "prefix_k" and
-    "prefix_v" and no weight gradient is formed."""
+    "prefix_v" and no weight-gradient product is formed (likewise for any
+    weight left out of grads)."""
     p = _cast(p, dtype)
     dy = np.asarray(dy, dtype=dtype)
     c = cache
@@ -393,12 +394,14 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     alpha = float(getattr(shape, "residual_alpha", 0.0))
 
     # y = h + g W_2^T + b_2   (ChatGLM-6B: y = alpha w + g W_2^T + b_2)
-    grads["w_2"] += dy.T @ c["g"]
+    if grads.wants("w_2"):
+        grads["w_2"] += dy.T @ c["g"]
     grads["b_2"] += dy.sum(axis=0)
     dg = dy @ p["w_2"]
     dz = dg * gelu_grad(c["z"])
     # z = w W_1^T + b_1
-    grads["w_1"] += dz.T @ c["w"]
+    if grads.wants("w_1"):
+        grads["w_1"] += dz.T @ c["w"]
     grads["b_1"] += dz.sum(axis=0)
     dw = dz @ p["w_1"]
     if alpha:
@@ -409,7 +412,8 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     grads["ln2_b"] += db2
     dh = dh_ln if alpha else dy + dh_ln
     # h = x + o W_o^T + b_o
-    grads["w_o"] += dh.T @ c["o"]
+    if grads.wants("w_o"):
+        grads["w_o"] += dh.T @ c["o"]
     grads["b_o"] += dh.sum(axis=0)
     do = (dh @ p["w_o"]).reshape(T, nh, d)
     if c["pk"] is None:
@@ -422,7 +426,8 @@ def block_backward(p: Dict[str, np.ndarray], cache, dy: np.ndarray, batch, shape
     dk = _rotate_qk(dkr, c["tables"], shape, inverse=True)
     dqkv = np.concatenate([dq.reshape(T, H), dk.reshape(T, H), dv.reshape(T, H)], axis=1)
     # qkv = u W_qkv^T + b_qkv
-    grads["w_qkv"] += dqkv.T @ c["u"]
+    if grads.wants("w_qkv"):
+        grads["w_qkv"] += dqkv.T @ c["u"]
     grads["b_qkv"] += dqkv.sum(axis=0)
     du = dqkv @ p["w_qkv"]
     if alpha:
@@ -440,6 +445,9 @@ class _Sink:
 
     def __init__(self, grads: Dict[str, np.ndarray]):
         self.g = grads
+
+    def wants(self, k) -> bool:
+        return k in self.g
 
     def __getitem__(self, k):
         return self.g[k] if k in self.g else _Discard()
