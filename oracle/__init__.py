@@ -28,12 +28,14 @@ What it follows:
 Arithmetic is numpy in the dtype the caller selects (float64 by default;
 float32 for the fp32 mode).  Linear layers use numpy matmul; attention builds
 the full L x L score matrix of each (sequence, head) with no blocking or
-online softmax.
+online softmax (``attention_query_rows`` builds the rows of a few queries
+of one sequence, for sequences too long for the full matrix).
 """
 
 from .block import (  # noqa: F401
     layer_norm, layer_norm_backward, gelu, gelu_grad, positions, rope_tables,
-    rope, glm_positions, allowed_mask, attention_forward, attention_backward, block_forward,
+    rope, glm_positions, allowed_mask, attention_forward, attention_backward, attention_query_rows,
+    block_forward,
     block_backward, stack_forward, stack_backward, zero_grads, zero_prefix_grads, client_token_ranges,
     pack_clients, unpack_clients,
 )

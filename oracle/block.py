@@ -291,6 +291,63 @@ def attention_backward(q: np.ndarray, k: np.ndarray, v: np.ndarray, do: np.ndarr
     return dq, dk, dv, dpk, dpv
 
 
+def attention_query_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, rows: np.ndarray,
+                         prefix: Optional[int] = None, pk: Optional[np.ndarray] = None,
+                         pv: Optional[np.ndarray] = None, do: Optional[np.ndarray] = None):
+    """The attention of ``attention_forward`` / ``attention_backward`` for a
+    few query rows of ONE sequence, for sequences too long for the L x L
+    score matrix: q, k, v [L, n_h, d] are that sequence's rows, ``rows`` the
+    query indices, ``prefix`` its prefix-LM length (None: causal), pk, pv the
+    P-tuning v2 prefix [L_p, n_h, d] (Appendix A; visible to every query).
+
+    Forward: o [len(rows), n_h, d] and lse [len(rows), n_h], the natural-log
+    sum over the visible keys of exp(q k'/sqrt(d)).  With ``do`` (the output
+    gradient of the given rows, [len(rows), n_h, d]; every other query row
+    of the sequence has a zero output gradient) also the gradients, by the
+    same equations as ``attention_backward``: dq of the given rows, dk, dv
+    [L, n_h, d] of the whole sequence, and dpk, dpv [L_p, n_h, d].  Query rows
+    with a zero output gradient have dP = 0 and D = 0, hence dS = 0: they add
+    nothing, so these are the whole sequence's gradients."""
+    L, nh, d = q.shape
+    scale = 1.0 / math.sqrt(d)
+    rows = np.asarray(rows, np.int64)
+    Lp = 0 if pk is None else pk.shape[0]
+    j = np.arange(L)[None, :]
+    i = rows[:, None]
+    own = j <= (i if prefix is None else np.maximum(i, int(prefix) - 1))
+    allowed = np.concatenate([np.ones((len(rows), Lp), bool), own], axis=1)
+    o = np.zeros((len(rows), nh, d), q.dtype)
+    lse = np.zeros((len(rows), nh), q.dtype)
+    grads = do is not None
+    if grads:
+        dq = np.zeros((len(rows), nh, d), q.dtype)
+        dk, dv = np.zeros_like(k), np.zeros_like(v)
+        dpk = np.zeros((Lp, nh, d), q.dtype)
+        dpv = np.zeros((Lp, nh, d), q.dtype)
+    for h in range(nh):
+        kk = np.concatenate([_prefix_head(pk, h, d, q.dtype), k[:, h]])
+        vv = np.concatenate([_prefix_head(pv, h, d, q.dtype), v[:, h]])
+        S = np.where(allowed, (q[rows, h] @ kk.T) * scale, -np.inf)
+        m = S.max(axis=1, keepdims=True)
+        e = np.where(allowed, np.exp(S - m), 0.0)
+        ssum = e.sum(axis=1, keepdims=True)
+        P = e / ssum
+        o[:, h] = P @ vv
+        lse[:, h] = (m + np.log(ssum))[:, 0]
+        if grads:
+            dP = do[:, h] @ vv.T
+            D = (P * dP).sum(axis=1, keepdims=True)
+            dS = P * (dP - D)
+            dq[:, h] = (dS @ kk) * scale
+            dkk = (dS.T @ q[rows, h]) * scale
+            dvv = P.T @ do[:, h]
+            dk[:, h], dv[:, h] = dkk[Lp:], dvv[Lp:]
+            dpk[:, h], dpv[:, h] = dkk[:Lp], dvv[:Lp]
+    if not grads:
+        return o, lse
+    return o, lse, dq, dk, dv, dpk, dpv
+
+
 # ----------------------------------------------------------------------------
 # One block (Section 3.1: an LLM-Block is self-attention followed by an FFN)
 # ----------------------------------------------------------------------------

@@ -141,6 +141,42 @@ def test_attention_backward_vs_autograd():
         assert rel_l2(a, ref.numpy()) < 1e-12
 
 
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+@pytest.mark.parametrize("num_prefix", [0, 3])
+def test_attention_query_rows_vs_torch_autograd(mask, num_prefix):
+    """The few-rows attention of one long sequence against torch SDPA with an
+    explicit mask and autograd: o and the log-sum-exp of the chosen rows, and
+    with a zero output gradient on every other row, dq of the rows and dk, dv
+    and the prefix gradients of the whole sequence."""
+    g = np.random.default_rng(7)
+    L, nh, d = 37, 2, 8
+    P = 9 if mask == "prefix" else None
+    q, k, v = (g.standard_normal((L, nh, d)) for _ in range(3))
+    pk, pv = (g.standard_normal((num_prefix, nh, d)) if num_prefix else None for _ in range(2))
+    rows = np.array([0, 5, 8, 9, 20, 35, 36])
+    do = g.standard_normal((len(rows), nh, d))
+    o, lse, dq, dk, dv, dpk, dpv = oracle.attention_query_rows(q, k, v, rows, P, pk, pv, do)
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    tpk, tpv = (torch.tensor(a if num_prefix else np.zeros((0, nh, d)), requires_grad=True) for a in (pk, pv))
+    i = torch.arange(L)[:, None]
+    j = torch.arange(L)[None, :]
+    m = j <= i if P is None else (j <= i) | (j < P)
+    m = torch.cat([torch.ones((L, num_prefix), dtype=torch.bool), m], dim=1)
+    kk, vv = torch.cat([tpk, tk]).transpose(0, 1), torch.cat([tpv, tv]).transpose(0, 1)
+    ref = F.scaled_dot_product_attention(tq.transpose(0, 1), kk, vv, attn_mask=m).transpose(0, 1)
+    S = torch.where(m, (tq.transpose(0, 1) @ kk.transpose(1, 2)) / math.sqrt(d), -torch.inf)
+    ref_lse = torch.logsumexp(S, dim=-1).transpose(0, 1)
+    assert rel_l2(o, ref.detach().numpy()[rows]) < 1e-12
+    assert rel_l2(lse, ref_lse.detach().numpy()[rows]) < 1e-12
+    full_do = torch.zeros((L, nh, d), dtype=torch.float64)
+    full_do[rows] = torch.tensor(do)
+    (ref * full_do).sum().backward()
+    assert rel_l2(dq, tq.grad.numpy()[rows]) < 1e-12
+    assert rel_l2(dk, tk.grad.numpy()) < 1e-12 and rel_l2(dv, tv.grad.numpy()) < 1e-12
+    if num_prefix:
+        assert rel_l2(dpk, tpk.grad.numpy()) < 1e-12 and rel_l2(dpv, tpv.grad.numpy()) < 1e-12
+
+
 # ---------------------------------------------------------------------------
 # LayerNorm, GeLU, rotary
 # ---------------------------------------------------------------------------
