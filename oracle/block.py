@@ -535,13 +535,16 @@ def stack_forward(layers: LayerSource, num_layers: int, x: np.ndarray, batch, sh
     """x_0 = x, x_l = Block_l(x_{l-1}), output x_N.  ``layers`` is a list of
     parameter dicts or a function l -> dict (lets a caller produce layers one
     at a time).  keep = "inputs" stores only each block's input (the backward
-    recomputes the block); "none" stores nothing."""
+    recomputes the block); "caches" stores each block's whole forward cache
+    (no recompute, more memory); "none" stores nothing."""
     xs = []
     cur = np.asarray(x, dtype=dtype)
     for l in range(num_layers):
         if keep == "inputs":
             xs.append(cur)
-        cur, _ = block_forward(_layer(layers, l), cur, batch, shape, dtype)
+        cur, cache = block_forward(_layer(layers, l), cur, batch, shape, dtype)
+        if keep == "caches":
+            xs.append(cache)
     return cur, xs
 
 
@@ -549,13 +552,17 @@ def stack_backward(layers: LayerSource, num_layers: int, xs: List[np.ndarray], d
                    batch, shape, grads: Optional[List[Dict[str, np.ndarray]]] = None,
                    dtype=np.float64):
     """Backward through blocks N..1: each block's forward is recomputed from
-    its stored input, then its backward runs; the dx of block l is the dy of
-    block l-1.  Returns (dx, grads) with grads[l] accumulated (+=)."""
+    its stored input (or taken from its stored cache, keep="caches"), then
+    its backward runs; the dx of block l is the dy of block l-1.  Returns
+    (dx, grads) with grads[l] accumulated (+=)."""
     if grads is None:
         grads = [zero_grads(shape, dtype) for _ in range(num_layers)]
     cur = np.asarray(dy, dtype=dtype)
     for l in reversed(range(num_layers)):
         p = _layer(layers, l)
-        _, cache = block_forward(p, xs[l], batch, shape, dtype)
+        if isinstance(xs[l], dict):
+            cache = xs[l]
+        else:
+            _, cache = block_forward(p, xs[l], batch, shape, dtype)
         cur = block_backward(p, cache, cur, batch, shape, grads[l], dtype)
     return cur, grads

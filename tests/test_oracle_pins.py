@@ -438,6 +438,21 @@ def test_I7_recompute_matches_stored_cache():
     np.testing.assert_array_equal(dx, dx2)
     for k in gr:
         np.testing.assert_array_equal(gr[k], gr2[0][k])
+    # the two-block stack: stored caches (no recompute) give the same bits
+    layers = _tiny_layers()
+    y1, xs = oracle.stack_forward(layers, 2, x, b, TINY)
+    y2, caches = oracle.stack_forward(layers, 2, x, b, TINY, keep="caches")
+    np.testing.assert_array_equal(y1, y2)
+    dx1, g1 = oracle.stack_backward(layers, 2, xs, dy, b, TINY)
+    dx3, g3 = oracle.stack_backward(layers, 2, caches, dy, b, TINY)
+    np.testing.assert_array_equal(dx1, dx3)
+    for l in range(2):
+        for k in g1[l]:
+            np.testing.assert_array_equal(g1[l][k], g3[l][k])
+    # weights left out of grads: the same dx, and no product is formed
+    dx4, g4 = oracle.stack_backward(layers, 2, caches, dy, b, TINY, grads=[{}, {"b_o": np.zeros(TINY.hidden)}])
+    np.testing.assert_array_equal(dx1, dx4)
+    np.testing.assert_array_equal(g4[1]["b_o"], g1[1]["b_o"])
 
 
 def test_I8_zero_output_projections_is_identity():
