@@ -1,4 +1,5 @@
-// Attention over packed ragged sequences, matrix-core tiles, fp32 softmax.
+// Attention over packed ragged sequences, matrix-core tiles, fp32 softmax:
+// the fp32 debug mode's kernels (bf16 runs on attention_bf16.hip).
 //
 // Every workgroup works inside one (sequence, head): its row range comes
 // from cu_seqlens, so no score ever crosses a sequence (hence a client)
@@ -553,19 +554,24 @@ static hipError_t bwd_t(const AttnDesc& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// bf16 always runs on the LDS-DMA kernels (attention_bf16.hip), which take
+// every supported shape, the P-tuning prefix included; these generic
+// kernels serve the fp32 debug mode, which has no prefix.
 hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;
-  if (dt == DT_BF16 && attn_bf16_ok(a)) return attn_fwd_bf16(a, st);
-  if (a.head_dim == 128) return dt == DT_BF16 ? fwd_t<bf16, 128>(a, st) : fwd_t<float, 128>(a, st);
-  if (a.head_dim == 64) return dt == DT_BF16 ? fwd_t<bf16, 64>(a, st) : fwd_t<float, 64>(a, st);
+  if (dt == DT_BF16) return attn_bf16_ok(a) ? attn_fwd_bf16(a, st) : hipErrorInvalidValue;
+  if (a.num_prefix > 0) return hipErrorInvalidValue;
+  if (a.head_dim == 128) return fwd_t<float, 128>(a, st);
+  if (a.head_dim == 64) return fwd_t<float, 64>(a, st);
   return hipErrorInvalidValue;
 }
 
 hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;
-  if (dt == DT_BF16 && attn_bf16_ok(a)) return attn_bwd_bf16(a, st);
-  if (a.head_dim == 128) return dt == DT_BF16 ? bwd_t<bf16, 128>(a, st) : bwd_t<float, 128>(a, st);
-  if (a.head_dim == 64) return dt == DT_BF16 ? bwd_t<bf16, 64>(a, st) : bwd_t<float, 64>(a, st);
+  if (dt == DT_BF16) return attn_bf16_ok(a) ? attn_bwd_bf16(a, st) : hipErrorInvalidValue;
+  if (a.num_prefix > 0) return hipErrorInvalidValue;
+  if (a.head_dim == 128) return bwd_t<float, 128>(a, st);
+  if (a.head_dim == 64) return bwd_t<float, 64>(a, st);
   return hipErrorInvalidValue;
 }
 

@@ -6,9 +6,10 @@
 // Data movement:
 //   * K, V (forward, dq) and Q, dO (dk/dv) tiles of 64 rows x d go from HBM
 //     straight into LDS with buffer loads in LDS-DMA mode, double-buffered:
-//     the next tile streams in while the current one is used.  Buffer
-//     resources are bounded at the sequence end, so rows past it read as
-//     zero.
+//     the next tile streams in while the current one is used.  Each tile
+//     gets its own buffer resource, based at its first row and bounded at
+//     the sequence end, so rows past it read as zero and offsets stay small
+//     at any sequence length.
 //   * Tiles stay in their global layout ([row][d], 16-byte chunks swizzled
 //     by chunk ^ 2 (row & 7) for d = 128, chunk ^ (row & 7) for d = 64).
 //     Operands whose contraction runs along the feature dimension use
@@ -72,6 +73,14 @@ __device__ __forceinline__ void dma_tile(i32x4 rs, long ld, int row0, uint32_t t
     const uint32_t voff = (uint32_t)((long)(row0 + row) * ld + q * 8) * 2u;
     dma_lds<16>(rs, tile + inst * 1024, voff);
   }
+}
+
+// Buffer resource over one 64-row tile of a sequence: rows row0 ..
+// min(row0 + 64, L) - 1 of the rows starting at base (row stride ld
+// elements); rows past the sequence end read as zero.  Rebasing per tile
+// keeps every buffer offset below 64 rows, whatever the sequence length.
+__device__ __forceinline__ i32x4 tile_rsrc(const bf16* base, long ld, int row0, int L) {
+  return buf_rsrc(base + (long)row0 * ld, (uint32_t)((long)min(L - row0, kRows) * ld * 2));
 }
 
 // Per-lane element offsets of the fragment reads inside a [64][D] tile, so
@@ -208,9 +217,8 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
   FragBase<D> fb;
   fb.init(fr, fg);
 
-  const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
-  const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
-  const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  const bf16* kbase = qkv + (long)si.r0 * ld + H + h * D;
+  const bf16* vbase = kbase + H;
   // key tiles 0 .. ntp-1: the prefix (row stride H), then the sequence's own
   const PrefixKV px(a, h, D);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
@@ -222,8 +230,9 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
       dma_tile<D>(px.rk, H, kt * kRows, sk, w, lane);
       dma_tile<D>(px.rv, H, kt * kRows, sv, w, lane);
     } else {
-      dma_tile<D>(rk, ld, (kt - px.ntiles) * kRows, sk, w, lane);
-      dma_tile<D>(rv, ld, (kt - px.ntiles) * kRows, sv, w, lane);
+      const int j0 = (kt - px.ntiles) * kRows;
+      dma_tile<D>(tile_rsrc(kbase, ld, j0, si.L), ld, 0, sk, w, lane);
+      dma_tile<D>(tile_rsrc(vbase, ld, j0, si.L), ld, 0, sv, w, lane);
     }
   };
   issue(0);
@@ -380,9 +389,8 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
   FragBase<D> fb;
   fb.init(fr, fg);
 
-  const uint32_t seq_bytes = (uint32_t)((long)si.L * ld * 2);
-  const auto rk = buf_rsrc(qkv + (long)si.r0 * ld + H + h * D, seq_bytes);
-  const auto rv = buf_rsrc(qkv + (long)si.r0 * ld + 2 * H + h * D, seq_bytes);
+  const bf16* kbase = qkv + (long)si.r0 * ld + H + h * D;
+  const bf16* vbase = kbase + H;
   const PrefixKV px(a, h, D);
   const int kv_end = min(si.L, max(q0 + BM, si.P));
   const int nkt = px.ntiles + (kv_end + kRows - 1) / kRows;
@@ -393,8 +401,9 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
       dma_tile<D>(px.rk, H, kt * kRows, sk, w, lane);
       dma_tile<D>(px.rv, H, kt * kRows, sv, w, lane);
     } else {
-      dma_tile<D>(rk, ld, (kt - px.ntiles) * kRows, sk, w, lane);
-      dma_tile<D>(rv, ld, (kt - px.ntiles) * kRows, sv, w, lane);
+      const int j0 = (kt - px.ntiles) * kRows;
+      dma_tile<D>(tile_rsrc(kbase, ld, j0, si.L), ld, 0, sk, w, lane);
+      dma_tile<D>(tile_rsrc(vbase, ld, j0, si.L), ld, 0, sv, w, lane);
     }
   };
   issue(0);
@@ -545,23 +554,24 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   FragBase<D> fb;
   fb.init(fr, fg);
 
-  const auto rq = buf_rsrc(qkv + (long)si.r0 * ld + h * D, (uint32_t)((long)si.L * ld * 2));
-  const auto ro = buf_rsrc(dout + (long)si.r0 * a.ld_dout + h * D, (uint32_t)((long)si.L * a.ld_dout * 2));
-  const auto rl = buf_rsrc(a.lse + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
-  const auto rd = buf_rsrc(a.delta + (long)si.r0 * nh + h, (uint32_t)((long)si.L * nh * 4 - h * 4));
+  const bf16* qbase = qkv + (long)si.r0 * ld + h * D;
+  const bf16* obase = dout + (long)si.r0 * a.ld_dout + h * D;
+  const float* lbase = a.lse + (long)si.r0 * nh + h;
+  const float* dbase = a.delta + (long)si.r0 * nh + h;
   const int qstart = (pre || k0 < si.P) ? 0 : k0 / kRows;
   const int nqt = (si.L + kRows - 1) / kRows;
   const uint32_t lds_q = FL_LDS_ADDR(&Qs[0][0]), lds_o = FL_LDS_ADDR(&Os[0][0]);
   const uint32_t lds_l = FL_LDS_ADDR(&Ls[0][0]), lds_d = FL_LDS_ADDR(&Ds[0][0]);
   // query tile qt lives in slot (qt - qstart) & 1
   auto issue = [&](int qt) {
-    const int slot = (qt - qstart) & 1;
-    dma_tile<D>(rq, ld, qt * kRows, lds_q + slot * (kRows * D * 2), w, lane);
-    dma_tile<D>(ro, a.ld_dout, qt * kRows, lds_o + slot * (kRows * D * 2), w, lane);
+    const int slot = (qt - qstart) & 1, q0 = qt * kRows;
+    dma_tile<D>(tile_rsrc(qbase, ld, q0, si.L), ld, 0, lds_q + slot * (kRows * D * 2), w, lane);
+    dma_tile<D>(tile_rsrc(obase, a.ld_dout, q0, si.L), a.ld_dout, 0, lds_o + slot * (kRows * D * 2), w, lane);
     // LSE (scaled on use) and delta rows: 64 x 4 bytes each
-    const uint32_t voff = (uint32_t)((qt * kRows + lane) * nh) * 4u;
-    if (w == 0) dma_lds<4>(rl, lds_l + slot * (kRows * 4), voff);
-    if (w == 1) dma_lds<4>(rd, lds_d + slot * (kRows * 4), voff);
+    const uint32_t voff = (uint32_t)(lane * nh) * 4u;
+    const uint32_t nb = (uint32_t)(min(si.L - q0, kRows) * nh * 4 - h * 4);
+    if (w == 0) dma_lds<4>(buf_rsrc(lbase + (long)q0 * nh, nb), lds_l + slot * (kRows * 4), voff);
+    if (w == 1) dma_lds<4>(buf_rsrc(dbase + (long)q0 * nh, nb), lds_d + slot * (kRows * 4), voff);
   };
   issue(qstart);
 
@@ -720,11 +730,9 @@ hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
 
 }  // namespace
 
-// Byte offsets inside one sequence stay below 2^32 for the buffer resources.
-bool attn_bf16_ok(const AttnDesc& a) {
-  const long ld = a.ld_qkv > a.ld_dout ? a.ld_qkv : a.ld_dout;
-  return (a.head_dim == 64 || a.head_dim == 128) && (long)a.max_seqlen * ld * 2 < (1L << 31);
-}
+// Buffer resources are rebased per 64-row tile, so any sequence length
+// works; head dims 64 and 128.
+bool attn_bf16_ok(const AttnDesc& a) { return a.head_dim == 64 || a.head_dim == 128; }
 
 hipError_t attn_fwd_bf16(const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;

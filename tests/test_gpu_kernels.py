@@ -479,3 +479,65 @@ def test_attention_prefix_fwd_bwd(heads, bname, num_prefix):
         pg = host(part).sum(axis=1)  # sequence partials -> the batch's prefix gradients
         assert rel_l2(pg[0], dpk.reshape(-1, H)) < tol, r
         assert rel_l2(pg[1], dpv.reshape(-1, H)) < tol, r
+
+
+@pytest.mark.parametrize("mask", ["causal", "prefix"])
+def test_attention_offsets_past_2_31_bytes(mask):
+    """One 90037-token sequence at the ChatGLM-6B width (32 heads of 128,
+    q|k|v rows of 24 KB, so the sequence spans 2.2 GB and its late tiles sit
+    past 2^31 bytes), with a 70-row P-tuning prefix and the inverse rotation.
+    The output gradient is zero except on a few rows at the start, middle and
+    end, so the oracle's few-rows attention gives the whole dk, dv and prefix
+    gradients; o, lse and dq are compared on those rows, and dq of every other
+    row must be exactly zero."""
+    nh, d, Lp = 32, 128, 70
+    H, L = nh * d, 90037
+    r = d // 2
+    P = L // 4 if mask == "prefix" else None
+    gen = torch.Generator(device="cuda").manual_seed(90037)
+    t = torch.randn((L, 3 * H), generator=gen, device="cuda").to(torch.bfloat16)
+    tpk = torch.randn((Lp, H), generator=gen, device="cuda").to(torch.bfloat16)
+    tpv = torch.randn((Lp, H), generator=gen, device="cuda").to(torch.bfloat16)
+    rows = np.unique(np.concatenate([[0, 1, 2, 63, 64, L // 2, P or 5], np.arange(L - 64, L)]))
+    do_rows = torch.randn((len(rows), H), generator=gen, device="cuda").to(torch.bfloat16)
+    tdo = torch.zeros((L, H), dtype=torch.bfloat16, device="cuda")
+    tdo[torch.from_numpy(rows).cuda()] = do_rows
+    assert L * 3 * H * 2 > (1 << 31)
+    cu = dev_i32(np.array([0, L]))
+    pre = dev_i32(np.array([P])) if P is not None else None
+    o = torch.full((L, H), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((L, nh), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_fwd(F.FL_BF16, t, o, lse, cu, pre, L, 1, L, H, nh, tpk, tpv, Lp)
+    pos = torch.empty(L, dtype=torch.int32, device="cuda")
+    ct = torch.empty(L * r // 2, dtype=torch.float32, device="cuda")
+    st = torch.empty_like(ct)
+    F.fl_test_rope(F.FL_BF16, torch.zeros((L, 3 * H), dtype=torch.bfloat16, device="cuda"), cu, 1, L, L, H, nh, r,
+                   10000.0, pos, ct, st)
+    dqkv = torch.full((L, 3 * H), float("nan"), dtype=torch.bfloat16, device="cuda")
+    delta = torch.empty((L, nh), dtype=torch.float32, device="cuda")
+    part = torch.full((2, 1, Lp, H), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, tdo, dqkv, delta, cu, pre, pos, ct, st, r, L, 1, L, H, nh,
+                            tpk, tpv, Lp, part)
+    sync()
+    qkv = host(t)
+    q, k, v = (qkv[:, i * H:(i + 1) * H].reshape(L, nh, d) for i in range(3))
+    pk, pv = host(tpk).reshape(Lp, nh, d), host(tpv).reshape(Lp, nh, d)
+    o_r, lse_r, dq_r, dk_r, dv_r, dpk, dpv = oracle.attention_query_rows(
+        q, k, v, rows, P, pk, pv, host(do_rows).reshape(-1, nh, d))
+    cos, sin = oracle.rope_tables(np.arange(L), r, 10000.0)
+    tol = TOL["bf16"] / 2
+    errs = {"o": rel_l2(host(o[torch.from_numpy(rows).cuda()]), o_r.reshape(-1, H)),
+            "lse": rel_l2(host(lse[torch.from_numpy(rows).cuda()]), lse_r)}
+    g = host(dqkv)
+    errs["dq"] = rel_l2(g[rows, :H], oracle.rope(dq_r, cos[rows], sin[rows], r, inverse=True).reshape(-1, H))
+    errs["dk"] = rel_l2(g[:, H:2 * H], oracle.rope(dk_r, cos, sin, r, inverse=True).reshape(L, H))
+    errs["dv"] = rel_l2(g[:, 2 * H:], dv_r.reshape(L, H))
+    pg = host(part)
+    errs["dprefix_k"] = rel_l2(pg[0, 0], dpk.reshape(Lp, H))
+    errs["dprefix_v"] = rel_l2(pg[1, 0], dpv.reshape(Lp, H))
+    print(f"[attention L={L} {mask}] {errs}", flush=True)
+    assert errs["lse"] < 1e-5
+    assert all(e < tol for e in errs.values()), errs
+    quiet = np.ones(L, bool)
+    quiet[rows] = False
+    assert (g[quiet, :H] == 0).all()
