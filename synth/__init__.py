@@ -32,7 +32,7 @@ __all__ = [
     "STREAM_PARAMS", "STREAM_X", "STREAM_DY", "STREAM_LENS", "STREAM_PREFIX", "STREAM_TOKENS",
     "PARAM_NAMES", "StackShape", "Batch", "Workload", "WORKLOADS",
     "bf16_round", "bf16_bits", "bits_to_f32", "rng", "make_batch",
-    "param_shapes", "layer_params", "prefix_params", "activations", "upstream_grad", "token_ids",
+    "param_shapes", "layer_params", "device_layer_params", "prefix_params", "activations", "upstream_grad", "token_ids",
 ]
 
 STREAM_PARAMS, STREAM_X, STREAM_DY, STREAM_LENS, STREAM_PREFIX, STREAM_TOKENS = 0, 1, 2, 3, 4, 5
@@ -211,6 +211,24 @@ def layer_params(shape: StackShape, layer: int, seed: int = 0, bf16: bool = True
         if name in ("ln1_g", "ln2_g"):
             a += np.float32(1.0)
         out[name] = bf16_round(a) if bf16 else a
+    return out
+
+
+def device_layer_params(shape: StackShape, layer: int, seed: int = 0, bf16: bool = True, std: float = 0.02):
+    """One layer's parameters drawn on the GPU (torch's seeded Philox
+    generator, seed * 100003 + layer): the distributions of ``layer_params``
+    (linear weights and biases N(0, std), LayerNorm gains 1 + N(0, std),
+    shifts N(0, std)) in the same draw order, rounded to bf16 (nearest even)
+    when bf16.  For full-size stacks, whose host draws would take minutes;
+    returns a dict of cuda tensors (not the same values as ``layer_params``)."""
+    import torch
+    gen = torch.Generator(device="cuda").manual_seed(seed * 100003 + layer)
+    out = {}
+    for name, shp in param_shapes(shape).items():
+        t = torch.randn(shp, generator=gen, device="cuda", dtype=torch.float32) * std
+        if name in ("ln1_g", "ln2_g"):
+            t += 1.0
+        out[name] = t.to(torch.bfloat16) if bf16 else t
     return out
 
 

@@ -24,8 +24,8 @@ class GpuStack:
         cache = {}  # layers given as the same dict share one device copy
         self.params = []
         for lp in layers:
-            if id(lp) not in cache:
-                cache[id(lp)] = {k: dev(v, dt) for k, v in lp.items()}
+            if id(lp) not in cache:  # host arrays are uploaded; device tensors used as they are
+                cache[id(lp)] = {k: v if isinstance(v, torch.Tensor) else dev(v, dt) for k, v in lp.items()}
             self.params.append(cache[id(lp)])
 
     def zero_grads(self, frozen: bool = False):
