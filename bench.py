@@ -504,10 +504,30 @@ def average_bench(w: synth.Workload, replicas: int, launches: int) -> dict:
             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def spread_order(lengths) -> list:
+    """Sequence indices in an order whose every prefix spreads over the
+    length distribution: the sequences at the quantiles 1/2, 1/4, 3/4, 1/8,
+    3/8, ... of the sorted lengths (van der Corput order), each once."""
+    order = list(np.argsort(np.asarray(lengths), kind="stable"))
+    n, out, seen = len(order), [], set()
+    k = 1
+    while len(out) < n:
+        den = 1 << k.bit_length()
+        i = int((int(f"{k:b}"[::-1], 2) / den) * n) if k > 0 else 0
+        k += 1
+        for j in (i, *range(n)):  # nearest not yet taken, upwards then from the start
+            if j < n and order[j] not in seen:
+                seen.add(order[j])
+                out.append(int(order[j]))
+                break
+    return out
+
+
 def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
-    """The CPU oracle (float64, numpy BLAS) on a bounded sample: one block's
-    forward + recompute + backward over whole sequences of the workload,
-    shortest first, until the budget is used; scaled to the full stack depth."""
+    """The CPU oracle (float32, numpy BLAS) on a bounded sample: one block's
+    forward + recompute + backward over whole sequences of the workload, taken
+    in an order that spreads over its length distribution (``spread_order``),
+    until the budget is used; scaled to the full stack depth."""
     import oracle
     blas = "unknown"
     try:
@@ -529,20 +549,21 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
     layer = synth.layer_params(w.shape, 0, seed=0, bf16=w.dtype == "bf16")
     if w.num_prefix:
         layer.update(synth.prefix_params(w.shape, 0, w.num_prefix, seed=0, bf16=w.dtype == "bf16"))
-    grads = ([oracle.zero_prefix_grads(w.num_prefix, w.shape.hidden)] if w.frozen else None)
-    order = np.argsort(b.seqlens, kind="stable")
+    f32 = np.float32
+    grads = ([oracle.zero_prefix_grads(w.num_prefix, w.shape.hidden, f32)] if w.frozen
+             else [oracle.zero_grads(one, f32)])
     done_tokens, spent = 0, 0.0
     seqs = []
-    for s in order:
+    for s in spread_order(b.seqlens):
         sub = synth.Batch(np.array([0, int(b.seqlens[s])], np.int32), np.array([0, 1], np.int32), b.mask,
                           None if b.prefix_len is None else np.array([int(b.prefix_len[s])], np.int32))
         L = sub.total_tokens
         x = synth.activations(L, w.shape.hidden, seed=1, bf16=w.dtype == "bf16")
         dy = synth.upstream_grad(L, w.shape.hidden, seed=1, bf16=w.dtype == "bf16", std=w.dy_std)
         t0 = time.perf_counter()
-        y, xs = oracle.stack_forward([layer], 1, x, sub, one)
+        y, xs = oracle.stack_forward([layer], 1, x, sub, one, f32)
         if w.backward:
-            oracle.stack_backward([layer], 1, xs, dy, sub, one, grads)
+            oracle.stack_backward([layer], 1, xs, dy, sub, one, grads, f32)
         spent += time.perf_counter() - t0
         done_tokens += L
         seqs.append(L)
@@ -556,8 +577,8 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
         # the final linear layer with the loss, forward and backward, on a few tokens
         n = 32
         g = np.random.default_rng(3)
-        wv = g.standard_normal((w.vocab, w.shape.hidden)) * 0.02
-        h = g.standard_normal((n, w.shape.hidden))
+        wv = (g.standard_normal((w.vocab, w.shape.hidden)) * 0.02).astype(f32)
+        h = g.standard_normal((n, w.shape.hidden)).astype(f32)
         lab = g.integers(0, w.vocab, n)
         t0 = time.perf_counter()
         lg, lse, _, _ = oracle.client.lm_head_forward(h, wv, lab)
@@ -571,11 +592,74 @@ def cpu_baseline(w: synth.Workload, b: synth.Batch, budget_s: float) -> dict:
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"1 of {nl} blocks, {'fwd+recompute+bwd' if w.backward else 'fwd'}, float64, "
-                   f"{len(seqs)} whole sequence(s) of lengths {seqs} ({done_tokens} tokens) in {spent:.1f} s; "
+        "sample": (f"1 of {nl} blocks, {'fwd+recompute+bwd' if w.backward else 'fwd'}, float32, "
+                   f"{len(seqs)} whole sequence(s) spread over the workload's length distribution "
+                   f"(lengths {seqs}, workload {int(b.seqlens.min())}..{int(b.seqlens.max())}, "
+                   f"mean {float(b.seqlens.mean()):.0f}; {done_tokens} tokens) in {spent:.1f} s; "
                    f"per-token time times {nl} blocks{head}; host {cpu}, BLAS {blas}, "
                    f"{len(os.sched_getaffinity(0))} cores visible"),
     }
+
+
+SECONDARY_WORKLOADS = (
+    ("chatglm6b_1blk_fwd_4x4x512", 10, 3),
+    ("chatglm6b_1blk_ragged_8x4", 10, 3),
+    ("chatglm6b_26blk_prefix_16x2x512", 3, 1),
+    ("chatglm6b_26blk_ptuning128_ragged_32x1_recompute", 3, 1),
+)
+
+
+def secondary_run(name: str, seed: int, steps: int, warmup: int) -> dict:
+    """A short timed run of another server-stack workload (same device
+    draws, launch timing on): tokens/s, ms per step, algorithmic MFMA
+    utilisation and the GEMMs' MFMA utilisation."""
+    import torch
+
+    from paper_2406_14898_amd import BatchDesc, ServerStack
+    from paper_2406_14898_amd import flglm as F
+    w = synth.WORKLOADS[name]
+    b = w.batch(seed=seed)
+    sh = w.shape
+    inp = device_inputs(w, b, seed)
+    params, grads, x, dy = inp["layers"], inp["grads"], inp["x"], inp["dy"]
+    ss = ServerStack(sh.num_layers, sh.hidden, sh.num_heads, sh.ffn_hidden, sh.rotary_dim, w.dtype, sh.rope_base,
+                     sh.ln_eps, w.num_prefix)
+    bd = BatchDesc.from_batch(b)
+    saved, ws = ss.buffers(bd, w.recompute, with_saved=w.backward)
+    y = torch.empty_like(x)
+    dx = torch.empty_like(x) if w.backward else None
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ss.forward(bd, params, x, y, saved, ws, w.recompute, stream)
+        if w.backward:
+            ss.backward(bd, params, grads, x, saved, dy, dx, ws, w.recompute, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    F.fl_stack_profile(ss.handle, 1)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    prof = F.profile_table(ss.handle)
+    F.fl_stack_profile(ss.handle, 0)
+    ss.close()
+    del inp, params, grads, x, dy, y, dx, saved, ws
+    torch.cuda.empty_cache()
+    peak = PEAK_TFLOPS[w.dtype] * 1e12
+    gemm_ms = sum(prof[k]["ms"] for k in GEMM_CLASSES if k in prof)
+    gemm_fl = sum(prof[k]["flops"] for k in GEMM_CLASSES if k in prof)
+    fl = algorithmic_flops(w, b)
+    return {"tokens_s": round(b.total_tokens / (ms / 1e3), 1), "ms_per_step": round(ms, 3), "steps": steps,
+            "warmup": warmup, "total_tokens": b.total_tokens, "blocks": sh.num_layers,
+            "backward": w.backward, "recompute": w.recompute, "mask": w.mask, "ptuning_prefix": w.num_prefix,
+            "mfma_util": round(fl["total"] / (ms / 1e3) / peak, 4),
+            "gemm_mfma_util": round(gemm_fl / (gemm_ms / 1e3) / peak, 4) if gemm_ms else None}
 
 
 def main() -> int:
@@ -587,6 +671,8 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of CPU oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the short runs of the other workloads reported under 'secondary'")
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
                     help="only run the counter-calibration copy kernel over MIB MiB")
@@ -827,10 +913,20 @@ def main() -> int:
                          "avg_launch_us": round(us, 2), "bytes_per_launch": per * arena.n,
                          "achieved_gbs": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    close()
+    del inp, params, grads
+    torch.cuda.empty_cache()
+    if not args.no_secondary and args.workload == DEFAULT_WORKLOAD and arena is None:
+        out["secondary"] = {}
+        for name, n_steps, n_warm in SECONDARY_WORKLOADS:
+            try:
+                out["secondary"][name] = secondary_run(name, args.seed, n_steps, n_warm)
+            except Exception as e:  # pragma: no cover - reported, the headline line still prints
+                out["secondary"][name] = {"error": repr(e)}
+            print(f"[bench] secondary {name}: {out['secondary'][name]}", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, b, args.cpu_budget)
-    close()
     print(json.dumps(out))
     return 0
 

@@ -164,3 +164,24 @@ def test_summarize_mfma_on_a_synthetic_run(tmp_path):
     assert int(line[1]) == 1 and float(line[2]) == 1024.0 and float(line[4]) == pytest.approx(1.0)
     assert float(line[5]) == pytest.approx((50.0 * 100 + 10.0 * 10) / 110, abs=0.05)
     assert not any(l.startswith("layernorm_fwd") for l in out.splitlines())
+
+
+def test_spread_order_covers_the_length_distribution():
+    """Every sequence once; the first picks are the median, then the
+    quartiles, so a budget-limited prefix of the order samples the whole
+    length distribution rather than its short end."""
+    lens = [5, 1, 9, 3, 7, 2, 8, 4]
+    o = bench.spread_order(lens)
+    assert sorted(o) == list(range(len(lens)))
+    assert [lens[i] for i in o[:3]] == [5, 3, 8]
+    b = synth.WORKLOADS["chatglm6b_26blk_ragged_32x1_recompute"].batch()
+    first = [int(b.seqlens[i]) for i in bench.spread_order(b.seqlens)[:3]]
+    assert min(first) > int(b.seqlens.min()) and max(first) < int(b.seqlens.max())
+    assert sorted(first)[1] == sorted(b.seqlens.tolist())[len(b.seqlens) // 2]
+
+
+def test_cpu_baseline_is_the_float32_oracle():
+    w = synth.WORKLOADS["tiny_2blk_fp32"]
+    r = bench.cpu_baseline(w, w.batch(), budget_s=0.01)
+    assert r["kind"] == "oracle" and r["value"] > 0 and r["cores"] >= 1
+    assert "float32" in r["sample"] and "spread over" in r["sample"]
