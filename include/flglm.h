@@ -172,6 +172,30 @@ int fl_server_stack_forward(fl_stack* stack, const fl_batch_desc* batch, const f
                             const void* x, void* y, void* saved, int recompute, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* Allocation-free inference forward, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  Computes what fl_server_stack_forward
+ * computes with saved = NULL (the same kernels in the same order: the same
+ * bits), with two differences:
+ *   - the workspace is a static device array of FL_NOALLOC_SCRATCH_BYTES
+ *     that the library holds on every GPU it runs on until the process ends
+ *     (its address is looked up on the first call on each device); a batch
+ *     whose forward needs more (at the ChatGLM-6B block shape, about 1800
+ *     tokens) gets FL_ERR_WORKSPACE;
+ *   - the batch plan travels in kernel arguments, not through pinned
+ *     staging: at most FL_NOALLOC_MAX_SEQS sequences, else FL_ERR_ARG.
+ * It calls no hipMalloc, hipFree, hipHostMalloc or event creation; launch
+ * timing (fl_stack_profile) is off for its launches.  Every call on one GPU
+ * shares that GPU's array and leaves it holding the last call's
+ * intermediates: calls that overlap on one GPU (other streams, threads or
+ * handles) race, so callers serialise them.  Validation errors are returned
+ * before anything is enqueued, as for the other entry points.
+ *   x  device [T, H]  (not modified);  y  device [T, H], not overlapping x */
+#define FL_NOALLOC_SCRATCH_BYTES (256u << 20)
+#define FL_NOALLOC_MAX_SEQS 256
+int fl_server_stack_forward_noalloc(fl_stack* stack, const fl_batch_desc* batch, const fl_layer_params* layers,
+                                    const void* x, void* y, void* stream);
+
 /* Backward through blocks N..1 after a forward with the same batch, params,
  * x and recompute flag that filled `saved`.
  *   dy  device [T, H]  dL/dh_{N-2} from the clients (not modified)

@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -240,14 +241,16 @@ void carve_plan(Carver& cv, const BatchInfo& bi, int rotary_dim, Plan* p) {
   p->sin_t = (float*)cv.take(tab);
 }
 
-void carve_acts(Carver& cv, const fl_stack* st, int T, Acts* a) {
+// with_z = false: no room for the FFN pre-activation (an inference forward
+// never stores it).
+void carve_acts(Carver& cv, const fl_stack* st, int T, Acts* a, bool with_z = true) {
   const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, nh = st->d.num_heads;
   a->u = cv.take(E * T * H);
   a->qkv = cv.take(E * T * 3 * H);
   a->o = cv.take(E * T * H);
   a->h = cv.take(E * T * H);
   a->w = cv.take(E * T * H);
-  a->z = cv.take(E * T * F);
+  a->z = with_z ? cv.take(E * T * F) : nullptr;
   a->g = cv.take(E * T * F);
   a->lse = (float*)cv.take(sizeof(float) * T * nh);
   a->mean1 = (float*)cv.take(sizeof(float) * T);
@@ -313,6 +316,27 @@ size_t work_bytes(const fl_stack* st, const BatchInfo& bi) {
   return cv.off;
 }
 
+// What an inference forward (no saved activations) touches: the batch plan,
+// the GEMM split-reduction scratch, one block's intermediates without z,
+// and the two ping-pong block outputs.  Same sizes as carve_work's, so the
+// GEMMs split their reductions the same way.
+void carve_fwd_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
+  const size_t E = st->E, H = st->d.hidden, T = bi.T;
+  *w = Work();
+  carve_plan(cv, bi, st->d.rotary_dim, &w->plan);
+  w->plan.gemm_part_bytes = st->d.dtype == FL_BF16 ? gemm_part_bytes() : 0;
+  w->plan.gemm_part = w->plan.gemm_part_bytes ? (float*)cv.take(w->plan.gemm_part_bytes) : nullptr;
+  carve_acts(cv, st, bi.T, &w->acts, false);
+  w->ping[0] = cv.take(E * T * H);
+  w->ping[1] = cv.take(E * T * H);
+}
+size_t fwd_work_bytes(const fl_stack* st, const BatchInfo& bi) {
+  Carver cv(nullptr);
+  Work w;
+  carve_fwd_work(cv, st, bi, &w);
+  return cv.off;
+}
+
 // ---------------------------------------------------------------------------
 // Checks on device pointers
 // ---------------------------------------------------------------------------
@@ -365,6 +389,19 @@ int check_grads(const fl_stack* st, const fl_layer_grads* grads) {
 // ---------------------------------------------------------------------------
 // Plan upload: host descriptor arrays -> pinned staging ring -> workspace.
 // ---------------------------------------------------------------------------
+// Once cu_seqlens and the prefix lengths are on the device: every row's
+// position inside its sequence and the rotary table.
+int plan_kernels(fl_stack* st, const BatchInfo& bi, const Plan& p, hipStream_t stream) {
+  hipStream_t s = stream;
+  LAUNCH(FL_PROF_PLAN, 0, 4.0 * bi.T, [&]() {
+    hipError_t e = st->d.rotary_2d ? seq_positions_2d(p.cu, bi.prefix ? p.prefix : nullptr, bi.S, p.pos, p.pos2, stream)
+                                   : seq_positions(p.cu, bi.S, p.pos, stream);
+    return e != hipSuccess ? e
+                           : rope_table(p.cos_t, p.sin_t, bi.maxL + 1, st->d.rotary_dim, st->d.rope_base, stream);
+  }());
+  return FL_OK;
+}
+
 int upload_plan(fl_stack* st, const fl_batch_desc* b, const BatchInfo& bi, const Plan& p, hipStream_t stream) {
   const size_t ncu = bi.S + 1, npre = bi.S;
   const size_t bytes = sizeof(int32_t) * (ncu + npre);
@@ -390,14 +427,7 @@ int upload_plan(fl_stack* st, const fl_batch_desc* b, const BatchInfo& bi, const
   HIP_OK(hipMemcpyAsync(p.prefix, h + ncu, sizeof(int32_t) * npre, hipMemcpyHostToDevice, stream));
   HIP_OK(hipEventRecord(st->ev[k], stream));
   st->ev_used[k] = true;
-  hipStream_t s = stream;
-  LAUNCH(FL_PROF_PLAN, 0, 4.0 * bi.T, [&]() {
-    hipError_t e = st->d.rotary_2d ? seq_positions_2d(p.cu, bi.prefix ? p.prefix : nullptr, bi.S, p.pos, p.pos2, stream)
-                                   : seq_positions(p.cu, bi.S, p.pos, stream);
-    return e != hipSuccess ? e
-                           : rope_table(p.cos_t, p.sin_t, bi.maxL + 1, st->d.rotary_dim, st->d.rope_base, stream);
-  }());
-  return FL_OK;
+  return plan_kernels(st, bi, p, stream);
 }
 
 // Algorithmic work of one launch, for the opt-in launch timing.
@@ -613,6 +643,62 @@ namespace flglm {
 int set_error(int code, const char* msg) { return fail(code, "%s", msg); }
 }  // namespace flglm
 
+// ---------------------------------------------------------------------------
+// Allocation-free inference forward: the workspace is this file-scope device
+// array (one per GPU, held until the process ends) instead of a caller
+// buffer, and the batch plan travels in kernel arguments instead of through
+// pinned host staging.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)FL_NOALLOC_SCRATCH_BYTES;
+// Host code never uses this name as an address (it is a host-side stand-in
+// there): it takes each device's address with hipGetSymbolAddress.
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct PlanArgs {
+  int32_t num_seqs;
+  int32_t cu[FL_NOALLOC_MAX_SEQS + 1];
+  int32_t prefix[FL_NOALLOC_MAX_SEQS];
+};
+__global__ void plan_args_kernel(PlanArgs a, int32_t* cu, int32_t* prefix) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= a.num_seqs) cu[i] = a.cu[i];
+  if (i < a.num_seqs) prefix[i] = a.prefix[i];
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The scratch array's address on the current device, looked up once per
+// device (with that device current) and kept.
+int scratch_base(void** out) {
+  int dev = -1;
+  HIP_OK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(FL_ERR_HIP, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    HIP_OK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(FL_ERR_HIP, "hipGetSymbolAddress gave no address for the scratch array");
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return FL_OK;
+}
+
+// Launch timing records events; the allocation-free call turns it off for
+// its own launches and restores it.
+struct ProfOff {
+  fl_stack* st;
+  bool was;
+  explicit ProfOff(fl_stack* s) : st(s), was(s->prof) { st->prof = false; }
+  ~ProfOff() { st->prof = was; }
+};
+
+}  // namespace
+
 // ===========================================================================
 // C ABI
 // ===========================================================================
@@ -754,6 +840,51 @@ int fl_server_stack_forward(fl_stack* st, const fl_batch_desc* b, const fl_layer
     const Acts& a = keep ? sv.acts[l] : w.acts;
     void* out = (l == N - 1) ? y : (saved ? sv.xin[l + 1] : w.ping[l & 1]);
     if ((rc = block_forward(st, bi, w.plan, layers[l], cur, a, out, s, keep))) return rc;
+    cur = out;
+  }
+  return FL_OK;
+}
+
+int fl_server_stack_forward_noalloc(fl_stack* st, const fl_batch_desc* b, const fl_layer_params* layers,
+                                    const void* x, void* y, void* stream) {
+  if (!st) return fail(FL_ERR_NULL, "stack is NULL");
+  BatchInfo bi;
+  int rc = validate_batch(b, &bi);
+  if (rc) return rc;
+  if (bi.S > FL_NOALLOC_MAX_SEQS)
+    return fail(FL_ERR_ARG, "%d sequences: the allocation-free forward takes at most %d", bi.S, FL_NOALLOC_MAX_SEQS);
+  if ((rc = check_params(st, layers))) return rc;
+  if (!x || !y) return fail(FL_ERR_NULL, "x / y is NULL");
+  if (!aligned16(x) || !aligned16(y)) return fail(FL_ERR_ALIGN, "x / y must be 16-byte aligned");
+  const size_t need = fwd_work_bytes(st, bi);
+  if (need > kScratchBytes)
+    return fail(FL_ERR_WORKSPACE, "batch of %d tokens needs %zu bytes of scratch; the static scratch holds %zu", bi.T,
+                need, kScratchBytes);
+  const size_t act = (size_t)st->E * bi.T * st->d.hidden;
+  if (overlap(x, act, y, act)) return fail(FL_ERR_ALIAS, "y overlaps x");
+  void* base = nullptr;
+  if ((rc = scratch_base(&base))) return rc;
+  if (overlap(base, kScratchBytes, x, act) || overlap(base, kScratchBytes, y, act))
+    return fail(FL_ERR_ALIAS, "x / y overlap the library's scratch array");
+
+  hipStream_t s = (hipStream_t)stream;
+  Carver cw(base);
+  Work w;
+  carve_fwd_work(cw, st, bi, &w);
+  PlanArgs pa;
+  pa.num_seqs = bi.S;
+  std::memcpy(pa.cu, b->cu_seqlens, sizeof(int32_t) * (bi.S + 1));
+  if (bi.prefix) std::memcpy(pa.prefix, b->prefix_len, sizeof(int32_t) * bi.S);
+  else std::memset(pa.prefix, 0, sizeof(int32_t) * bi.S);
+  ProfOff off(st);
+  hipLaunchKernelGGL(plan_args_kernel, dim3((bi.S + 1 + 255) / 256), dim3(256), 0, s, pa, w.plan.cu, w.plan.prefix);
+  HIP_OK(hipGetLastError());
+  if ((rc = plan_kernels(st, bi, w.plan, s))) return rc;
+  const int N = st->d.num_layers;
+  const void* cur = x;
+  for (int l = 0; l < N; ++l) {
+    void* out = (l == N - 1) ? y : w.ping[l & 1];
+    if ((rc = block_forward(st, bi, w.plan, layers[l], cur, w.acts, out, s, false))) return rc;
     cur = out;
   }
   return FL_OK;

@@ -25,6 +25,8 @@ FL_MASK_CAUSAL, FL_MASK_PREFIX = 0, 1
 FL_GEMM_NT, FL_GEMM_NN, FL_GEMM_TN = 0, 1, 2
 FL_EPI_STORE, FL_EPI_BIAS, FL_EPI_BIAS_RES, FL_EPI_BIAS_GELU, FL_EPI_GELU_BWD, FL_EPI_ACC_F32, FL_EPI_RES = range(7)
 FL_PROF_NUM_CLASSES = 14
+FL_NOALLOC_SCRATCH_BYTES = 256 << 20
+FL_NOALLOC_MAX_SEQS = 256
 
 PARAM_FIELDS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
                 "ln1_g", "ln1_b", "ln2_g", "ln2_b")
@@ -33,7 +35,8 @@ PREFIX_FIELDS = ("prefix_k", "prefix_v")  # P-tuning v2 prefix keys / values
 #: every extern "C" symbol the headers declare
 EXPORTS = (
     "fl_stack_create", "fl_stack_destroy", "fl_stack_saved_bytes", "fl_stack_workspace_bytes",
-    "fl_server_stack_forward", "fl_server_stack_backward", "fl_client_token_range",
+    "fl_server_stack_forward", "fl_server_stack_forward_noalloc", "fl_server_stack_backward",
+    "fl_client_token_range",
     "fl_pack_clients", "fl_unpack_clients", "fl_last_error",
     "fl_adam_step", "fl_average_replicas",
     "fl_client_create", "fl_client_destroy", "fl_client_workspace_bytes", "fl_embedding_forward",
@@ -98,6 +101,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_stack_saved_bytes": [vp, P(fl_batch_desc), ctypes.c_int, P(sz)],
         "fl_stack_workspace_bytes": [vp, P(fl_batch_desc), ctypes.c_int, P(sz)],
         "fl_server_stack_forward": [vp, P(fl_batch_desc), P(fl_layer_params), vp, vp, vp, ctypes.c_int, vp, sz, vp],
+        "fl_server_stack_forward_noalloc": [vp, P(fl_batch_desc), P(fl_layer_params), vp, vp, vp],
         "fl_server_stack_backward": [vp, P(fl_batch_desc), P(fl_layer_params), P(fl_layer_grads), vp, vp, vp, vp,
                                      ctypes.c_int, vp, sz, vp],
         "fl_client_token_range": [P(fl_batch_desc), i32, P(i64), P(i64)],
@@ -250,6 +254,13 @@ def fl_server_stack_forward(handle: int, batch: BatchDesc, layers: Sequence[fl_l
     arr = (fl_layer_params * len(layers))(*layers)
     _check(load().fl_server_stack_forward(handle, ctypes.byref(batch.desc), arr, _ptr(x), _ptr(y), _ptr(saved),
                                           int(recompute), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def fl_server_stack_forward_noalloc(handle: int, batch: BatchDesc, layers: Sequence[fl_layer_params], x, y,
+                                    stream=None) -> None:
+    arr = (fl_layer_params * len(layers))(*layers)
+    _check(load().fl_server_stack_forward_noalloc(handle, ctypes.byref(batch.desc), arr, _ptr(x), _ptr(y),
+                                                  _stream(stream)))
 
 
 def fl_server_stack_backward(handle: int, batch: BatchDesc, layers: Sequence[fl_layer_params],

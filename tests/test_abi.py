@@ -272,3 +272,25 @@ def test_missing_library_raises_instead_of_falling_back():
     r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "HIP library not built" in r.stdout
+
+
+def test_noalloc_forward_rejects_what_does_not_fit():
+    """The allocation-free forward's limits are checked on the host before
+    anything else: a batch larger than the static scratch array, or with more
+    sequences than its kernel-argument plan holds."""
+    _lib()
+    h = F.fl_stack_create(F.stack_desc(1, 4096, 32, 16384, 64, F.FL_BF16))
+    L = F.fl_layer_params(*([256] * 12))
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_server_stack_forward_noalloc(h, F.BatchDesc([0, 4000], [0, 1]), [L], 1 << 40, 1 << 41, 0)
+    assert e.value.code == F.FL_ERR_WORKSPACE and "scratch" in str(e.value)
+    many = list(range(F.FL_NOALLOC_MAX_SEQS + 2))
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_server_stack_forward_noalloc(h, F.BatchDesc(many, [0, F.FL_NOALLOC_MAX_SEQS + 1]), [L], 1 << 40,
+                                          1 << 41, 0)
+    assert e.value.code == F.FL_ERR_ARG
+    # a batch that fits: rejected only for the NULL output (still no device work)
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_server_stack_forward_noalloc(h, F.BatchDesc([0, 1000], [0, 1]), [L], 1 << 40, None, 0)
+    assert e.value.code == F.FL_ERR_NULL
+    F.fl_stack_destroy(h)
