@@ -157,6 +157,140 @@ __device__ __forceinline__ void tile_coords2(int wg, int nwg, int tiles_m, int t
   tn = in_group / gsize;
 }
 
+// Bare workgroup barrier: a fence would also wait for DMA stages in flight.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Epilogue of one 256 x 256 tile from the wave accumulators acc[i][j]
+// (wave tile rows 128 (wave & 1) + 16 j, columns 64 (wave >> 1) + 16 i), with
+// the LDS at stg (at least 128 KB, free: every wave is past its operand
+// reads) as staging.
+template <int EPI>
+__device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc)[kWTN][kWTM], float* stg, int tm,
+                                              int m0, int n0, int tid) {
+  asm volatile("" : "+v"(tid));  // keeps the epilogue's per-lane values out of the main loop's live range
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int fr = lane & 15, fg = lane >> 4;
+  auto barrier = [&]() { wg_barrier(); };
+  // Epilogue, staged through LDS so that every global access is a full row
+  // segment: the accumulators of one 128-row half of the tile go to LDS as
+  // fp32 ([128][256], 16-byte chunk c of row r at c ^ (r & 15)); then each
+  // wave owns whole rows, a lane four consecutive columns, and bias,
+  // residual, GeLU input and output rows are read and written contiguously
+  // (a lane of the matrix core holds 4 columns of 16 different rows, which
+  // as direct stores cost more than the reduction for K = 4096).
+  const int n = n0 + 4 * lane;
+  float bias[4] = {0.f, 0.f, 0.f, 0.f};
+  // EPI_GELU_BWD with colsum: this lane's four columns summed over its rows
+  // (the stored, rounded values), in row order
+  float csum[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
+    Vec4<bf16> b;
+    b.load(p.bias + n);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bias[e] = b.get(e);
+  }
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    constexpr int kRows = 128 / kWaves;
+    const int mbase = m0 + half * 128 + wave;
+    if (wm == half) {
+#pragma unroll
+      for (int j = 0; j < kWTM; ++j) {
+        const int r = 16 * j + fr;
+#pragma unroll
+        for (int i = 0; i < kWTN; ++i) {
+          const int c = (wn * 64 + 16 * i + 4 * fg) >> 2;
+          st16(stg + r * 256 + ((c ^ (r & 15)) << 2), __builtin_bit_cast(u32x4, acc[i][j]));
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();
+    // Rows wave + 8 q, in batches whose global loads (residual, GeLU input,
+    // fp32 accumulator) are issued together before their first use.
+    constexpr int kBatch = EPI == EPI_ACC_F32 ? 4 : 8;
+#pragma unroll
+    for (int q0 = 0; q0 < kRows; q0 += kBatch) {
+      Vec4<bf16> ext[kBatch];
+      Vec4<float> cacc[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const long m = mbase + (q0 + u) * kWaves;
+        if (m < p.M) {
+          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) ext[u].load(p.R + m * p.ldr + n);
+          if constexpr (EPI == EPI_GELU_BWD) ext[u].load(p.Z + m * p.ldz + n);
+          if constexpr (EPI == EPI_ACC_F32) cacc[u].load(static_cast<float*>(p.C) + m * p.ldc + n);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int r = wave + (q0 + u) * kWaves;
+        const long m = mbase + (q0 + u) * kWaves;
+        if (m >= p.M) break;
+        const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
+        if constexpr (EPI == EPI_ACC_F32) {
+          float o[4] = {cacc[u].get(0) + v[0], cacc[u].get(1) + v[1], cacc[u].get(2) + v[2], cacc[u].get(3) + v[3]};
+          cacc[u].set(o);
+          cacc[u].store(static_cast<float*>(p.C) + m * p.ldc + n);
+        } else {
+          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] += p.res_scale * ext[u].get(e);
+          }
+          if constexpr (EPI == EPI_GELU_BWD) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[u].get(e));
+          }
+        Vec4<bf16> o;
+          o.set(v);
+          if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
+          if constexpr (EPI == EPI_GELU_BWD) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) csum[e] += o.get(e);
+          }
+          if constexpr (EPI == EPI_BIAS_GELU) {
+            float g[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
+            Vec4<bf16> og;
+            og.set(g);
+            og.store(p.C2 + m * p.ldc2 + n);
+          }
+        }
+      }
+    }
+    // the second half, or the next tile's loads, overwrite the staging area
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    barrier();
+  }
+  if constexpr (EPI == EPI_GELU_BWD) {
+    if (p.colsum) {
+      // the eight waves' partial column sums, added in wave order (the
+      // operand tiles are free: every wave has passed the barrier above)
+      float* cs = stg;
+      st16(cs + wave * kBN + 4 * lane, __builtin_bit_cast(u32x4, f32x4{csum[0], csum[1], csum[2], csum[3]}));
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();
+      if (tid < kBN) {
+        float t = 0.f;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) t += cs[w2 * kBN + tid];
+        p.colsum[(long)tm * p.N + n0 + tid] = t;
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier();  // the next tile's loads overwrite cs
+    }
+  }
+}
+
 template <bool AK, bool BKc, int EPI>
 __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kTileElems];  // [stage][A/B]
@@ -356,122 +490,9 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
     continue;
   }
 
-  // Epilogue, staged through LDS so that every global access is a full row
-  // segment: the accumulators of one 128-row half of the tile go to LDS as
-  // fp32 ([128][256], 16-byte chunk c of row r at c ^ (r & 15)); then each
-  // wave owns whole rows, a lane four consecutive columns, and bias,
-  // residual, GeLU input and output rows are read and written contiguously
-  // (a lane of the matrix core holds 4 columns of 16 different rows, which
-  // as direct stores cost more than the reduction for K = 4096).
-  float* stg = reinterpret_cast<float*>(&smem[0][0][0]);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   barrier();  // every wave is done with the operand tiles
-  const int n = n0 + 4 * lane;
-  float bias[4] = {0.f, 0.f, 0.f, 0.f};
-  // EPI_GELU_BWD with colsum: this lane's four columns summed over its rows
-  // (the stored, rounded values), in row order
-  float csum[4] = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
-    Vec4<bf16> b;
-    b.load(p.bias + n);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) bias[e] = b.get(e);
-  }
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    constexpr int kRows = 128 / kWaves;
-    const int mbase = m0 + half * 128 + wave;
-    if (wm == half) {
-#pragma unroll
-      for (int j = 0; j < kWTM; ++j) {
-        const int r = 16 * j + fr;
-#pragma unroll
-        for (int i = 0; i < kWTN; ++i) {
-          const int c = (wn * 64 + 16 * i + 4 * fg) >> 2;
-          st16(stg + r * 256 + ((c ^ (r & 15)) << 2), __builtin_bit_cast(u32x4, acc[i][j]));
-        }
-      }
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    barrier();
-    // Rows wave + 8 q, in batches whose global loads (residual, GeLU input,
-    // fp32 accumulator) are issued together before their first use.
-    constexpr int kBatch = EPI == EPI_ACC_F32 ? 4 : 8;
-#pragma unroll
-    for (int q0 = 0; q0 < kRows; q0 += kBatch) {
-      Vec4<bf16> ext[kBatch];
-      Vec4<float> cacc[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const long m = mbase + (q0 + u) * kWaves;
-        if (m < p.M) {
-          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) ext[u].load(p.R + m * p.ldr + n);
-          if constexpr (EPI == EPI_GELU_BWD) ext[u].load(p.Z + m * p.ldz + n);
-          if constexpr (EPI == EPI_ACC_F32) cacc[u].load(static_cast<float*>(p.C) + m * p.ldc + n);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int r = wave + (q0 + u) * kWaves;
-        const long m = mbase + (q0 + u) * kWaves;
-        if (m >= p.M) break;
-        const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
-        if constexpr (EPI == EPI_ACC_F32) {
-          float o[4] = {cacc[u].get(0) + v[0], cacc[u].get(1) + v[1], cacc[u].get(2) + v[2], cacc[u].get(3) + v[3]};
-          cacc[u].set(o);
-          cacc[u].store(static_cast<float*>(p.C) + m * p.ldc + n);
-        } else {
-          if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += p.res_scale * ext[u].get(e);
-          }
-          if constexpr (EPI == EPI_GELU_BWD) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[u].get(e));
-          }
-        Vec4<bf16> o;
-          o.set(v);
-          if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
-          if constexpr (EPI == EPI_GELU_BWD) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) csum[e] += o.get(e);
-          }
-          if constexpr (EPI == EPI_BIAS_GELU) {
-            float g[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
-            Vec4<bf16> og;
-            og.set(g);
-            og.store(p.C2 + m * p.ldc2 + n);
-          }
-        }
-      }
-    }
-    // the second half, or the next tile's loads, overwrite the staging area
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    barrier();
-  }
-  if constexpr (EPI == EPI_GELU_BWD) {
-    if (p.colsum) {
-      // the eight waves' partial column sums, added in wave order (the
-      // operand tiles are free: every wave has passed the barrier above)
-      float* cs = reinterpret_cast<float*>(&smem[0][0][0]);
-      st16(cs + wave * kBN + 4 * lane, __builtin_bit_cast(u32x4, f32x4{csum[0], csum[1], csum[2], csum[3]}));
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();
-      if (tid < kBN) {
-        float t = 0.f;
-#pragma unroll
-        for (int w2 = 0; w2 < kWaves; ++w2) t += cs[w2 * kBN + tid];
-        p.colsum[(long)tm * p.N + n0 + tid] = t;
-      }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();  // the next tile's loads overwrite cs
-    }
-  }
+  tile_epilogue<EPI>(p, acc, reinterpret_cast<float*>(&smem[0][0][0]), tm, m0, n0, tid);
   }
 }
 
