@@ -57,6 +57,15 @@ int fl_test_layernorm_fwd(int dtype, const void* x, const void* g, const void* b
  * are produced by the column-sum kernel, see fl_test_colsum). */
 int fl_test_layernorm_bwd(int dtype, const void* dy, const void* x, const float* mean, const float* rstd,
                           const void* g, const void* dres, void* dx, int T, int H, void* stream);
+/* The LayerNorm backward the stack runs, fused with its column sums: dx as
+ * above (dres may be NULL: no residual), and, when given (fp32, +=),
+ * dgamma[n] = sum_t dy[t][n] xh[t][n], dbeta[n] = sum_t dy[t][n] (both or
+ * neither) and dsum[n] = sum_t dx[t][n] (the stored, rounded dx).  partial:
+ * device fp32 scratch of 3 * 512 * H floats (needed when any sum is asked
+ * for). */
+int fl_test_layernorm_bwd_fused(int dtype, const void* dy, const void* x, const float* mean, const float* rstd,
+                                const void* g, const void* dres, void* dx, int T, int H, float* dgamma, float* dbeta,
+                                float* dsum, float* partial, void* stream);
 /* out[n] += sum_t X[t][n] (mode 0); mode 1: out[n] += sum_t X[t][n] *
  * (Y[t][n] - mean[t]) * rstd[t] and out2[n] += sum_t X[t][n].
  * partial: device fp32 scratch of at least ceil(T/256) * N * 2 floats. */

@@ -181,6 +181,90 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, con
   if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
 }
 
+// The stack's LayerNorm forward: workgroup b of kLnBlocks takes an even
+// share of the rows across all H columns, wave w columns [512 w, 512 w + 512)
+// (eight per lane, the gain and shift loaded once into registers), rows four
+// at a time; the row sums and then the sums of squared deviations are
+// combined over the waves through LDS in wave order (two-pass statistics,
+// as in ln_fwd_kernel).  Each row read is one contiguous 1 KB segment per
+// wave, and the grid is one balanced round.
+template <typename T>
+__global__ void __launch_bounds__(512) ln_fwd_rows_kernel(const T* x, const T* g, const T* b, T* y, float* mean,
+                                                          float* rstd, int T_, int H, float eps) {
+  __shared__ float red[2][4][8];  // [phase][row][wave]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = w * 512 + lane * 8;
+  const bool on = col < H;
+  const int nw = (H + 511) / 512;
+  const int r0 = (int)((long)T_ * blockIdx.x / kLnBlocks), r1 = (int)((long)T_ * (blockIdx.x + 1) / kLnBlocks);
+  float gv[8], bv[8];
+  {
+    Vec8<T> gg, bb;
+    if (on) { gg.load(g + col); bb.load(b + col); } else { gg.zero(); bb.zero(); }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { gv[e] = gg.get(e); bv[e] = bb.get(e); }
+  }
+  const float invH = 1.f / (float)H;
+  for (int rb = r0; rb < r1; rb += 4) {
+    Vec8<T> xv[4];
+    float s[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (on && rb + u < r1) xv[u].load(x + (long)(rb + u) * H + col); else xv[u].zero();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float t = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t += xv[u].get(e);
+      s[u] = wave_sum(t);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) red[0][u][w] = s[u];
+    }
+    __syncthreads();
+    float mu[4], ss[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float t = 0.f;
+      for (int v = 0; v < nw; ++v) t += red[0][u][v];
+      mu[u] = t * invH;
+      float q = 0.f;
+      if (on) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { const float d = xv[u].get(e) - mu[u]; q += d * d; }
+      }
+      ss[u] = wave_sum(q);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) red[1][u][w] = ss[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float t = 0.f;
+      for (int v = 0; v < nw; ++v) t += red[1][u][v];
+      const float rs = 1.0f / sqrtf(t * invH + eps);
+      const int r = rb + u;
+      if (r < r1) {
+        if (on) {
+          float out[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) out[e] = (xv[u].get(e) - mu[u]) * rs * gv[e] + bv[e];
+          Vec8<T> o;
+          o.set(out);
+          o.store(y + (long)r * H + col);
+        }
+        if (threadIdx.x == 0) { mean[r] = mu[u]; rstd[r] = rs; }
+      }
+    }
+    // red[0] is rewritten by the next batch only after its every wave has
+    // passed this batch's second barrier, red[1] after its first
+  }
+}
+
 template <typename T, int MAXC>
 __global__ void __launch_bounds__(256) ln_bwd_dx_kernel(const T* dy, const T* x, const float* mean,
                                                         const float* rstd, const T* g, const T* dres, T* dx, int T_,
@@ -275,11 +359,147 @@ hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, 
                        : ln_fwd_t<float>(x, g, b, y, mean, rstd, T_, H, eps, st);
 }
 
+hipError_t layernorm_fwd_rows(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
+                              float* rstd, int T_, int H, float eps, hipStream_t st) {
+  if (T_ <= 0) return hipSuccess;
+  if (H > 4096 || H % 8 != 0) return hipErrorInvalidValue;
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((ln_fwd_rows_kernel<bf16>), dim3(kLnBlocks), dim3(512), 0, st, (const bf16*)x, (const bf16*)g,
+                       (const bf16*)b, (bf16*)y, mean, rstd, T_, H, eps);
+  else
+    hipLaunchKernelGGL((ln_fwd_rows_kernel<float>), dim3(kLnBlocks), dim3(512), 0, st, (const float*)x,
+                       (const float*)g, (const float*)b, (float*)y, mean, rstd, T_, H, eps);
+  return hipGetLastError();
+}
+
 hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
                             const void* g, const void* dres, void* dx, int T_, int H, hipStream_t st) {
   if (T_ <= 0) return hipSuccess;
   return dt == DT_BF16 ? ln_bwd_t<bf16>(dy, x, mean, rstd, g, dres, dx, T_, H, st)
                        : ln_bwd_t<float>(dy, x, mean, rstd, g, dres, dx, T_, H, st);
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm backward fused with the column sums that follow it.  Workgroup b
+// of kLnBlocks takes rows [T b / kLnBlocks, T (b + 1) / kLnBlocks) (an even
+// share, so the grid is one balanced round) across all H columns: wave w
+// owns columns [512 w, 512 w + 512), eight per lane, so each row read is one
+// contiguous 1 KB segment per wave.  Rows go four at a time; a row's two
+// sums (of dxh and dxh * xh) are combined over the waves through LDS in wave
+// order, then every lane finishes its columns of dx and adds, per column
+// and in row order, dy * xh (the gain gradient), dy (the shift gradient) and
+// optionally dx itself (the bias gradient of the layer that produced this
+// LayerNorm's input).  The per-block sums go to partial [b][H] (fp32), which
+// colsum_finish adds in block order: deterministic.  One pass reads dy, x
+// (and dres) once, instead of once for dx and again for the column sums.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T* x, const float* mean,
+                                                           const float* rstd, const T* g, const T* dres, T* dx,
+                                                           int T_, int H, float* pg, float* pb, float* pout) {
+  __shared__ float red[2][4][8][2];  // [batch parity][row][wave][sum]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = w * 512 + lane * 8;
+  const bool on = col < H;
+  const int nw = (H + 511) / 512;  // waves holding columns
+  const int r0 = (int)((long)T_ * blockIdx.x / kLnBlocks), r1 = (int)((long)T_ * (blockIdx.x + 1) / kLnBlocks);
+  float gv[8], ag[8], ab[8], ao[8];
+  {
+    Vec8<T> gg;
+    if (on) gg.load(g + col); else gg.zero();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { gv[e] = gg.get(e); ag[e] = 0.f; ab[e] = 0.f; ao[e] = 0.f; }
+  }
+  const float invH = 1.f / (float)H;
+  int par = 0;
+  for (int rb = r0; rb < r1; rb += 4, par ^= 1) {
+    Vec8<T> a[4], xx[4], rr[4];
+    float mu[4], rs[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = rb + u;
+      const bool ok = on && r < r1;
+      if (ok) {
+        a[u].load(dy + (long)r * H + col);
+        xx[u].load(x + (long)r * H + col);
+        if (dres) rr[u].load(dres + (long)r * H + col); else rr[u].zero();
+      } else {
+        a[u].zero(); xx[u].zero(); rr[u].zero();
+      }
+      mu[u] = r < r1 ? mean[r] : 0.f;
+      rs[u] = r < r1 ? rstd[r] : 0.f;
+    }
+    float s1[4], s2[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      s1[u] = 0.f; s2[u] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xh = (xx[u].get(e) - mu[u]) * rs[u], d = a[u].get(e) * gv[e];
+        s1[u] += d;
+        s2[u] += d * xh;
+      }
+      s1[u] = wave_sum(s1[u]);
+      s2[u] = wave_sum(s2[u]);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) { red[par][u][w][0] = s1[u]; red[par][u][w][1] = s2[u]; }
+    }
+    __syncthreads();  // one barrier per batch: the other parity's slots are free again
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float t1 = 0.f, t2 = 0.f;
+      for (int v = 0; v < nw; ++v) { t1 += red[par][u][v][0]; t2 += red[par][u][v][1]; }
+      const float m1 = t1 * invH, m2 = t2 * invH;
+      const int r = rb + u;
+      if (on && r < r1) {
+        float out[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float xh = (xx[u].get(e) - mu[u]) * rs[u], dv = a[u].get(e);
+          out[e] = rr[u].get(e) + rs[u] * (dv * gv[e] - m1 - xh * m2);
+          ag[e] += dv * xh;
+          ab[e] += dv;
+        }
+        Vec8<T> o;
+        o.set(out);
+        o.store(dx + (long)r * H + col);
+        if (pout) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ao[e] += o.get(e);  // the stored (rounded) values
+        }
+      }
+    }
+  }
+  if (on) {
+    const long base = (long)blockIdx.x * H + col;
+    if (pg) {
+      st16(pg + base, u32x4{__float_as_uint(ag[0]), __float_as_uint(ag[1]), __float_as_uint(ag[2]), __float_as_uint(ag[3])});
+      st16(pg + base + 4, u32x4{__float_as_uint(ag[4]), __float_as_uint(ag[5]), __float_as_uint(ag[6]), __float_as_uint(ag[7])});
+      st16(pb + base, u32x4{__float_as_uint(ab[0]), __float_as_uint(ab[1]), __float_as_uint(ab[2]), __float_as_uint(ab[3])});
+      st16(pb + base + 4, u32x4{__float_as_uint(ab[4]), __float_as_uint(ab[5]), __float_as_uint(ab[6]), __float_as_uint(ab[7])});
+    }
+    if (pout) {
+      st16(pout + base, u32x4{__float_as_uint(ao[0]), __float_as_uint(ao[1]), __float_as_uint(ao[2]), __float_as_uint(ao[3])});
+      st16(pout + base + 4, u32x4{__float_as_uint(ao[4]), __float_as_uint(ao[5]), __float_as_uint(ao[6]), __float_as_uint(ao[7])});
+    }
+  }
+}
+
+hipError_t layernorm_bwd_fused(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
+                               const void* g, const void* dres, void* dx, int T_, int H, float* pg, float* pb,
+                               float* pout, hipStream_t st) {
+  if (T_ <= 0) return hipSuccess;
+  if (H > 4096 || H % 8 != 0 || (pg == nullptr) != (pb == nullptr)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)kLnBlocks), blk(512);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((ln_bwd_fused_kernel<bf16>), grid, blk, 0, st, (const bf16*)dy, (const bf16*)x, mean, rstd,
+                       (const bf16*)g, (const bf16*)dres, (bf16*)dx, T_, H, pg, pb, pout);
+  else
+    hipLaunchKernelGGL((ln_bwd_fused_kernel<float>), grid, blk, 0, st, (const float*)dy, (const float*)x, mean,
+                       rstd, (const float*)g, (const float*)dres, (float*)dx, T_, H, pg, pb, pout);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

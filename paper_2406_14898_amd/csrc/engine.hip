@@ -280,6 +280,7 @@ struct Work {
   void *dz, *dh, *tmp, *dqkv;
   float* delta;
   float *part, *part2;
+  float* lnp[3];  // fused LayerNorm backward partials: gain, shift, output sums, [kLnBlocks][H] each
   float* dprefix;
 };
 void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
@@ -298,6 +299,7 @@ void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   const size_t nmax = std::max(F, 3 * H);
   w->part = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
   w->part2 = (float*)cv.take(sizeof(float) * colsum_blocks(bi.T) * nmax);
+  for (int i = 0; i < 3; ++i) w->lnp[i] = (float*)cv.take(sizeof(float) * kLnBlocks * H);
   // per-sequence P-tuning v2 prefix gradients, [2][S][L_p][H] fp32
   const size_t np = st->d.num_prefix;
   w->dprefix = np ? (float*)cv.take(sizeof(float) * 2 * bi.S * np * H) : nullptr;
@@ -512,25 +514,37 @@ int colsum_into(fl_stack* st, DType dt, const void* X, long ldx, int T, int N, f
   return FL_OK;
 }
 
-// LayerNorm backward: dx = dres + LN^T(dy); gain/shift gradients += column sums.
+// LayerNorm backward: dx = dres + LN^T(dy); gain / shift gradients (NULL:
+// frozen) += their column sums and, with dsum, dsum += the column sums of dx
+// (the bias gradient of the projection that produced the LayerNorm's
+// input), all in the one pass over dy and x.
 int ln_backward(fl_stack* st, DType dt, const void* dy, const void* xin, const float* mean, const float* rstd,
-                const void* gamma, const void* dres, void* dx, float* dgamma, float* dbeta, int T, int H,
+                const void* gamma, const void* dres, void* dx, float* dgamma, float* dbeta, float* dsum, int T, int H,
                 const Work& w, hipStream_t s) {
   const double TH = (double)T * H, E = st->E;
-  LAUNCH(FL_PROF_LAYERNORM_BWD, 0, 4 * TH * E + 8.0 * T,
-         layernorm_bwd_dx(dt, dy, xin, mean, rstd, gamma, dres, dx, T, H, s));
-  if (!dgamma) return FL_OK;  // frozen weights
-  LAUNCH(FL_PROF_COLSUM, 0, 2 * TH * E + 8.0 * T, [&]() {
-    hipError_t e = colsum_partial(dt, 1, dy, H, xin, mean, rstd, T, H, w.part, w.part2, s);
-    if (e == hipSuccess) e = colsum_finish(w.part, colsum_blocks(T), H, dgamma, s);
-    return e != hipSuccess ? e : colsum_finish(w.part2, colsum_blocks(T), H, dbeta, s);
+  LAUNCH(FL_PROF_LAYERNORM_BWD, 0, (dres ? 4 : 3) * TH * E + 8.0 * T,
+         layernorm_bwd_fused(dt, dy, xin, mean, rstd, gamma, dres, dx, T, H, dgamma ? w.lnp[0] : nullptr,
+                             dgamma ? w.lnp[1] : nullptr, dsum ? w.lnp[2] : nullptr, s));
+  if (!dgamma && !dsum) return FL_OK;
+  LAUNCH(FL_PROF_COLSUM, 0, 4.0 * kLnBlocks * H * ((dgamma ? 2 : 0) + (dsum ? 1 : 0)), [&]() {
+    hipError_t e = hipSuccess;
+    if (dgamma) {
+      e = colsum_finish(w.lnp[0], kLnBlocks, H, dgamma, s);
+      if (e == hipSuccess) e = colsum_finish(w.lnp[1], kLnBlocks, H, dbeta, s);
+    }
+    return (e != hipSuccess || !dsum) ? e : colsum_finish(w.lnp[2], kLnBlocks, H, dsum, s);
   }());
   return FL_OK;
 }
 
 // One block backward: dy -> dx, gradients += .
+// dx_sum (or NULL): receives += the column sums of dx, formed in the last
+// LayerNorm backward's pass (dx is the dy of the block below, whose bias
+// gradient db_2 is that sum); b2_done: this block's db_2 was already added
+// that way by the block above.
 int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Work& w, const fl_layer_params& p,
-                   const fl_layer_grads& gr, const void* x, const Acts& a, const void* dy, void* dx, hipStream_t s) {
+                   const fl_layer_grads& gr, const void* x, const Acts& a, const void* dy, void* dx, hipStream_t s,
+                   float* dx_sum, bool b2_done) {
   const DType dt = (DType)st->d.dtype;
   const int T = bi.T, H = st->d.hidden, F = st->d.ffn_hidden;
   const double E = st->E;
@@ -544,7 +558,7 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   // y = h + g W_2^T + b_2
   GemmDesc g;
   if (train_w) {
-    if ((rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
+    if (!b2_done && (rc = colsum_into(st, dt, dy, H, T, H, gr.b_2, w, s))) return rc;
     g.A = dy; g.B = a.g; g.C = gr.w_2; g.M = H; g.N = F; g.K = T; g.lda = H; g.ldb = F; g.ldc = F;
     LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, F, T), gemm_bytes(H, F, T, E, 8),
            gemm(dt, GEMM_TN, EPI_ACC_F32, with_part(g, plan), s));
@@ -577,13 +591,13 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   }
   LAUNCH(FL_PROF_GEMM_NN, gemm_flops(T, H, F), gemm_bytes(T, H, F, E, E),
          gemm(dt, GEMM_NN, alpha > 0.f ? EPI_RES : EPI_STORE, with_part(g, plan), s));
-  // w = LN2(h); h also feeds y directly (plain residual)
+  // w = LN2(h); h also feeds y directly (plain residual).  db_o = the column
+  // sums of dh, formed in the same pass.
   if ((rc = ln_backward(st, dt, w.tmp, a.h, a.mean2, a.rstd2, p.ln2_g, alpha > 0.f ? nullptr : dy, w.dh, gr.ln2_g,
-                        gr.ln2_b, T, H, w, s)))
+                        gr.ln2_b, train_w ? gr.b_o : nullptr, T, H, w, s)))
     return rc;
   // h = x + o W_o^T + b_o
   if (train_w) {
-    if ((rc = colsum_into(st, dt, w.dh, H, T, H, gr.b_o, w, s))) return rc;
     g = GemmDesc();
     g.A = w.dh; g.B = a.o; g.C = gr.w_o; g.M = H; g.N = H; g.K = T; g.lda = H; g.ldb = H; g.ldc = H;
     LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(H, H, T), gemm_bytes(H, H, T, E, 8),
@@ -634,7 +648,7 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
          gemm(dt, GEMM_NN, alpha > 0.f ? EPI_RES : EPI_STORE, with_part(g, plan), s));
   // u = LN1(x); x also feeds h directly (plain residual)
   return ln_backward(st, dt, w.tmp, x, a.mean1, a.rstd1, p.ln1_g, alpha > 0.f ? nullptr : w.dh, dx, gr.ln1_g,
-                     gr.ln1_b, T, H, w, s);
+                     gr.ln1_b, dx_sum, T, H, w, s);
 }
 
 }  // namespace
@@ -930,7 +944,12 @@ int fl_server_stack_backward(fl_stack* st, const fl_batch_desc* b, const fl_laye
       a = &w.acts;
     }
     void* gout = (l == 0) ? dx : w.ping[(N - 1 - l) & 1];
-    if ((rc = block_backward(st, bi, w.plan, w, layers[l], grads[l], xin, *a, gcur, gout, s))) return rc;
+    // block l's dx is block l - 1's dy: its column sums (block l - 1's db_2)
+    // come out of block l's last LayerNorm backward
+    float* below_b2 = l > 0 ? grads[l - 1].b_2 : nullptr;
+    const bool b2_done = l < N - 1 && grads[l].b_2 != nullptr;
+    if ((rc = block_backward(st, bi, w.plan, w, layers[l], grads[l], xin, *a, gcur, gout, s, below_b2, b2_done)))
+      return rc;
     gcur = gout;
   }
   return FL_OK;

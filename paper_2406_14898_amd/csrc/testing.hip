@@ -95,6 +95,25 @@ int fl_test_layernorm_bwd(int dtype, const void* dy, const void* x, const float*
   return herr(layernorm_bwd_dx((DType)dtype, dy, x, mean, rstd, g, dres, dx, T, H, (hipStream_t)stream));
 }
 
+int fl_test_layernorm_bwd_fused(int dtype, const void* dy, const void* x, const float* mean, const float* rstd,
+                                const void* g, const void* dres, void* dx, int T, int H, float* dgamma, float* dbeta,
+                                float* dsum, float* partial, void* stream) {
+  if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
+  if (!dy || !x || !mean || !rstd || !g || !dx) return set_error(FL_ERR_NULL, "NULL argument");
+  if ((dgamma == nullptr) != (dbeta == nullptr)) return set_error(FL_ERR_ARG, "dgamma and dbeta: both or neither");
+  if ((dgamma || dsum) && !partial) return set_error(FL_ERR_NULL, "NULL partial");
+  if (T < 0 || H < 256 || H % 256 || H > 4096) return set_error(FL_ERR_ARG, "bad T / H");
+  hipStream_t s = (hipStream_t)stream;
+  float* pg = dgamma ? partial : nullptr;
+  float* pb = dgamma ? partial + (size_t)kLnBlocks * H : nullptr;
+  float* po = dsum ? partial + (size_t)2 * kLnBlocks * H : nullptr;
+  int rc = herr(layernorm_bwd_fused((DType)dtype, dy, x, mean, rstd, g, dres, dx, T, H, pg, pb, po, s));
+  if (!rc && dgamma) rc = herr(colsum_finish(pg, kLnBlocks, H, dgamma, s));
+  if (!rc && dgamma) rc = herr(colsum_finish(pb, kLnBlocks, H, dbeta, s));
+  if (!rc && dsum) rc = herr(colsum_finish(po, kLnBlocks, H, dsum, s));
+  return rc;
+}
+
 int fl_test_colsum(int dtype, int mode, const void* X, const void* Y, const float* mean, const float* rstd, int T,
                    int N, float* out, float* out2, float* partial, void* stream) {
   if (!dtype_ok(dtype) || (mode != 0 && mode != 1)) return set_error(FL_ERR_ARG, "bad dtype / mode");

@@ -42,7 +42,8 @@ EXPORTS = (
     "fl_client_create", "fl_client_destroy", "fl_client_workspace_bytes", "fl_embedding_forward",
     "fl_embedding_backward", "fl_lm_head_forward", "fl_lm_head_backward",
     "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
-    "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_colsum",
+    "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_layernorm_bwd_fused",
+    "fl_test_colsum",
     "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
 )
 
@@ -126,6 +127,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_test_layernorm_fwd": [ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                   vp],
         "fl_test_layernorm_bwd": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int, vp],
+        "fl_test_layernorm_bwd_fused": [ctypes.c_int] + [vp] * 7 + [ctypes.c_int, ctypes.c_int] + [vp] * 5,
         "fl_test_colsum": [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp],
         "fl_test_rope": [ctypes.c_int, vp, vp] + [ctypes.c_int] * 6 + [ctypes.c_float, vp, vp, vp, vp],
         "fl_test_attention_fwd": [ctypes.c_int, vp, vp, vp, vp, vp] + [ctypes.c_int] * 5 + [vp, vp, ctypes.c_int, vp],
@@ -404,6 +406,13 @@ def fl_test_layernorm_fwd(dtype, x, g, b, y, mean, rstd, T, H, eps, stream=None)
 def fl_test_layernorm_bwd(dtype, dy, x, mean, rstd, g, dres, dx, T, H, stream=None) -> None:
     _check(load().fl_test_layernorm_bwd(dtype, _ptr(dy), _ptr(x), _ptr(mean), _ptr(rstd), _ptr(g), _ptr(dres),
                                         _ptr(dx), T, H, _stream(stream)))
+
+
+def fl_test_layernorm_bwd_fused(dtype, dy, x, mean, rstd, g, dres, dx, T, H, dgamma=None, dbeta=None, dsum=None,
+                                partial=None, stream=None) -> None:
+    _check(load().fl_test_layernorm_bwd_fused(dtype, _ptr(dy), _ptr(x), _ptr(mean), _ptr(rstd), _ptr(g), _ptr(dres),
+                                              _ptr(dx), T, H, _ptr(dgamma), _ptr(dbeta), _ptr(dsum), _ptr(partial),
+                                              _stream(stream)))
 
 
 def fl_test_colsum(dtype, mode, X, Y, mean, rstd, T, N, out, out2, partial, stream=None) -> None:

@@ -228,6 +228,49 @@ def test_layernorm_fwd_bwd(dt, H):
 
 
 @pytest.mark.parametrize("dt", DT)
+@pytest.mark.parametrize("H,T", [(256, 3), (768, 513), (4096, 2011)])
+@pytest.mark.parametrize("with_res", [True, False])
+def test_layernorm_bwd_fused(dt, H, T, with_res):
+    """The stack's LayerNorm backward with its column sums in the same pass:
+    dx (with and without the residual term), the gain and shift gradients and
+    the column sums of dx, against the oracle's LayerNorm backward.  T = 3
+    leaves most of the 512 row blocks empty; T = 2011 splits unevenly."""
+    code, tdt = DTYPES[dt]
+    x = rnd((T, H), 31, 2.0, dt=dt) + np.float32(0.5)
+    x = synth.bf16_round(x) if dt == "bf16" else x
+    g = rnd((H,), 32, 0.1, dt=dt) + np.float32(1.0)
+    g = synth.bf16_round(g) if dt == "bf16" else g
+    b = rnd((H,), 33, 0.1, dt=dt)
+    _, xhat, rstd = oracle.layer_norm(x.astype(np.float64), g, b, 1e-5)
+    dx_, dg_ = dev(x, dt), dev(g, dt)
+    mean = torch.from_numpy(x.astype(np.float64).mean(1).astype(np.float32)).cuda()
+    rs = torch.from_numpy(rstd[:, 0].astype(np.float32)).cuda()
+    dy = rnd((T, H), 34, dt=dt)
+    dres = rnd((T, H), 35, dt=dt) if with_res else np.zeros((T, H), np.float32)
+    dxr, dgr, dbr = oracle.layer_norm_backward(dy.astype(np.float64), xhat, rstd, g.astype(np.float64))
+    out = torch.full((T, H), float("nan"), dtype=tdt, device="cuda")
+    og = torch.zeros(H, dtype=torch.float32, device="cuda")
+    ob = torch.ones(H, dtype=torch.float32, device="cuda")
+    osum = torch.full((H,), 2.0, dtype=torch.float32, device="cuda")
+    part = torch.full((3 * 512 * H,), float("nan"), dtype=torch.float32, device="cuda")
+    F.fl_test_layernorm_bwd_fused(code, dev(dy, dt), dx_, mean, rs, dg_, dev(dres, dt) if with_res else None, out,
+                                  T, H, og, ob, osum, part)
+    sync()
+    got = host(out)
+    assert rel_l2(got, dxr + dres) < TOL[dt] / 4
+    assert rel_l2(host(og), dgr) < 1e-4
+    assert rel_l2(host(ob), dbr + 1.0) < 1e-5
+    # the sum of what was stored (rounded), added in fp32
+    assert rel_l2(host(osum), got.sum(0) + 2.0) < 1e-5
+    # dx only: no sums asked for, no scratch needed
+    out2 = torch.full((T, H), float("nan"), dtype=tdt, device="cuda")
+    F.fl_test_layernorm_bwd_fused(code, dev(dy, dt), dx_, mean, rs, dg_, dev(dres, dt) if with_res else None, out2,
+                                  T, H)
+    sync()
+    assert torch.equal(out2, out)
+
+
+@pytest.mark.parametrize("dt", DT)
 def test_colsum_many_blocks(dt):
     code, _ = DTYPES[dt]
     T, N = 1000, 1536

@@ -305,9 +305,13 @@ def test_launch_profile_accounts_every_launch():
     N = SHAPE.num_layers
     per_block = {"layernorm_fwd": 2, "gemm_nt_bias": 1, "rope_qk": 1, "attn_fwd": 1, "gemm_nt_bias_res": 2,
                  "gemm_nt_bias_gelu": 1, "gemm_tn_acc": 4, "gemm_nn_gelu_bwd": 1, "gemm_nn": 3,
-                 "layernorm_bwd": 2, "colsum": 6, "attn_bwd": 1}
+                 "layernorm_bwd": 2, "attn_bwd": 1}
     want = {k: v * N for k, v in per_block.items()}
     want["plan"] = 2
+    # column-sum launches: db_1's finish, db_qkv, and the two LayerNorm
+    # backward finishes (gain / shift, plus db_o and the block below's db_2);
+    # the top block also sums its own dy for db_2
+    want["colsum"] = 4 * N + 1
     assert {k: r["launches"] for k, r in prof.items()} == want
     assert all(r["ms"] > 0 for r in prof.values())
     w = synth.WORKLOADS["tiny_2blk_fp32"]
