@@ -69,6 +69,9 @@ template <> struct Vec8<bf16> {
   __device__ __forceinline__ void load(const bf16* p) { r = ld16(p); }
   __device__ __forceinline__ void store(bf16* p) const { st16(p, r); }
   __device__ __forceinline__ void zero() { r = u32x4{0, 0, 0, 0}; }
+  // Opaque redefinition: values converted from the vector before this point
+  // are not reused after it (the compiler re-reads the packed registers).
+  __device__ __forceinline__ void settle() { asm volatile("" : "+v"(r)); }
   __device__ __forceinline__ float get(int i) const {
     uint32_t w = r[i >> 1];
     return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
@@ -85,6 +88,7 @@ template <> struct Vec8<float> {
   __device__ __forceinline__ void load(const float* p) { r0 = ld16(p); r1 = ld16(p + 4); }
   __device__ __forceinline__ void store(float* p) const { st16(p, r0); st16(p + 4, r1); }
   __device__ __forceinline__ void zero() { r0 = u32x4{0, 0, 0, 0}; r1 = r0; }
+  __device__ __forceinline__ void settle() { asm volatile("" : "+v"(r0), "+v"(r1)); }
   __device__ __forceinline__ float get(int i) const { return __uint_as_float(i < 4 ? r0[i & 3] : r1[i & 3]); }
   __device__ __forceinline__ f32x8 frag() const {
     f32x4 a = __builtin_bit_cast(f32x4, r0), b = __builtin_bit_cast(f32x4, r1);

@@ -181,90 +181,6 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, con
   if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
 }
 
-// The stack's LayerNorm forward: workgroup b of kLnBlocks takes an even
-// share of the rows across all H columns, wave w columns [512 w, 512 w + 512)
-// (eight per lane, the gain and shift loaded once into registers), rows four
-// at a time; the row sums and then the sums of squared deviations are
-// combined over the waves through LDS in wave order (two-pass statistics,
-// as in ln_fwd_kernel).  Each row read is one contiguous 1 KB segment per
-// wave, and the grid is one balanced round.
-template <typename T>
-__global__ void __launch_bounds__(512) ln_fwd_rows_kernel(const T* x, const T* g, const T* b, T* y, float* mean,
-                                                          float* rstd, int T_, int H, float eps) {
-  __shared__ float red[2][4][8];  // [phase][row][wave]
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int col = w * 512 + lane * 8;
-  const bool on = col < H;
-  const int nw = (H + 511) / 512;
-  const int r0 = (int)((long)T_ * blockIdx.x / kLnBlocks), r1 = (int)((long)T_ * (blockIdx.x + 1) / kLnBlocks);
-  float gv[8], bv[8];
-  {
-    Vec8<T> gg, bb;
-    if (on) { gg.load(g + col); bb.load(b + col); } else { gg.zero(); bb.zero(); }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) { gv[e] = gg.get(e); bv[e] = bb.get(e); }
-  }
-  const float invH = 1.f / (float)H;
-  for (int rb = r0; rb < r1; rb += 4) {
-    Vec8<T> xv[4];
-    float s[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (on && rb + u < r1) xv[u].load(x + (long)(rb + u) * H + col); else xv[u].zero();
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float t = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) t += xv[u].get(e);
-      s[u] = wave_sum(t);
-    }
-    if (lane == 0) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) red[0][u][w] = s[u];
-    }
-    __syncthreads();
-    float mu[4], ss[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float t = 0.f;
-      for (int v = 0; v < nw; ++v) t += red[0][u][v];
-      mu[u] = t * invH;
-      float q = 0.f;
-      if (on) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) { const float d = xv[u].get(e) - mu[u]; q += d * d; }
-      }
-      ss[u] = wave_sum(q);
-    }
-    if (lane == 0) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) red[1][u][w] = ss[u];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float t = 0.f;
-      for (int v = 0; v < nw; ++v) t += red[1][u][v];
-      const float rs = 1.0f / sqrtf(t * invH + eps);
-      const int r = rb + u;
-      if (r < r1) {
-        if (on) {
-          float out[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) out[e] = (xv[u].get(e) - mu[u]) * rs * gv[e] + bv[e];
-          Vec8<T> o;
-          o.set(out);
-          o.store(y + (long)r * H + col);
-        }
-        if (threadIdx.x == 0) { mean[r] = mu[u]; rstd[r] = rs; }
-      }
-    }
-    // red[0] is rewritten by the next batch only after its every wave has
-    // passed this batch's second barrier, red[1] after its first
-  }
-}
-
 template <typename T, int MAXC>
 __global__ void __launch_bounds__(256) ln_bwd_dx_kernel(const T* dy, const T* x, const float* mean,
                                                         const float* rstd, const T* g, const T* dres, T* dx, int T_,
@@ -359,19 +275,6 @@ hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, 
                        : ln_fwd_t<float>(x, g, b, y, mean, rstd, T_, H, eps, st);
 }
 
-hipError_t layernorm_fwd_rows(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
-                              float* rstd, int T_, int H, float eps, hipStream_t st) {
-  if (T_ <= 0) return hipSuccess;
-  if (H > 4096 || H % 8 != 0) return hipErrorInvalidValue;
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL((ln_fwd_rows_kernel<bf16>), dim3(kLnBlocks), dim3(512), 0, st, (const bf16*)x, (const bf16*)g,
-                       (const bf16*)b, (bf16*)y, mean, rstd, T_, H, eps);
-  else
-    hipLaunchKernelGGL((ln_fwd_rows_kernel<float>), dim3(kLnBlocks), dim3(512), 0, st, (const float*)x,
-                       (const float*)g, (const float*)b, (float*)y, mean, rstd, T_, H, eps);
-  return hipGetLastError();
-}
-
 hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
                             const void* g, const void* dres, void* dx, int T_, int H, hipStream_t st) {
   if (T_ <= 0) return hipSuccess;
@@ -447,6 +350,10 @@ __global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T*
       for (int u = 0; u < 4; ++u) { red[par][u][w][0] = s1[u]; red[par][u][w][1] = s2[u]; }
     }
     __syncthreads();  // one barrier per batch: the other parity's slots are free again
+    // the packed rows are re-read from here on (the values converted before
+    // the barrier are not kept live across it: 128 registers instead of 188)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) { a[u].settle(); xx[u].settle(); }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       float t1 = 0.f, t2 = 0.f;

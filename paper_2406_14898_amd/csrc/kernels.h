@@ -79,10 +79,6 @@ hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float
 // LayerNorm forward: y = (x - mean) * rstd * g + b, saving mean and rstd.
 hipError_t layernorm_fwd(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
                          float* rstd, int T, int H, float eps, hipStream_t st);
-// The kernel layernorm_fwd runs for H <= 4096: one workgroup per even share of
-// the rows (kLnBlocks of them).
-hipError_t layernorm_fwd_rows(DType dt, const void* x, const void* g, const void* b, void* y, float* mean,
-                              float* rstd, int T, int H, float eps, hipStream_t st);
 // LayerNorm backward (input grad only): dx = dres + rstd*(dxh - mean(dxh) - xh*mean(dxh*xh)),
 // dxh = dy * g, xh = (x - mean) * rstd.  dres may alias nothing written here.
 hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float* mean, const float* rstd,
