@@ -168,7 +168,7 @@ __device__ __forceinline__ void wg_barrier() {
 // (wave tile rows 128 (wave & 1) + 16 j, columns 64 (wave >> 1) + 16 i), with
 // the LDS at stg (at least 128 KB, free: every wave is past its operand
 // reads) as staging.
-template <int EPI>
+template <int EPI, int BATCH>
 __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc)[kWTN][kWTM], float* stg, int tm,
                                               int m0, int n0, int tid) {
   asm volatile("" : "+v"(tid));  // keeps the epilogue's per-lane values out of the main loop's live range
@@ -213,7 +213,7 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
     barrier();
     // Rows wave + 8 q, in batches whose global loads (residual, GeLU input,
     // fp32 accumulator) are issued together before their first use.
-    constexpr int kBatch = EPI == EPI_ACC_F32 ? 4 : 8;
+    constexpr int kBatch = BATCH;
 #pragma unroll
     for (int q0 = 0; q0 < kRows; q0 += kBatch) {
       Vec4<bf16> ext[kBatch];
@@ -291,7 +291,14 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
   }
 }
 
-template <bool AK, bool BKc, int EPI>
+// Rows of the epilogue whose global reads are issued together: 16 for the
+// residual epilogues (a half's whole share: 6 % faster on the 41447 x 4096 x
+// 4096 output projection than 8), 8 elsewhere (16 measured no faster), 4 for
+// the fp32 accumulator.
+template <int EPI>
+constexpr int epi_batch() { return (EPI == EPI_BIAS_RES || EPI == EPI_RES) ? 16 : EPI == EPI_ACC_F32 ? 4 : 8; }
+
+template <bool AK, bool BKc, int EPI, int BATCH = epi_batch<EPI>()>
 __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kTileElems];  // [stage][A/B]
 
@@ -492,7 +499,7 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
 
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   barrier();  // every wave is done with the operand tiles
-  tile_epilogue<EPI>(p, acc, reinterpret_cast<float*>(&smem[0][0][0]), tm, m0, n0, tid);
+  tile_epilogue<EPI, BATCH>(p, acc, reinterpret_cast<float*>(&smem[0][0][0]), tm, m0, n0, tid);
   }
 }
 
