@@ -50,8 +50,12 @@ __device__ __forceinline__ SeqB seqb(const int32_t* cu, const int32_t* prefix, i
   si.P = prefix ? prefix[s] : 0;
   return si;
 }
-// Branch-free (bitwise) so that masking stays a select per element.
-__device__ __forceinline__ bool vis(int i, int j, int L, int P) { return (j < L) & ((j <= i) | (j < P)); }
+// Query i of a sequence of L rows whose first P rows are its context sees
+// keys j < L with j <= i or j < P: exactly the keys j < vis_end(i, L, P).
+__device__ __forceinline__ int vis_end(int i, int L, int P) { return min(L, max(i + 1, P)); }
+// Key j < L is seen by the queries i >= vis_start(j, P) (all of them when j
+// is a context key); a key past the sequence end by none.
+__device__ __forceinline__ int vis_start(int j, int L, int P) { return j >= L ? (1 << 30) : (j < P ? 0 : j); }
 
 template <int D>
 __device__ __forceinline__ int swz(int row) {
@@ -291,14 +295,12 @@ __global__ void __launch_bounds__(256, 2) fwd_kernel(AttnDesc a) {
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
       if (!full) {
-        const int qi = qlo + 16 * qs + fr;
+        // key j0 + 16 at + 4 fg + i is visible iff 16 at + i < rel
+        const int rel = (pre ? px.n : vis_end(qlo + 16 * qs + fr, si.L, si.P)) - j0 - 4 * fg;
 #pragma unroll
         for (int at = 0; at < 4; ++at)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            st[qs][at][i] = (pre ? j0 + 16 * at + 4 * fg + i < px.n : vis(qi, j0 + 16 * at + 4 * fg + i, si.L, si.P))
-                                ? st[qs][at][i]
-                                : -INFINITY;
+          for (int i = 0; i < 4; ++i) st[qs][at][i] = 16 * at + i < rel ? st[qs][at][i] : -INFINITY;
       }
       float mx = st[qs][0][0];
 #pragma unroll
@@ -479,11 +481,19 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            float pr = ex2(fmaf(st[qs][u][i], sl2, -lse2[qs]));
-            const int j = j0 + 16 * (2 * c2 + u) + 4 * fg + i;
-            pr = (full | (pre ? j < px.n : vis(qi, j, si.L, si.P))) ? pr : 0.f;
+            const float pr = ex2(fmaf(st[qs][u][i], sl2, -lse2[qs]));
             st[qs][u][i] = pr * (dp[qs][u][i] - dlt[qs]);
           }
+        // masking only where the tile straddles the diagonal, the prefix end
+        // or the sequence end (a wave-uniform test: full tiles skip it)
+        if (!full) {
+          // key j0 + 32 c2 + 16 u + 4 fg + i is visible iff 16 u + i < rel
+          const int rel = (pre ? px.n : vis_end(qi, si.L, si.P)) - j0 - 32 * c2 - 4 * fg;
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) st[qs][u][i] = 16 * u + i < rel ? st[qs][u][i] : 0.f;
+        }
         df[qs] = pack_p(st[qs][0], st[qs][1]);
       }
 #pragma unroll
@@ -578,6 +588,7 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   const int klo = k0 + 16 * w;  // this wave's keys: klo + fr (prefix rows for a prefix tile)
   const int kj = klo + fr;
   const bool kvalid = kj < (pre ? a.num_prefix : si.L);
+  const int kstart = pre ? 0 : vis_start(kj, si.L, si.P);
   // key / value rows of this lane: the prefix buffers (row stride H) or qkv
   const bf16* krow = pre ? static_cast<const bf16*>(a.pk) + (long)kj * H + h * D
                          : qkv + (long)(si.r0 + kj) * ld + H + h * D;
@@ -630,10 +641,16 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
       // rows qb + 16 q + 4 g + i of this lane's column kj
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float pv = ex2(fmaf(st[q][i], sl2, -lq[q & 1][i] * kLog2e));
-        pv = (full | vis(qb + 16 * q + 4 * fg + i, kj, si.L, si.P)) ? pv : 0.f;
+        const float pv = ex2(fmaf(st[q][i], sl2, -lq[q & 1][i] * kLog2e));
         pr[q][i] = pv;
         dsv[q][i] = pv * (dp[q][i] - dq[q & 1][i]);
+      }
+      if (!full) {  // diagonal or ragged tiles only (wave-uniform)
+        // query qb + 16 q + 4 fg + i sees this lane's key iff 16 q + i >= rel
+        const int rel = kstart - qb - 4 * fg;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (16 * q + i < rel) { pr[q][i] = 0.f; dsv[q][i] = 0.f; }
       }
       if (q & 1) {
         pf[q >> 1] = pack_p(pr[q - 1], pr[q]);
