@@ -158,7 +158,12 @@ int fl_stack_destroy(fl_stack* stack);
  * block's forward from its input). */
 int fl_stack_saved_bytes(const fl_stack* stack, const fl_batch_desc* batch, int recompute, size_t* bytes);
 /* Bytes of device workspace needed by forward / backward / pack calls for
- * this batch (one size serves all of them). */
+ * this batch (one size serves all of them).  In bf16 it includes room for
+ * the backward's attention softmax gradient dS (Appendix A form of the
+ * attention), stored once and read by the dq pass: one 64 x 64 bf16 tile per
+ * head and per pair of 64-row query / key tiles with a visible pair, when
+ * that totals at most 8 GiB (beyond, dq recomputes it and nothing is
+ * stored). */
 int fl_stack_workspace_bytes(const fl_stack* stack, const fl_batch_desc* batch, int recompute, size_t* bytes);
 
 /* Forward through the N server blocks (Section 3.1, h_{N-2} =

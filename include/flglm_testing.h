@@ -87,12 +87,18 @@ int fl_test_attention_fwd(int dtype, const void* qkv, void* o, float* lse, const
  * rotary_dim 0 disables the inverse rotation, otherwise pos/cos/sin come
  * from fl_test_rope's scratch.  With a prefix, dprefix_part receives the
  * per-sequence prefix gradients, fp32 [2][S][num_prefix][H] (keys, then
- * values). */
+ * values).  ds_work (device, ds_bytes >= fl_test_attention_ds_bytes) holds
+ * the stored softmax gradient of the bf16 kernels, which dq then reads; NULL:
+ * dq recomputes it. */
 int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float* lse, const void* dout, void* dqkv,
                           float* delta, const int32_t* cu_dev, const int32_t* prefix_dev, const int32_t* pos,
                           const float* cos_t, const float* sin_t, int rotary_dim, int T, int S, int max_seqlen, int H,
                           int num_heads, const void* pk, const void* pv, int num_prefix, float* dprefix_part,
-                          void* stream);
+                          void* ds_work, size_t ds_bytes, void* stream);
+/* Bytes of ds_work for fl_test_attention_bwd over these host sequence bounds
+ * (cu_host [S+1], prefix_host [S] or NULL). */
+int fl_test_attention_ds_bytes(const int32_t* cu_host, const int32_t* prefix_host, int S, int num_heads,
+                               int num_prefix, size_t* bytes);
 
 #ifdef __cplusplus
 }

@@ -198,6 +198,26 @@ __device__ __forceinline__ bool tile_full(int j0, int qlo, int L, int P) {
   return j0 + kRows <= L && (j0 + kRows - 1 <= qlo || j0 + kRows <= P);
 }
 
+// Stored softmax gradient (dS, bf16) of the backward, in 64 x 64 tiles, one
+// per (query tile, key tile) pair that holds a visible pair: query tile qt of
+// a sequence meets the ntp prefix key tiles and the sequence's key tiles
+// kt < max(qt + 1, np), np = ceil(P / 64) (the context keys every query
+// sees).  Tiles of a sequence and head are numbered row by row: query tile
+// qt starts at ds_row_off(qt) and its key tiles follow in order, prefix
+// first.  A tile holds dS^T in the order the dk/dv kernel's lanes hold it:
+// 16-byte chunk c = (2 w + p) 64 + 16 g + r holds, for key 16 w + r, the
+// queries 32 p + 4 g + e (e < 4) and 32 p + 16 + 4 g + e - 4 (e >= 4), so
+// every store is a whole 1 KB block; keys 32 c2 .. + 31 are the contiguous
+// half c2.
+__host__ __device__ __forceinline__ long ds_row_off(int qt, int ntp, int np) {
+  if (qt <= np) return (long)qt * (ntp + np);
+  return (long)np * (ntp + np) + (long)(qt - np) * ntp + ((long)qt * (qt + 1) - (long)np * (np + 1)) / 2;
+}
+__host__ __device__ __forceinline__ long ds_seq_tiles(int L, int P, int ntp) {
+  return ds_row_off((L + kRows - 1) / kRows, ntp, (P + kRows - 1) / kRows);
+}
+constexpr long kDsTileElems = (long)kRows * kRows;
+
 // ---------------------------------------------------------------------------
 // Forward: 128 queries per workgroup (4 waves x 32), key tiles of 64.
 // ---------------------------------------------------------------------------
@@ -535,7 +555,8 @@ __global__ void __launch_bounds__(256, 2) dq_kernel(AttnDesc a) {
 // as zero (and their LSE and delta as zero), which makes their dS and their
 // dO rows zero: they add nothing, so again only diagonal tiles are masked.
 // ---------------------------------------------------------------------------
-template <int D>
+// DS: also store dS^T (the tiles dq_ds_kernel reads; see ds_row_off).
+template <int D, bool DS>
 __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   constexpr int NC = D / 32, ND = D / 16, BK = 64;
   __shared__ __attribute__((aligned(1024))) bf16 Qs[2][kRows * D];
@@ -605,16 +626,44 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   f32x4 dk[ND], dv[ND];
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) { dk[dt] = f32x4{0.f, 0.f, 0.f, 0.f}; dv[dt] = dk[dt]; }
+  // stored dS^T: this lane's chunks of the tile of query tile qt (tile
+  // column u of its tile row)
+  bf16* ds_seq = nullptr;
+  int ds_np = 0;
+  if constexpr (DS) {
+    ds_np = (si.P + kRows - 1) / kRows;
+    ds_seq = static_cast<bf16*>(a.ds) + (a.ds_off[s] + (long)h * ds_seq_tiles(si.L, si.P, ntp)) * kDsTileElems +
+             (2 * w * 64 + lane) * 8;
+  }
+  // two 1 KB stores per wave and query tile (chunk pairs p = 0, 1), the same
+  // number on every step
+  auto ds_store = [&](int qt, int p, u32x4 v) {
+    // streamed (non-temporal): dS is read once, by the dq kernel, and must not
+    // evict the Q / dO tiles the other workgroups of this head re-read
+    __builtin_nontemporal_store(
+        v, reinterpret_cast<u32x4*>(ds_seq + (ds_row_off(qt, ntp, ds_np) + u) * kDsTileElems + p * 64 * 8));
+  };
 
   auto step = [&](auto slot, int qt) {
     constexpr int SL = decltype(slot)::value;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // The next tile's DMA was issued before this wave's dS stores of the
+    // previous step (two): waiting for all but those two is enough.
+    if (DS && qt != qstart)
+      asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     bar();
     if (qt + 1 < nqt) issue(qt + 1);
     const int qb = qt * kRows;
     // queries [qb, qb + 64) against keys [klo, klo + 16); prefix keys are
     // visible to all
-    if (!pre && qb + kRows - 1 < klo && klo >= si.P) return;
+    if (!pre && qb + kRows - 1 < klo && klo >= si.P) {
+      if constexpr (DS) {
+        ds_store(qt, 0, u32x4{0u, 0u, 0u, 0u});
+        ds_store(qt, 1, u32x4{0u, 0u, 0u, 0u});
+      }
+      return;
+    }
     const bool full = pre || qb >= klo + 15 || klo + 15 < si.P;
     const bf16* qs_ = Qs[SL];
     const bf16* os_ = Os[SL];
@@ -655,6 +704,8 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
       if (q & 1) {
         pf[q >> 1] = pack_p(pr[q - 1], pr[q]);
         df[q >> 1] = pack_p(dsv[q - 1], dsv[q]);
+        if constexpr (DS)  // a key past the sequence end stores zeros (its dS is not masked)
+          ds_store(qt, q >> 1, kvalid ? __builtin_bit_cast(u32x4, df[q >> 1]) : u32x4{0u, 0u, 0u, 0u});
       }
     };
     bf16x8 fq[3], fo[3];
@@ -726,6 +777,173 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward, dq from the stored dS: dq = scale sum_k dS[q][k] K[k] (no
+// recomputation of S and dP).  256 queries per workgroup, one 64-row query
+// tile per wave, key tiles in halves of 32 through three LDS stages: per
+// stage, the half K tile and the matching halves of the four dS^T tiles of
+// the workgroup's query tiles come in by DMA (a tile that does not exist,
+// i.e. holds no visible pair, reads as zero), and both operands are read
+// with transpose reads.  The workgroup walks the key tiles its last query
+// tile sees; a wave whose own query tile does not see a key tile skips it.
+// ---------------------------------------------------------------------------
+// dS^T chunk c of a tile sits at LDS chunk c ^ (4 ((c >> 4) & 3)): the
+// transpose reads (16 lanes: 4 keys x 4 query groups) then hit 16 distinct
+// bank groups.
+__device__ __forceinline__ int ds_swz(int c) { return c ^ (((c >> 4) & 3) << 2); }
+
+template <int D>
+__global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
+  constexpr int ND = D / 16, QS = 4, BM = 256, NS = 3, HR = 32;  // stages, rows per half tile
+  constexpr int KCH = D / 8;                                      // 16-byte chunks per K row
+  constexpr int KDMA = HR * KCH / 64 / 4;                         // K DMA instructions per wave per stage
+  constexpr int DMA = KDMA + 4;                                   // + one per dS half tile
+  constexpr int HALF = HR * kRows;                                // elements of a dS half tile
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[NS][HR * D];
+  __shared__ __attribute__((aligned(1024))) bf16 Ss[NS][4][HALF];
+
+  const WgCoord wc = wg_coord((a.max_seqlen + BM - 1) / BM, a.num_heads);
+  if (wc.s >= a.num_seqs) return;
+  const int s = wc.s, h = wc.h, q0 = wc.tile * BM;
+  const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
+  if (q0 >= si.L) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+  const long ld = a.ld_qkv;
+  const int H = a.hidden;
+  FragBase<D> fb;
+  fb.init(fr, fg);
+  // dS fragment of query group qs: keys 4 fg + (s / 4) (+ 16) of the half,
+  // queries 16 qs + 4 (s % 4) .. + 3, s = fr; byte offset of the first read
+  // for qs = 0 (+ 1 KB per query pair, + 8 bytes for an odd group, + 2 KB
+  // for the second read)
+  const int t4 = fr & 3;
+  const uint32_t ds_rd = (uint32_t)((t4 * 16 + ((4 * fg + (fr >> 2)) ^ (4 * t4))) * 16);
+
+  const bf16* kbase = qkv + (long)si.r0 * ld + H + h * D;
+  const PrefixKV px(a, h, D);
+  const int ntp = px.ntiles, np = (si.P + kRows - 1) / kRows, nt = (si.L + kRows - 1) / kRows;
+  const int qt0 = q0 / kRows, qlast = min(qt0 + 3, nt - 1);
+  const int nkt = ntp + max(qlast + 1, np);  // key tiles of the last query tile
+  const int nst = 2 * nkt;                   // stages: (key tile, half)
+  const int qt = qt0 + w;                    // this wave's query tile
+  const int my_nkt = qt < nt ? ntp + max(qt + 1, np) : 0;
+  const bf16* ds_seq =
+      static_cast<const bf16*>(a.ds) + (a.ds_off[s] + (long)h * ds_seq_tiles(si.L, si.P, ntp)) * kDsTileElems;
+  const uint32_t lds_k = FL_LDS_ADDR(&Ks[0][0]), lds_s = FL_LDS_ADDR(&Ss[0][0][0]);
+  // per-lane source offsets: K rows (as dma_tile), dS chunk of this lane
+  const uint32_t ds_src = (uint32_t)(ds_swz(w * 64 + lane) * 16);
+  auto issue = [&](int g) {
+    const int kc = g >> 1, c2 = g & 1, slot = g % NS;
+    const uint32_t sk = lds_k + slot * (HR * D * 2);
+    // a half past the sequence end (row0 >= L) gets no records: reads zero
+    const int row0 = (kc - ntp) * kRows + HR * c2;
+    i32x4 rk = kc < ntp ? px.rk
+                        : buf_rsrc(kbase + (long)row0 * ld, (uint32_t)((long)max(0, min(si.L - row0, HR)) * ld * 2));
+    rk = i32x4{__builtin_amdgcn_readfirstlane(rk[0]), __builtin_amdgcn_readfirstlane(rk[1]),
+               __builtin_amdgcn_readfirstlane(rk[2]), __builtin_amdgcn_readfirstlane(rk[3])};
+    const int r0 = kc < ntp ? kc * kRows + HR * c2 : 0;
+    const long ldk = kc < ntp ? H : ld;
+#pragma unroll
+    for (int i = 0; i < KDMA; ++i) {
+      const int inst = i * 4 + w;
+      const int row = inst * (64 / KCH) + lane / KCH;
+      const int q = (lane % KCH) ^ swz<D>(row);
+      dma_lds<16>(rk, sk + inst * 1024, (uint32_t)((long)(r0 + row) * ldk + q * 8) * 2u);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int q = qt0 + t;
+      const bool has = q < nt && kc < ntp + max(q + 1, np);
+      const bf16* src = ds_seq + (has ? (ds_row_off(q, ntp, np) + kc) * kDsTileElems + c2 * HALF : 0);
+      dma_lds<16>(buf_rsrc(src, has ? (uint32_t)(HALF * 2) : 0u),
+                  lds_s + (slot * 4 + t) * (uint32_t)(HALF * 2) + w * 1024, ds_src);
+    }
+  };
+  issue(0);
+  if (nst > 1) issue(1);
+
+  f32x4 acc[ND][QS];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int g = 0; g < nst; ++g) {
+    // stage g landed (stage g + 1, if issued, may still be in flight)
+    if (g + 1 < nst)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(DMA) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    bar();  // and every wave is past stage g - 1, whose slot stage g + 2 takes
+    if (g + 2 < nst) issue(g + 2);
+    if ((g >> 1) >= my_nkt) continue;
+    const int slot = g % NS;
+    const bf16* ks = Ks[slot];
+    const char* ss = reinterpret_cast<const char*>(Ss[slot][w]);
+    bf16x8 df[QS];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      const char* p = ss + ds_rd + (qs >> 1) * 1024 + (qs & 1) * 8;
+      i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p));
+      i16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 2048));
+      df[qs] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      const bf16x8 kt_ = rd_tr<D>(ks + fb.tr[dt]);
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = mma16(kt_, df[qs], acc[dt][qs]);
+    }
+  }
+
+  const float sc = 1.f / sqrtf((float)D);
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    const int qi = qt * kRows + 16 * qs + fr;
+    if (qi >= si.L) continue;
+    f32x4 g[ND];
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) g[dt] = acc[dt][qs] * sc;
+    rope_back<D>(g, qi, a.rotary_dim, fg, a.cos_t, a.sin_t);
+    bf16* dq = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + qi) * a.ld_dqkv + h * D;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      const float v[4] = {g[dt][0], g[dt][1], g[dt][2], g[dt][3]};
+      Vec4<bf16> ov;
+      ov.set(v);
+      ov.store(dq + 16 * dt + 4 * fg);
+    }
+  }
+}
+
+// Tile offsets of the stored dS: off[s] = sum over sequences before s of
+// num_heads * ds_seq_tiles, off[S] = the total (one workgroup, chunked scan).
+__global__ void __launch_bounds__(256) ds_offsets_kernel(const int32_t* cu, const int32_t* prefix, int S, int nh,
+                                                         int ntp, int64_t* off) {
+  __shared__ long sh[256];
+  const int t = threadIdx.x;
+  long carry = 0;
+  for (int s0 = 0; s0 < S; s0 += 256) {
+    const int s = s0 + t;
+    long v = 0;
+    if (s < S) v = (long)nh * ds_seq_tiles(cu[s + 1] - cu[s], prefix ? prefix[s] : 0, ntp);
+    sh[t] = v;
+    __syncthreads();
+    for (int o = 1; o < 256; o <<= 1) {
+      const long x = t >= o ? sh[t - o] : 0;
+      __syncthreads();
+      sh[t] += x;
+      __syncthreads();
+    }
+    if (s < S) off[s] = carry + sh[t] - v;
+    carry += sh[255];
+    __syncthreads();
+  }
+  if (t == 0) off[S] = carry;
+}
+
 template <int D>
 hipError_t fwd_launch(const AttnDesc& a, hipStream_t st) {
   const dim3 grid = wg_grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
@@ -738,7 +956,16 @@ hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
   hipError_t e = attn_delta(DT_BF16, a, st);
   if (e != hipSuccess) return e;
   const dim3 gkv = wg_grid((a.num_prefix + 63) / 64 + (a.max_seqlen + 63) / 64, a.num_heads, a.num_seqs);
-  hipLaunchKernelGGL((dkdv_kernel<D>), gkv, dim3(256), 0, st, a);
+  if (a.ds) {
+    // dk, dv and the stored dS, then dq from dS
+    if ((e = attn_ds_offsets(a, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((dkdv_kernel<D, true>), gkv, dim3(256), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 gq = wg_grid((a.max_seqlen + 255) / 256, a.num_heads, a.num_seqs);
+    hipLaunchKernelGGL((dq_ds_kernel<D>), gq, dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((dkdv_kernel<D, false>), gkv, dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const dim3 gq = wg_grid((a.max_seqlen + 127) / 128, a.num_heads, a.num_seqs);
   hipLaunchKernelGGL((dq_kernel<D>), gq, dim3(256), 0, st, a);
@@ -747,6 +974,12 @@ hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
 
 }  // namespace
 
+hipError_t attn_ds_offsets(const AttnDesc& a, hipStream_t st) {
+  hipLaunchKernelGGL(ds_offsets_kernel, dim3(1), dim3(256), 0, st, a.cu_seqlens, a.prefix_len, a.num_seqs,
+                     a.num_heads, (a.num_prefix + kRows - 1) / kRows, a.ds_off);
+  return hipGetLastError();
+}
+
 // Buffer resources are rebased per 64-row tile, so any sequence length
 // works; head dims 64 and 128.
 bool attn_bf16_ok(const AttnDesc& a) { return a.head_dim == 64 || a.head_dim == 128; }
@@ -754,6 +987,13 @@ bool attn_bf16_ok(const AttnDesc& a) { return a.head_dim == 64 || a.head_dim == 
 hipError_t attn_fwd_bf16(const AttnDesc& a, hipStream_t st) {
   if (a.num_seqs <= 0 || a.max_seqlen <= 0) return hipSuccess;
   return a.head_dim == 128 ? fwd_launch<128>(a, st) : fwd_launch<64>(a, st);
+}
+
+size_t attn_ds_tiles(const int32_t* cu, const int32_t* prefix, int num_seqs, int num_heads, int num_prefix) {
+  const int ntp = (num_prefix + kRows - 1) / kRows;
+  size_t n = 0;
+  for (int s = 0; s < num_seqs; ++s) n += (size_t)num_heads * ds_seq_tiles(cu[s + 1] - cu[s], prefix ? prefix[s] : 0, ntp);
+  return n;
 }
 
 hipError_t attn_bwd_bf16(const AttnDesc& a, hipStream_t st) {

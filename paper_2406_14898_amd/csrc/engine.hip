@@ -135,6 +135,9 @@ struct BatchInfo {
   int T, S, C, maxL;
   bool prefix;
   double pairs;  // sum over sequences of visible (query, key) pairs
+  // the descriptor's host sequence bounds (valid during the call)
+  const int32_t* cu_host;
+  const int32_t* prefix_host;
 };
 
 int validate_batch(const fl_batch_desc* b, BatchInfo* bi) {
@@ -179,6 +182,8 @@ int validate_batch(const fl_batch_desc* b, BatchInfo* bi) {
   bi->C = b->num_clients;
   bi->maxL = maxL;
   bi->prefix = b->mask_kind == FL_MASK_PREFIX;
+  bi->cu_host = cu;
+  bi->prefix_host = bi->prefix ? b->prefix_len : nullptr;
   bi->pairs = 0;
   for (int s = 0; s < b->num_seqs; ++s) {
     const double L = cu[s + 1] - cu[s];
@@ -282,7 +287,15 @@ struct Work {
   float *part, *part2;
   float* lnp[3];  // fused LayerNorm backward partials: gain, shift, output sums, [kLnBlocks][H] each
   float* dprefix;
+  // stored attention softmax gradient (bf16, see attn_ds_tiles) and its
+  // per-sequence offsets; null above kAttnDsMaxBytes (dq then recomputes it)
+  void* ds;
+  int64_t* ds_off;
 };
+// The stored softmax gradient grows with the sum of squared sequence
+// lengths (about 1.9 GB for 32 heads over 32 sequences of 512 to 2048
+// tokens); beyond this, the backward recomputes it in the dq kernel.
+constexpr size_t kAttnDsMaxBytes = size_t(8) << 30;
 void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   const size_t E = st->E, H = st->d.hidden, F = st->d.ffn_hidden, T = bi.T;
   carve_plan(cv, bi, st->d.rotary_dim, &w->plan);
@@ -303,6 +316,16 @@ void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   // per-sequence P-tuning v2 prefix gradients, [2][S][L_p][H] fp32
   const size_t np = st->d.num_prefix;
   w->dprefix = np ? (float*)cv.take(sizeof(float) * 2 * bi.S * np * H) : nullptr;
+  w->ds = nullptr;
+  w->ds_off = nullptr;
+  if (st->d.dtype == FL_BF16) {
+    const size_t ds_bytes =
+        attn_ds_tiles(bi.cu_host, bi.prefix_host, bi.S, st->d.num_heads, st->d.num_prefix) * kAttnDsTileBytes;
+    if (ds_bytes <= kAttnDsMaxBytes) {
+      w->ds_off = (int64_t*)cv.take(attn_ds_off_bytes(bi.S));
+      w->ds = cv.take(ds_bytes);
+    }
+  }
 }
 
 size_t saved_bytes(const fl_stack* st, const BatchInfo& bi, bool recompute) {
@@ -619,6 +642,7 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.pos = plan.pos; ad.cos_t = plan.cos_t; ad.sin_t = plan.sin_t;
   ad.rotary_dim = st->d.rotary_2d ? 0 : st->d.rotary_dim;
   ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix; ad.dprefix_part = w.dprefix;
+  ad.ds = w.ds; ad.ds_off = w.ds_off;
   const double pairs = bi.pairs + (double)st->d.num_prefix * T;
   LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
   if (st->d.rotary_2d)  // dq and dk rotated back: first half by p1, second by the block position

@@ -144,7 +144,23 @@ struct AttnDesc {
   const void* pv = nullptr;
   int num_prefix = 0;
   float* dprefix_part = nullptr;
+  // Backward (bf16 kernels): storage for the softmax gradient dS, 64 x 64
+  // bf16 tiles (attn_ds_tiles of them), and ds_off, device int64 [S + 1]
+  // scratch for their per-sequence offsets.  Null ds: the dq kernel
+  // recomputes S and dP instead of reading dS.
+  void* ds = nullptr;
+  int64_t* ds_off = nullptr;
 };
+// Tiles of stored dS a backward over these (host) sequence bounds needs:
+// per sequence and head, one per (64-query tile, 64-key tile) pair holding a
+// visible pair, prefix key tiles included.
+size_t attn_ds_tiles(const int32_t* cu_host, const int32_t* prefix_host, int num_seqs, int num_heads,
+                     int num_prefix);
+constexpr size_t kAttnDsTileBytes = 64 * 64 * 2;
+// Fills a.ds_off from the device sequence bounds (ds_off[S] = the total).
+hipError_t attn_ds_offsets(const AttnDesc& a, hipStream_t st);
+// Bytes of the ds_off table (S + 1 int64), rounded up to 256.
+inline size_t attn_ds_off_bytes(int num_seqs) { return ((size_t)(num_seqs + 1) * 8 + 255) / 256 * 256; }
 hipError_t attn_fwd(DType dt, const AttnDesc& a, hipStream_t st);
 hipError_t attn_bwd(DType dt, const AttnDesc& a, hipStream_t st);
 // delta[t][h] = rowsum(dO * O), the backward pre-pass.

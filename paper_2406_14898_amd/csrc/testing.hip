@@ -173,7 +173,7 @@ int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float
                           float* delta, const int32_t* cu_dev, const int32_t* prefix_dev, const int32_t* pos,
                           const float* cos_t, const float* sin_t, int rotary_dim, int T, int S, int max_seqlen, int H,
                           int num_heads, const void* pk, const void* pv, int num_prefix, float* dprefix_part,
-                          void* stream) {
+                          void* ds_work, size_t ds_bytes, void* stream) {
   if (!dtype_ok(dtype)) return set_error(FL_ERR_ARG, "bad dtype");
   if (!qkv || !o || !lse || !dout || !dqkv || !delta || !cu_dev) return set_error(FL_ERR_NULL, "NULL argument");
   if (num_heads <= 0 || H % num_heads) return set_error(FL_ERR_ARG, "bad heads");
@@ -190,7 +190,34 @@ int fl_test_attention_bwd(int dtype, const void* qkv, const void* o, const float
   a.dout = dout; a.ld_dout = H; a.delta = delta; a.dqkv = dqkv; a.ld_dqkv = 3L * H;
   a.pos = pos; a.cos_t = cos_t; a.sin_t = sin_t; a.rotary_dim = rotary_dim;
   a.pk = pk; a.pv = pv; a.num_prefix = num_prefix; a.dprefix_part = dprefix_part;
+  if (ds_work) {
+    // [S + 1] int64 offsets (256-byte aligned), then the tiles; the tile
+    // count needs the host bounds, so only the size is checked here
+    if (dtype != FL_BF16) return set_error(FL_ERR_ARG, "stored dS needs bf16");
+    const size_t head = attn_ds_off_bytes(S);
+    if (ds_bytes < head || ((uintptr_t)ds_work & 255)) return set_error(FL_ERR_WORKSPACE, "ds_work too small or unaligned");
+    a.ds_off = static_cast<int64_t*>(ds_work);
+    a.ds = static_cast<char*>(ds_work) + head;
+    // the tile count from the device bounds, checked before anything writes
+    // tiles
+    hipStream_t sm = (hipStream_t)stream;
+    int64_t total = 0;
+    if (hipError_t e = attn_ds_offsets(a, sm); e != hipSuccess) return herr(e);
+    if (hipError_t e = hipMemcpyAsync(&total, a.ds_off + S, sizeof(total), hipMemcpyDeviceToHost, sm); e != hipSuccess)
+      return herr(e);
+    if (hipError_t e = hipStreamSynchronize(sm); e != hipSuccess) return herr(e);
+    if (total < 0 || ds_bytes < head + (size_t)total * kAttnDsTileBytes)
+      return set_error(FL_ERR_WORKSPACE, "ds_work smaller than the stored dS needs");
+  }
   return herr(attn_bwd((DType)dtype, a, (hipStream_t)stream));
+}
+
+int fl_test_attention_ds_bytes(const int32_t* cu_host, const int32_t* prefix_host, int S, int num_heads,
+                               int num_prefix, size_t* bytes) {
+  if (!cu_host || !bytes) return set_error(FL_ERR_NULL, "NULL argument");
+  if (S < 1 || num_heads < 1 || num_prefix < 0) return set_error(FL_ERR_ARG, "bad sizes");
+  *bytes = attn_ds_off_bytes(S) + attn_ds_tiles(cu_host, prefix_host, S, num_heads, num_prefix) * kAttnDsTileBytes;
+  return FL_OK;
 }
 
 }  // extern "C"

@@ -44,7 +44,7 @@ EXPORTS = (
     "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_layernorm_bwd_fused",
     "fl_test_colsum",
-    "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd",
+    "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd", "fl_test_attention_ds_bytes",
 )
 
 
@@ -131,7 +131,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_test_colsum": [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp],
         "fl_test_rope": [ctypes.c_int, vp, vp] + [ctypes.c_int] * 6 + [ctypes.c_float, vp, vp, vp, vp],
         "fl_test_attention_fwd": [ctypes.c_int, vp, vp, vp, vp, vp] + [ctypes.c_int] * 5 + [vp, vp, ctypes.c_int, vp],
-        "fl_test_attention_bwd": [ctypes.c_int] + [vp] * 11 + [ctypes.c_int] * 6 + [vp, vp, ctypes.c_int, vp, vp],
+        "fl_test_attention_bwd": [ctypes.c_int] + [vp] * 11 + [ctypes.c_int] * 6 + [vp, vp, ctypes.c_int, vp, vp,
+                                                                                    ctypes.c_size_t, vp],
+        "fl_test_attention_ds_bytes": [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_size_t)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -434,8 +437,22 @@ def fl_test_attention_fwd(dtype, qkv, o, lse, cu_dev, prefix_dev, T, S, max_seql
 
 def fl_test_attention_bwd(dtype, qkv, o, lse, dout, dqkv, delta, cu_dev, prefix_dev, pos, cos_t, sin_t, rotary_dim,
                           T, S, max_seqlen, H, num_heads, pk=None, pv=None, num_prefix=0, dprefix_part=None,
-                          stream=None) -> None:
+                          ds_work=None, stream=None) -> None:
+    """ds_work: device byte tensor of fl_test_attention_ds_bytes bytes (dq
+    reads the stored softmax gradient), or None (dq recomputes it)."""
+    nbytes = ds_work.numel() * ds_work.element_size() if ds_work is not None else 0
     _check(load().fl_test_attention_bwd(dtype, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(dout), _ptr(dqkv), _ptr(delta),
                                         _ptr(cu_dev), _ptr(prefix_dev), _ptr(pos), _ptr(cos_t), _ptr(sin_t),
                                         rotary_dim, T, S, max_seqlen, H, num_heads, _ptr(pk), _ptr(pv), num_prefix,
-                                        _ptr(dprefix_part), _stream(stream)))
+                                        _ptr(dprefix_part), _ptr(ds_work), nbytes, _stream(stream)))
+
+
+def fl_test_attention_ds_bytes(cu_host, prefix_host, num_heads, num_prefix=0) -> int:
+    """Bytes of ds_work for these host sequence bounds (numpy int32 cu_host
+    [S+1], prefix_host [S] or None)."""
+    cu = np.ascontiguousarray(cu_host, dtype=np.int32)
+    pre = None if prefix_host is None else np.ascontiguousarray(prefix_host, dtype=np.int32)
+    out = ctypes.c_size_t(0)
+    _check(load().fl_test_attention_ds_bytes(cu.ctypes.data, None if pre is None else pre.ctypes.data,
+                                             len(cu) - 1, num_heads, num_prefix, ctypes.byref(out)))
+    return int(out.value)

@@ -294,3 +294,34 @@ def test_noalloc_forward_rejects_what_does_not_fit():
         F.fl_server_stack_forward_noalloc(h, F.BatchDesc([0, 1000], [0, 1]), [L], 1 << 40, None, 0)
     assert e.value.code == F.FL_ERR_NULL
     F.fl_stack_destroy(h)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_attention_ds_tiles_count_visible_tile_pairs(seed):
+    """The stored softmax gradient holds one 64 x 64 tile per (query tile, key
+    tile) pair with at least one visible pair (the oracle's mask), plus the
+    prefix key tiles every query tile meets, per head: the size the library
+    asks for equals that brute-force count (host-only)."""
+    import numpy as np
+    import oracle
+    _lib()
+    rng = np.random.default_rng(seed)
+    S = int(rng.integers(1, 6))
+    lens = rng.integers(1, 300, S)
+    if seed == 0:
+        lens[:] = [64, 128, 1, 65, 192][:S] if S <= 5 else lens
+    prefix = None if seed % 2 else rng.integers(0, lens + 1).astype(np.int32)
+    nh, num_prefix = int(rng.integers(1, 4)), int(rng.choice([0, 1, 64, 70]))
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ntp = (num_prefix + 63) // 64
+    tiles = 0
+    for s in range(S):
+        L = int(lens[s])
+        m = oracle.allowed_mask(L, None if prefix is None else int(prefix[s]))
+        nt = (L + 63) // 64
+        for qt in range(nt):
+            tiles += ntp
+            for kt in range(nt):
+                tiles += bool(m[64 * qt:64 * qt + 64, 64 * kt:64 * kt + 64].any())
+    off_bytes = ((S + 1) * 8 + 255) // 256 * 256
+    assert F.fl_test_attention_ds_bytes(cu, prefix, nh, num_prefix) == off_bytes + nh * tiles * 64 * 64 * 2

@@ -352,6 +352,12 @@ def _lse_ref(q, k, b):
     return out
 
 
+def _ds_work(cu_seqlens, prefix_len, nh, num_prefix=0):
+    """Device workspace for the stored softmax gradient of a bf16 backward."""
+    n = F.fl_test_attention_ds_bytes(np.asarray(cu_seqlens), prefix_len, nh, num_prefix)
+    return torch.empty(n, dtype=torch.uint8, device="cuda")
+
+
 @pytest.mark.parametrize("dt", DT)
 @pytest.mark.parametrize("heads", [(2, 128), (4, 64)])
 @pytest.mark.parametrize("bname", list(BATCHES))
@@ -376,10 +382,12 @@ def test_attention_fwd_bwd(dt, heads, bname):
     assert rel_l2(host(o), o_ref) < TOL[dt] / 2
     assert rel_l2(host(lse), _lse_ref(q, k, b)) < 1e-5
 
-    # backward, with and without the inverse rotation of dq, dk
+    # backward, with and without the inverse rotation of dq, dk; bf16 with
+    # dq recomputing the softmax gradient and with dq reading it stored
     do = rnd((T, H), 22, dt=dt)
     dq, dk, dv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b)
-    for r in (0, d // 2):
+    pre_h = b.prefix_len if b.mask == "prefix" else None
+    for r, stored in [(0, False), (d // 2, False)] + ([(0, True), (d // 2, True)] if dt == "bf16" else []):
         dqr, dkr = dq, dk
         pos = ct = st = None
         if r:
@@ -394,20 +402,23 @@ def test_attention_fwd_bwd(dt, heads, bname):
             F.fl_test_rope(code, scratch, cu, b.num_seqs, T, b.max_seqlen, H, nh, r, 10000.0, pos, ct, st)
         dqkv = torch.full((T, 3 * H), float("nan"), dtype=tdt, device="cuda")
         delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+        ds = _ds_work(b.cu_seqlens, pre_h, nh) if stored else None
         F.fl_test_attention_bwd(code, t, o, lse, dev(do, dt), dqkv, delta, cu, pre, pos, ct, st, r, T, b.num_seqs,
-                                b.max_seqlen, H, nh)
+                                b.max_seqlen, H, nh, ds_work=ds)
         sync()
         g = host(dqkv)
         tol = TOL[dt] / 2
-        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
-        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
-        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, (r, stored)
+        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, (r, stored)
+        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, (r, stored)
 
 
+@pytest.mark.parametrize("stored", [False, True])
 @pytest.mark.parametrize("mask", ["causal", "prefix"])
-def test_attention_long_sequence(mask):
+def test_attention_long_sequence(mask, stored):
     """One 8192-token sequence (bf16, 2 heads of 128; prefix-LM with a
-    2048-token context), forward and backward with the inverse rotation."""
+    2048-token context), forward and backward with the inverse rotation; dq
+    from the recomputed or the stored softmax gradient."""
     nh, d = 2, 128
     H, T = nh * d, 8192
     b = synth.Batch(np.array([0, T], np.int32), np.array([0, 1], np.int32), mask,
@@ -431,8 +442,9 @@ def test_attention_long_sequence(mask):
     do = rnd((T, H), 24, dt="bf16")
     dqkv = torch.empty((T, 3 * H), dtype=torch.bfloat16, device="cuda")
     delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+    ds = _ds_work(b.cu_seqlens, b.prefix_len if mask == "prefix" else None, nh) if stored else None
     F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, dev(do, "bf16"), dqkv, delta, cu, pre, pos, ct, st, r, T, 1, T,
-                            H, nh)
+                            H, nh, ds_work=ds)
     sync()
     assert rel_l2(host(o), oracle.attention_forward(q, k, v, b).reshape(T, H)) < TOL["bf16"] / 2
     dq, dk, dv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b)
@@ -441,6 +453,41 @@ def test_attention_long_sequence(mask):
     assert rel_l2(g[:, :H], oracle.rope(dq, cos, sin, r, inverse=True).reshape(T, H)) < TOL["bf16"] / 2
     assert rel_l2(g[:, H:2 * H], oracle.rope(dk, cos, sin, r, inverse=True).reshape(T, H)) < TOL["bf16"] / 2
     assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < TOL["bf16"] / 2
+
+
+def test_attention_stored_ds_deterministic_and_checked():
+    """bf16 backward with the stored softmax gradient: two calls give the same
+    bits, the result agrees with the recomputing dq, and a ds_work one tile
+    short is refused (FL_ERR_WORKSPACE) before any tile is written."""
+    nh, d = 4, 128
+    H = nh * d
+    b = BATCHES["ragged_prefix"]
+    T, S = b.total_tokens, b.num_seqs
+    t = dev(_qkv(T, H, 31, "bf16"), "bf16")
+    cu, pre = dev_i32(b.cu_seqlens), dev_i32(b.prefix_len)
+    o = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+    F.fl_test_attention_fwd(F.FL_BF16, t, o, lse, cu, pre, T, S, b.max_seqlen, H, nh)
+    do = dev(rnd((T, H), 32), "bf16")
+    delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
+    outs = []
+    for stored in (True, True, False):
+        dqkv = torch.full((T, 3 * H), float("nan"), dtype=torch.bfloat16, device="cuda")
+        ds = _ds_work(b.cu_seqlens, b.prefix_len, nh) if stored else None
+        F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, do, dqkv, delta, cu, pre, None, None, None, 0, T, S,
+                                b.max_seqlen, H, nh, ds_work=ds)
+        sync()
+        outs.append(host(dqkv))
+    assert np.array_equal(outs[0], outs[1])
+    assert rel_l2(outs[0][:, :H], outs[2][:, :H]) < 1e-2
+    assert np.array_equal(outs[0][:, H:], outs[2][:, H:])  # dk, dv: the same kernel either way
+    n = F.fl_test_attention_ds_bytes(b.cu_seqlens, b.prefix_len, nh)
+    short = torch.empty(n - 64 * 64 * 2, dtype=torch.uint8, device="cuda")
+    dqkv = torch.empty((T, 3 * H), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(F.FlglmError) as e:
+        F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, do, dqkv, delta, cu, pre, None, None, None, 0, T, S,
+                                b.max_seqlen, H, nh, ds_work=short)
+    assert e.value.code == F.FL_ERR_WORKSPACE
 
 
 # ---------------------------------------------------------------------------
@@ -495,7 +542,8 @@ def test_attention_prefix_fwd_bwd(heads, bname, num_prefix):
 
     do = rnd((T, H), 53)
     dq, dk, dv, dpk, dpv = oracle.attention_backward(q, k, v, do.astype(np.float64).reshape(T, nh, d), b, pk3, pv3)
-    for r in (0, d // 2):
+    pre_h = b.prefix_len if b.mask == "prefix" else None
+    for r, stored in [(0, False), (d // 2, False), (0, True), (d // 2, True)]:
         dqr, dkr = dq, dk
         pos = ct = st = None
         if r:
@@ -511,17 +559,18 @@ def test_attention_prefix_fwd_bwd(heads, bname, num_prefix):
         dqkv = torch.full((T, 3 * H), float("nan"), dtype=torch.bfloat16, device="cuda")
         delta = torch.empty((T, nh), dtype=torch.float32, device="cuda")
         part = torch.full((2, S, num_prefix, H), float("nan"), dtype=torch.float32, device="cuda")
+        ds = _ds_work(b.cu_seqlens, pre_h, nh, num_prefix) if stored else None
         F.fl_test_attention_bwd(F.FL_BF16, t, o, lse, dev(do, "bf16"), dqkv, delta, cu, pre, pos, ct, st, r, T, S,
-                                b.max_seqlen, H, nh, tpk, tpv, num_prefix, part)
+                                b.max_seqlen, H, nh, tpk, tpv, num_prefix, part, ds_work=ds)
         sync()
         g = host(dqkv)
         tol = TOL["bf16"] / 2
-        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, r
-        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, r
-        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, r
+        assert rel_l2(g[:, :H], dqr.reshape(T, H)) < tol, (r, stored)
+        assert rel_l2(g[:, H:2 * H], dkr.reshape(T, H)) < tol, (r, stored)
+        assert rel_l2(g[:, 2 * H:], dv.reshape(T, H)) < tol, (r, stored)
         pg = host(part).sum(axis=1)  # sequence partials -> the batch's prefix gradients
-        assert rel_l2(pg[0], dpk.reshape(-1, H)) < tol, r
-        assert rel_l2(pg[1], dpv.reshape(-1, H)) < tol, r
+        assert rel_l2(pg[0], dpk.reshape(-1, H)) < tol, (r, stored)
+        assert rel_l2(pg[1], dpv.reshape(-1, H)) < tol, (r, stored)
 
 
 @pytest.mark.parametrize("mask", ["causal", "prefix"])
