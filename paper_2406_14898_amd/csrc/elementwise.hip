@@ -62,13 +62,14 @@ hipError_t rope_table(float* ct, float* stbl, int max_pos, int r, float base, hi
   return hipGetLastError();
 }
 
-// One thread rotates 4 pairs (i, i + r/2), i..i+3, of one head of q or k.
+// One thread rotates 8 pairs (i, i + r/2), i..i+7, of one head of q or k
+// (16-byte loads for bf16; r / 2 is a multiple of 8).
 template <typename T>
 // pos2 (GLM 2-D positions): the same thread also rotates the matching pairs
 // of dims [r, 2r) by pos2, so both halves take one pass over q and k.
 __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const int32_t* pos2, const float* ct,
                                const float* stbl, int T_, int H, int d, int r, float sign) {
-  const int half = r / 2, groups = half / 4;
+  const int half = r / 2, groups = half / 8;
   const int nh = H / d;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   const long per_row = 2L * nh * groups;
@@ -77,48 +78,36 @@ __global__ void rope_qk_kernel(T* qkv, long ld, const int32_t* pos, const int32_
   int rem = (int)(idx % per_row);
   const int part = rem / (nh * groups);
   rem %= nh * groups;
-  const int h = rem / groups, i = (rem % groups) * 4;
+  const int h = rem / groups, i = (rem % groups) * 8;
   T* base = qkv + (long)t * ld + part * H + h * d;
-  const int p = pos[t];
-  Vec4<T> a, b;
-  a.load(base + i);
-  b.load(base + half + i);
-  const float* c = ct + (long)p * half + i;
-  const float* s = stbl + (long)p * half + i;
-  float ya[4], yb[4];
+  auto rotate = [&](int off, int p) {
+    Vec8<T> a, b;
+    a.load(base + off + i);
+    b.load(base + off + half + i);
+    Vec8<float> c, sn;
+    c.load(ct + (long)p * half + i);
+    sn.load(stbl + (long)p * half + i);
+    float ya[8], yb[8];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float x1 = a.get(e), x2 = b.get(e), sn = sign * s[e];
-    ya[e] = x1 * c[e] - x2 * sn;
-    yb[e] = x2 * c[e] + x1 * sn;
-  }
-  a.set(ya);
-  b.set(yb);
-  a.store(base + i);
-  b.store(base + half + i);
-  if (pos2) {
-    const int p2 = pos2[t];
-    a.load(base + r + i);
-    b.load(base + r + half + i);
-    const float* c2 = ct + (long)p2 * half + i;
-    const float* s2 = stbl + (long)p2 * half + i;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float x1 = a.get(e), x2 = b.get(e), sn = sign * s2[e];
-      ya[e] = x1 * c2[e] - x2 * sn;
-      yb[e] = x2 * c2[e] + x1 * sn;
+    for (int e = 0; e < 8; ++e) {
+      const float x1 = a.get(e), x2 = b.get(e), se = sign * sn.get(e);
+      ya[e] = x1 * c.get(e) - x2 * se;
+      yb[e] = x2 * c.get(e) + x1 * se;
     }
     a.set(ya);
     b.set(yb);
-    a.store(base + r + i);
-    b.store(base + r + half + i);
-  }
+    a.store(base + off + i);
+    b.store(base + off + half + i);
+  };
+  rotate(0, pos[t]);
+  if (pos2) rotate(r, pos2[t]);
 }
 
 hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float* ct, const float* stbl, int T_,
                    int H, int d, int r, hipStream_t st, float sign, const int32_t* pos2) {
-  const long n = (long)T_ * 2 * (H / d) * (r / 8);
+  const long n = (long)T_ * 2 * (H / d) * (r / 16);
   if (n <= 0) return hipSuccess;
+  if (r % 16 != 0) return hipErrorInvalidValue;
   dim3 g((unsigned)((n + 255) / 256));
   if (dt == DT_BF16)
     hipLaunchKernelGGL(rope_qk_kernel<bf16>, g, dim3(256), 0, st, (bf16*)qkv, ld, pos, pos2, ct, stbl, T_, H, d, r,
@@ -130,8 +119,10 @@ hipError_t rope_qk(DType dt, void* qkv, long ld, const int32_t* pos, const float
 }
 
 // ---------------------------------------------------------------------------
-// LayerNorm: one wave per row, the row held in registers (MAXC 8-element
-// chunks per lane, H <= 512 * MAXC).
+// LayerNorm: one wave per row, the row held in registers in its storage
+// type (MAXC 8-element chunks per lane, H <= 512 * MAXC) and converted on
+// each of the three passes: half the registers of an fp32 copy for bf16
+// rows, so twice as many rows are in flight per CU.
 // ---------------------------------------------------------------------------
 template <typename T, int MAXC>
 __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, const T* b, T* y, float* mean,
@@ -141,28 +132,32 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, con
   if (row >= T_) return;
   const int nch = H / 8;
   const T* xr = x + (long)row * H;
-  float v[MAXC][8];
-  float s = 0.f;
+  Vec8<T> v[MAXC];
 #pragma unroll
   for (int c = 0; c < MAXC; ++c) {
     const int idx = lane + 64 * c;
-    if (idx < nch) {
-      Vec8<T> t;
-      t.load(xr + idx * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) { v[c][e] = t.get(e); s += v[c][e]; }
-    }
+    if (idx < nch) v[c].load(xr + idx * 8);
+    else v[c].zero();
   }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += v[c].get(e);
   const float mu = wave_sum(s) / (float)H;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) v[c].settle();
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < MAXC; ++c) {
     if (lane + 64 * c < nch) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) { const float dlt = v[c][e] - mu; ss += dlt * dlt; }
+      for (int e = 0; e < 8; ++e) { const float dlt = v[c].get(e) - mu; ss += dlt * dlt; }
     }
   }
   const float rs = 1.0f / sqrtf(wave_sum(ss) / (float)H + eps);
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) v[c].settle();
   T* yr = y + (long)row * H;
 #pragma unroll
   for (int c = 0; c < MAXC; ++c) {
@@ -173,7 +168,7 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* x, const T* g, con
       bb.load(b + idx * 8);
       float out[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) out[e] = (v[c][e] - mu) * rs * gg.get(e) + bb.get(e);
+      for (int e = 0; e < 8; ++e) out[e] = (v[c].get(e) - mu) * rs * gg.get(e) + bb.get(e);
       o.set(out);
       o.store(yr + idx * 8);
     }
@@ -426,8 +421,8 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* X, long ld
   float a1[8], a2[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) { a1[e] = 0.f; a2[e] = 0.f; }
-  // rows r0 + w, r0 + w + 4, ... in order; four of them loaded before any is
-  // added, so each wave keeps four loads in flight (same summation order)
+  // rows r0 + w, r0 + w + 4, ... in order; eight of them loaded before any
+  // is added, so each wave keeps eight loads in flight (same summation order)
   auto add = [&](const Vec8<T>& xv, const Vec8<T>& yv, int r) {
     if constexpr (MODE == 0) {
 #pragma unroll
@@ -443,15 +438,16 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* X, long ld
   };
   if (col < N) {
     int r = r0 + w;
-    for (; r + 12 < r1; r += 16) {
-      Vec8<T> xv[4], yv[4];
+    constexpr int B = MODE == 0 ? 8 : 4;
+    for (; r + 4 * (B - 1) < r1; r += 4 * B) {
+      Vec8<T> xv[B], yv[B];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < B; ++u) {
         xv[u].load(X + (long)(r + 4 * u) * ldx + col);
         if constexpr (MODE == 1) yv[u].load(Y + (long)(r + 4 * u) * ldx + col);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) add(xv[u], yv[u], r + 4 * u);
+      for (int u = 0; u < B; ++u) add(xv[u], yv[u], r + 4 * u);
     }
     for (; r < r1; r += 4) {
       Vec8<T> xv, yv;
