@@ -291,11 +291,12 @@ hipError_t layernorm_bwd_dx(DType dt, const void* dy, const void* x, const float
 // colsum_finish adds in block order: deterministic.  One pass reads dy, x
 // (and dres) once, instead of once for dx and again for the column sums.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T* x, const float* mean,
-                                                           const float* rstd, const T* g, const T* dres, T* dx,
-                                                           int T_, int H, float* pg, float* pb, float* pout) {
-  __shared__ float red[2][4][8][2];  // [batch parity][row][wave][sum]
+// (bf16: at most 128 registers, two workgroups per CU)
+template <typename T, int R>
+__global__ void __launch_bounds__(512, sizeof(T) == 2 ? 4 : 2)
+    ln_bwd_fused_kernel(const T* dy, const T* x, const float* __restrict__ mean, const float* __restrict__ rstd,
+                        const T* g, const T* dres, T* dx, int T_, int H, float* pg, float* pb, float* pout) {
+  __shared__ float red[2][R][8][2];  // [batch parity][row][wave][sum]
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = w * 512 + lane * 8;
   const bool on = col < H;
@@ -309,31 +310,37 @@ __global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T*
     for (int e = 0; e < 8; ++e) { gv[e] = gg.get(e); ag[e] = 0.f; ab[e] = 0.f; ao[e] = 0.f; }
   }
   const float invH = 1.f / (float)H;
-  int par = 0;
-  for (int rb = r0; rb < r1; rb += 4, par ^= 1) {
-    Vec8<T> a[4], xx[4], rr[4];
-    float mu[4], rs[4];
+  // Two row batches in flight: batch i + 1 is loaded before batch i's
+  // barrier, so its memory latency overlaps the barrier, the output and the
+  // stores of batch i.
+  Vec8<T> a[2][R], xx[2][R], rr[2][R];
+  auto load = [&](int buf, int rb) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < R; ++u) {
       const int r = rb + u;
-      const bool ok = on && r < r1;
-      if (ok) {
-        a[u].load(dy + (long)r * H + col);
-        xx[u].load(x + (long)r * H + col);
-        if (dres) rr[u].load(dres + (long)r * H + col); else rr[u].zero();
+      if (on && r < r1) {
+        a[buf][u].load(dy + (long)r * H + col);
+        xx[buf][u].load(x + (long)r * H + col);
+        if (dres) rr[buf][u].load(dres + (long)r * H + col); else rr[buf][u].zero();
       } else {
-        a[u].zero(); xx[u].zero(); rr[u].zero();
+        a[buf][u].zero(); xx[buf][u].zero(); rr[buf][u].zero();
       }
+    }
+  };
+  auto batch = [&](auto bufc, int rb, int par) {
+    constexpr int B = decltype(bufc)::value;
+    float mu[R], rs[R], s1[R], s2[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int r = rb + u;
+      // row statistics: wave-uniform (scalar) loads, which do not queue
+      // behind the vector stores of the previous batch
       mu[u] = r < r1 ? mean[r] : 0.f;
       rs[u] = r < r1 ? rstd[r] : 0.f;
-    }
-    float s1[4], s2[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
       s1[u] = 0.f; s2[u] = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float xh = (xx[u].get(e) - mu[u]) * rs[u], d = a[u].get(e) * gv[e];
+        const float xh = (xx[B][u].get(e) - mu[u]) * rs[u], d = a[B][u].get(e) * gv[e];
         s1[u] += d;
         s2[u] += d * xh;
       }
@@ -342,15 +349,16 @@ __global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T*
     }
     if (lane == 0) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) { red[par][u][w][0] = s1[u]; red[par][u][w][1] = s2[u]; }
+      for (int u = 0; u < R; ++u) { red[par][u][w][0] = s1[u]; red[par][u][w][1] = s2[u]; }
     }
+    if (rb + R < r1) load(B ^ 1, rb + R);
     __syncthreads();  // one barrier per batch: the other parity's slots are free again
-    // the packed rows are re-read from here on (the values converted before
-    // the barrier are not kept live across it: 128 registers instead of 188)
+    // the packed rows are re-read from here on (values converted before the
+    // barrier are not kept live across it)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) { a[u].settle(); xx[u].settle(); }
+    for (int u = 0; u < R; ++u) { a[B][u].settle(); xx[B][u].settle(); }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < R; ++u) {
       float t1 = 0.f, t2 = 0.f;
       for (int v = 0; v < nw; ++v) { t1 += red[par][u][v][0]; t2 += red[par][u][v][1]; }
       const float m1 = t1 * invH, m2 = t2 * invH;
@@ -359,8 +367,8 @@ __global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T*
         float out[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float xh = (xx[u].get(e) - mu[u]) * rs[u], dv = a[u].get(e);
-          out[e] = rr[u].get(e) + rs[u] * (dv * gv[e] - m1 - xh * m2);
+          const float xh = (xx[B][u].get(e) - mu[u]) * rs[u], dv = a[B][u].get(e);
+          out[e] = rr[B][u].get(e) + rs[u] * (dv * gv[e] - m1 - xh * m2);
           ag[e] += dv * xh;
           ab[e] += dv;
         }
@@ -372,6 +380,16 @@ __global__ void __launch_bounds__(512) ln_bwd_fused_kernel(const T* dy, const T*
           for (int e = 0; e < 8; ++e) ao[e] += o.get(e);  // the stored (rounded) values
         }
       }
+    }
+  };
+  load(0, r0);
+  int par = 0;
+  for (int rb = r0; rb < r1; rb += 2 * R) {
+    batch(std::integral_constant<int, 0>{}, rb, par);
+    par ^= 1;
+    if (rb + R < r1) {
+      batch(std::integral_constant<int, 1>{}, rb + R, par);
+      par ^= 1;
     }
   }
   if (on) {
@@ -395,12 +413,13 @@ hipError_t layernorm_bwd_fused(DType dt, const void* dy, const void* x, const fl
   if (T_ <= 0) return hipSuccess;
   if (H > 4096 || H % 8 != 0 || (pg == nullptr) != (pb == nullptr)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)kLnBlocks), blk(512);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL((ln_bwd_fused_kernel<bf16>), grid, blk, 0, st, (const bf16*)dy, (const bf16*)x, mean, rstd,
+  if (dt == DT_BF16) {
+    hipLaunchKernelGGL((ln_bwd_fused_kernel<bf16, 2>), grid, blk, 0, st, (const bf16*)dy, (const bf16*)x, mean, rstd,
                        (const bf16*)g, (const bf16*)dres, (bf16*)dx, T_, H, pg, pb, pout);
-  else
-    hipLaunchKernelGGL((ln_bwd_fused_kernel<float>), grid, blk, 0, st, (const float*)dy, (const float*)x, mean,
+  } else {
+    hipLaunchKernelGGL((ln_bwd_fused_kernel<float, 2>), grid, blk, 0, st, (const float*)dy, (const float*)x, mean,
                        rstd, (const float*)g, (const float*)dres, (float*)dx, T_, H, pg, pb, pout);
+  }
   return hipGetLastError();
 }
 
@@ -495,14 +514,21 @@ hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const voi
 }
 
 // out[n] += sum over the nblk partial rows.  A workgroup takes 64 columns;
-// its four waves sum contiguous quarters of the rows (eight loads in flight
-// per lane), and the quarters are added in order through LDS: a fixed order,
-// so the result is deterministic.
-__global__ void __launch_bounds__(256) colsum_finish_kernel(const float* part, int nblk, int N, float* out) {
-  __shared__ float q[4][64];
+// its 16 waves sum contiguous sixteenths of the rows (eight loads in flight
+// per lane), and the sixteenths are added in order through LDS: a fixed
+// order, so the result is deterministic.  Up to three (partial, out) pairs
+// of one shape go in one launch (grid y).
+struct FinishSet {
+  const float* part[3];
+  float* out[3];
+};
+__global__ void __launch_bounds__(1024) colsum_finish_kernel(FinishSet fs, int nblk, int N) {
+  constexpr int NW = 16;
+  __shared__ float q[NW][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = blockIdx.x * 64 + lane;
-  const int per = (nblk + 3) / 4;
+  const float* part = fs.part[blockIdx.y];
+  const int per = (nblk + NW - 1) / NW;
   const int b0 = min(nblk, w * per), b1 = min(nblk, b0 + per);
   float s = 0.f;
   if (n < N) {
@@ -518,13 +544,26 @@ __global__ void __launch_bounds__(256) colsum_finish_kernel(const float* part, i
   }
   q[w][lane] = s;
   __syncthreads();
-  if (w == 0 && n < N) out[n] += ((q[0][lane] + q[1][lane]) + q[2][lane]) + q[3][lane];
+  if (w == 0 && n < N) {
+    float t = q[0][lane];
+#pragma unroll
+    for (int v = 1; v < NW; ++v) t += q[v][lane];
+    fs.out[blockIdx.y][n] += t;
+  }
+}
+
+hipError_t colsum_finish_n(const float* const* parts, float* const* outs, int count, int nblk, int N,
+                           hipStream_t st) {
+  if (N <= 0 || count <= 0) return hipSuccess;
+  if (count > 3) return hipErrorInvalidValue;
+  FinishSet fs{};
+  for (int i = 0; i < count; ++i) { fs.part[i] = parts[i]; fs.out[i] = outs[i]; }
+  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 63) / 64, count), dim3(1024), 0, st, fs, nblk, N);
+  return hipGetLastError();
 }
 
 hipError_t colsum_finish(const float* part, int nblk, int N, float* out, hipStream_t st) {
-  if (N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 63) / 64), dim3(256), 0, st, part, nblk, N, out);
-  return hipGetLastError();
+  return colsum_finish_n(&part, &out, 1, nblk, N, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -550,12 +550,15 @@ int ln_backward(fl_stack* st, DType dt, const void* dy, const void* xin, const f
                              dgamma ? w.lnp[1] : nullptr, dsum ? w.lnp[2] : nullptr, s));
   if (!dgamma && !dsum) return FL_OK;
   LAUNCH(FL_PROF_COLSUM, 0, 4.0 * kLnBlocks * H * ((dgamma ? 2 : 0) + (dsum ? 1 : 0)), [&]() {
-    hipError_t e = hipSuccess;
+    const float* parts[3];
+    float* outs[3];
+    int n = 0;
     if (dgamma) {
-      e = colsum_finish(w.lnp[0], kLnBlocks, H, dgamma, s);
-      if (e == hipSuccess) e = colsum_finish(w.lnp[1], kLnBlocks, H, dbeta, s);
+      parts[n] = w.lnp[0]; outs[n++] = dgamma;
+      parts[n] = w.lnp[1]; outs[n++] = dbeta;
     }
-    return (e != hipSuccess || !dsum) ? e : colsum_finish(w.lnp[2], kLnBlocks, H, dsum, s);
+    if (dsum) { parts[n] = w.lnp[2]; outs[n++] = dsum; }
+    return colsum_finish_n(parts, outs, n, kLnBlocks, H, s);
   }());
   return FL_OK;
 }

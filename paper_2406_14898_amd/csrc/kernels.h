@@ -105,6 +105,9 @@ inline int colsum_blocks(int T) { return (T + kColsumRows - 1) / kColsumRows; }
 hipError_t colsum_partial(DType dt, int mode, const void* X, long ldx, const void* Y, const float* mean,
                           const float* rstd, int T, int N, float* partial, float* partial2, hipStream_t st);
 hipError_t colsum_finish(const float* partial, int nblk, int N, float* out, hipStream_t st);
+// colsum_finish of up to three partial arrays of one shape in one launch.
+hipError_t colsum_finish_n(const float* const* partials, float* const* outs, int count, int nblk, int N,
+                           hipStream_t st);
 
 // P-tuning v2 prefix gradients: out_k += sum_s part[0][s], out_v += sum_s
 // part[1][s] over n = num_prefix * hidden elements (n % 4 == 0; fixed order).
