@@ -42,16 +42,17 @@ GEMM_CLASSES = MFMA_CLASSES[:6]   # the block GEMMs
 # bf16 path (a class may launch several kernels), and the sources they are
 # built from (a stored counter reading is stale once these change).
 CLASS_KERNELS = {
-    "gemm_nt_bias": ("gemm_bf16_kernel<true, true, 1>",),
-    "gemm_nt_bias_res": ("gemm_bf16_kernel<true, true, 2>",),
-    "gemm_nt_bias_gelu": ("gemm_bf16_kernel<true, true, 3>",),
-    "gemm_nn_gelu_bwd": ("gemm_bf16_kernel<true, false, 4>",),
-    "gemm_nn": ("gemm_bf16_kernel<true, false, 0>", "gemm_bf16_kernel<true, false, 6>"),
+    # (the epilogue's row-batch template argument follows the epilogue code)
+    "gemm_nt_bias": ("gemm_bf16_kernel<true, true, 1,",),
+    "gemm_nt_bias_res": ("gemm_bf16_kernel<true, true, 2,",),
+    "gemm_nt_bias_gelu": ("gemm_bf16_kernel<true, true, 3,",),
+    "gemm_nn_gelu_bwd": ("gemm_bf16_kernel<true, false, 4,",),
+    "gemm_nn": ("gemm_bf16_kernel<true, false, 0,", "gemm_bf16_kernel<true, false, 6,"),
     "gemm_tn_acc": ("gemm_bf16_kernel<false, false",),
     "attn_fwd": ("::fwd_kernel<",),
-    "attn_bwd": ("attn_delta_kernel", "::dkdv_kernel<", "::dq_kernel<"),
+    "attn_bwd": ("attn_delta_kernel", "ds_offsets_kernel", "::dkdv_kernel<", "::dq_kernel<", "::dq_ds_kernel<"),
     "layernorm_fwd": ("ln_fwd_kernel",),
-    "layernorm_bwd": ("ln_bwd_dx_kernel",),
+    "layernorm_bwd": ("ln_bwd_fused_kernel", "ln_bwd_dx_kernel"),
     "rope_qk": ("rope_qk_kernel",),
     "colsum": ("colsum_partial_kernel", "colsum_finish_kernel"),
     "prefix_grad": ("prefix_grad_reduce_kernel",),

@@ -60,8 +60,8 @@ def _disp(*names):
     return [("1", i, n, 1.0) for i, n in enumerate(names)]
 
 
-GEMM_RES = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, true, 2>(G2Args)"
-GEMM_TN = "flglm::(anonymous namespace)::gemm_bf16_kernel<false, false, 5>(G2Args)"
+GEMM_RES = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, true, 2, 16>(G2Args)"
+GEMM_TN = "flglm::(anonymous namespace)::gemm_bf16_kernel<false, false, 5, 4>(G2Args)"
 LN = "void flglm::ln_fwd_kernel<bf16, 8>(...)"
 DELTA, DKDV, DQ = "attn_delta_kernel<bf16, 128>", "flglm::(anonymous namespace)::dkdv_kernel<128>", \
     "flglm::(anonymous namespace)::dq_kernel<128>"
@@ -83,7 +83,7 @@ def test_multi_kernel_class_counts_once():
 
 
 PART, FIN = "void flglm::colsum_partial_kernel<bf16, 0>(...)", "flglm::colsum_finish_kernel(...)"
-GELU_BWD = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, false, 4>(G2Args)"
+GELU_BWD = "flglm::(anonymous namespace)::gemm_bf16_kernel<true, false, 4, 8>(G2Args)"
 
 
 def test_finish_after_a_gemm_is_a_column_sum_launch():
