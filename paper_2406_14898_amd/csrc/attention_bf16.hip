@@ -879,6 +879,13 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
     bar();  // and every wave is past stage g - 1, whose slot stage g + 2 takes
     if (g + 2 < nst) issue(g + 2);
     if ((g >> 1) >= my_nkt) continue;
+    // query groups (16 rows) of this wave that no key of the half sees (on
+    // its diagonal tile) or past the sequence end: their dS is zero
+    const int kc = g >> 1, kh = (kc - ntp) * kRows + HR * (g & 1);
+    auto idle = [&](int qs) {
+      const int q16 = qt * kRows + 16 * qs;
+      return (kc >= ntp && q16 + 15 < kh && kh >= si.P) || q16 >= si.L;
+    };
     const int slot = g % NS;
     const bf16* ks = Ks[slot];
     const char* ss = reinterpret_cast<const char*>(Ss[slot][w]);
@@ -890,11 +897,14 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
       i16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 2048));
       df[qs] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
     }
+    bf16x8 kt_[ND];
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) {
-      const bf16x8 kt_ = rd_tr<D>(ks + fb.tr[dt]);
+    for (int dt = 0; dt < ND; ++dt) kt_[dt] = rd_tr<D>(ks + fb.tr[dt]);
 #pragma unroll
-      for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = mma16(kt_, df[qs], acc[dt][qs]);
+    for (int qs = 0; qs < QS; ++qs) {
+      if (idle(qs)) continue;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) acc[dt][qs] = mma16(kt_[dt], df[qs], acc[dt][qs]);
     }
   }
 
