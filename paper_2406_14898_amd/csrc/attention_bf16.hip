@@ -122,6 +122,17 @@ __device__ __forceinline__ bf16x8 pack_p(const f32x4& x, const f32x4& y) {
 }
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
 
+// Sum over the 16 lanes of each row of the wave (lanes 16 g .. 16 g + 15) in
+// a fixed order: an inclusive scan by DPP row shifts of 1, 2, 4 and 8, after
+// which lane 16 g + 15 holds the row's sum.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x111, 0xf, 0xf, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x112, 0xf, 0xf, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x114, 0xf, 0xf, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x118, 0xf, 0xf, true));
+  return v;
+}
+
 __device__ __forceinline__ void bar() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -748,11 +759,11 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
     step(Slot<0>{}, qt);
     if (qt + 1 < nqt) step(Slot<1>{}, qt + 1);
   }
-  if (!kvalid) return;
   const float sc = 1.f / sqrtf((float)D);
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) dk[dt] *= sc;
   if (pre) {
+    if (!kvalid) return;
     // this sequence's share of the prefix gradients, fp32, unrotated
     float* pk_out = a.dprefix_part + ((long)s * a.num_prefix + kj) * H + h * D;
     float* pv_out = pk_out + (long)a.num_seqs * a.num_prefix * H;
@@ -763,17 +774,48 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
     }
     return;
   }
-  rope_back<D>(dk, kj, a.rotary_dim, fg, a.cos_t, a.sin_t);
-  bf16* row = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + kj) * a.ld_dqkv + h * D;
+  if (kvalid) rope_back<D>(dk, kj, a.rotary_dim, fg, a.cos_t, a.sin_t);
+  Vec4<bf16> ok[ND], ov[ND];
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) {
     const float vk[4] = {dk[dt][0], dk[dt][1], dk[dt][2], dk[dt][3]};
     const float vv[4] = {dv[dt][0], dv[dt][1], dv[dt][2], dv[dt][3]};
-    Vec4<bf16> ok, ov;
-    ok.set(vk);
-    ov.set(vv);
-    ok.store(row + H + 16 * dt + 4 * fg);
-    ov.store(row + 2 * H + 16 * dt + 4 * fg);
+    ok[dt].set(vk);
+    ov[dt].set(vv);
+  }
+  if constexpr (DS) {
+    if (a.bias_part) {
+      // column sums of the stored dk and dv rows of this 64-key tile: over
+      // the wave's 16 keys (row16_sum), then the four waves in order
+      // through the (now free) Q tile
+      float* red = reinterpret_cast<float*>(&Qs[0][0]);  // [wave][dk | dv][D]
+      __syncthreads();  // every wave is past its last reads of the tiles
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) {
+        f32x4 sk, sv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sk[e] = row16_sum(kvalid ? ok[dt].get(e) : 0.f);
+          sv[e] = row16_sum(kvalid ? ov[dt].get(e) : 0.f);
+        }
+        if (fr == 15) {
+          st16(red + (w * 2 + 0) * D + 16 * dt + 4 * fg, __builtin_bit_cast(u32x4, sk));
+          st16(red + (w * 2 + 1) * D + 16 * dt + 4 * fg, __builtin_bit_cast(u32x4, sv));
+        }
+      }
+      __syncthreads();
+      for (int c = tid; c < 2 * D; c += 256) {
+        const float t = ((red[c] + red[2 * D + c]) + red[4 * D + c]) + red[6 * D + c];
+        a.bias_part[(long)(a.tile_base[s] + k0 / kRows) * 3 * H + (c < D ? H : 2 * H) + h * D + c % D] = t;
+      }
+    }
+  }
+  if (!kvalid) return;
+  bf16* row = static_cast<bf16*>(a.dqkv) + (long)(si.r0 + kj) * a.ld_dqkv + h * D;
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) {
+    ok[dt].store(row + H + 16 * dt + 4 * fg);
+    ov[dt].store(row + 2 * H + 16 * dt + 4 * fg);
   }
 }
 
@@ -909,6 +951,11 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
   }
 
   const float sc = 1.f / sqrtf((float)D);
+  // column sums of the stored dq rows of this wave's query tile: this
+  // lane's rows in query-group order, then over the 16 lanes (row16_sum)
+  f32x4 bsum[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) bsum[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
     const int qi = qt * kRows + 16 * qs + fr;
@@ -924,34 +971,62 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
       Vec4<bf16> ov;
       ov.set(v);
       ov.store(dq + 16 * dt + 4 * fg);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bsum[dt][e] += ov.get(e);
+    }
+  }
+  if (a.bias_part && qt < nt) {
+    // over the wave's 16 lanes of a column (row16_sum): lane 16 g + 15 holds
+    // columns 16 dt + 4 g .. + 3 of the whole 64-row tile
+    float* out = a.bias_part + (long)(a.tile_base[s] + qt) * 3 * H + h * D;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      f32x4 t;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t[e] = row16_sum(bsum[dt][e]);
+      if (fr == 15) st16(out + 16 * dt + 4 * fg, __builtin_bit_cast(u32x4, t));
     }
   }
 }
 
 // Tile offsets of the stored dS: off[s] = sum over sequences before s of
 // num_heads * ds_seq_tiles, off[S] = the total (one workgroup, chunked scan).
+// With tile_base: tile_base[s] = the 64-row tiles of the sequences before s.
 __global__ void __launch_bounds__(256) ds_offsets_kernel(const int32_t* cu, const int32_t* prefix, int S, int nh,
-                                                         int ntp, int64_t* off) {
-  __shared__ long sh[256];
+                                                         int ntp, int64_t* off, int32_t* tile_base) {
+  __shared__ long sh[2][256];
   const int t = threadIdx.x;
-  long carry = 0;
+  long carry = 0, carry_t = 0;
   for (int s0 = 0; s0 < S; s0 += 256) {
     const int s = s0 + t;
-    long v = 0;
-    if (s < S) v = (long)nh * ds_seq_tiles(cu[s + 1] - cu[s], prefix ? prefix[s] : 0, ntp);
-    sh[t] = v;
+    long v = 0, vt = 0;
+    if (s < S) {
+      const int L = cu[s + 1] - cu[s];
+      v = (long)nh * ds_seq_tiles(L, prefix ? prefix[s] : 0, ntp);
+      vt = (L + kRows - 1) / kRows;
+    }
+    sh[0][t] = v;
+    sh[1][t] = vt;
     __syncthreads();
     for (int o = 1; o < 256; o <<= 1) {
-      const long x = t >= o ? sh[t - o] : 0;
+      const long x = t >= o ? sh[0][t - o] : 0, xt = t >= o ? sh[1][t - o] : 0;
       __syncthreads();
-      sh[t] += x;
+      sh[0][t] += x;
+      sh[1][t] += xt;
       __syncthreads();
     }
-    if (s < S) off[s] = carry + sh[t] - v;
-    carry += sh[255];
+    if (s < S) {
+      off[s] = carry + sh[0][t] - v;
+      if (tile_base) tile_base[s] = (int32_t)(carry_t + sh[1][t] - vt);
+    }
+    carry += sh[0][255];
+    carry_t += sh[1][255];
     __syncthreads();
   }
-  if (t == 0) off[S] = carry;
+  if (t == 0) {
+    off[S] = carry;
+    if (tile_base) tile_base[S] = (int32_t)carry_t;
+  }
 }
 
 template <int D>
@@ -986,7 +1061,7 @@ hipError_t bwd_launch(const AttnDesc& a, hipStream_t st) {
 
 hipError_t attn_ds_offsets(const AttnDesc& a, hipStream_t st) {
   hipLaunchKernelGGL(ds_offsets_kernel, dim3(1), dim3(256), 0, st, a.cu_seqlens, a.prefix_len, a.num_seqs,
-                     a.num_heads, (a.num_prefix + kRows - 1) / kRows, a.ds_off);
+                     a.num_heads, (a.num_prefix + kRows - 1) / kRows, a.ds_off, a.bias_part ? a.tile_base : nullptr);
   return hipGetLastError();
 }
 

@@ -291,6 +291,11 @@ struct Work {
   // per-sequence offsets; null above kAttnDsMaxBytes (dq then recomputes it)
   void* ds;
   int64_t* ds_off;
+  // with ds: b_qkv's column sums per 64-row tile of each sequence, formed by
+  // the attention backward (bias_rows x 3H fp32) and its tile table
+  float* bias_part;
+  int32_t* tile_base;
+  int bias_rows;
 };
 // The stored softmax gradient grows with the sum of squared sequence
 // lengths (about 1.9 GB for 32 heads over 32 sequences of 512 to 2048
@@ -318,12 +323,20 @@ void carve_work(Carver& cv, const fl_stack* st, const BatchInfo& bi, Work* w) {
   w->dprefix = np ? (float*)cv.take(sizeof(float) * 2 * bi.S * np * H) : nullptr;
   w->ds = nullptr;
   w->ds_off = nullptr;
+  w->bias_part = nullptr;
+  w->tile_base = nullptr;
+  w->bias_rows = 0;
   if (st->d.dtype == FL_BF16) {
     const size_t ds_bytes =
         attn_ds_tiles(bi.cu_host, bi.prefix_host, bi.S, st->d.num_heads, st->d.num_prefix) * kAttnDsTileBytes;
     if (ds_bytes <= kAttnDsMaxBytes) {
       w->ds_off = (int64_t*)cv.take(attn_ds_off_bytes(bi.S));
       w->ds = cv.take(ds_bytes);
+      int rows = 0;
+      for (int q = 0; q < bi.S; ++q) rows += (bi.cu_host[q + 1] - bi.cu_host[q] + 63) / 64;
+      w->bias_rows = rows;
+      w->tile_base = (int32_t*)cv.take(sizeof(int32_t) * (bi.S + 1));
+      w->bias_part = (float*)cv.take(sizeof(float) * (size_t)rows * 3 * H);
     }
   }
 }
@@ -646,6 +659,13 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   ad.rotary_dim = st->d.rotary_2d ? 0 : st->d.rotary_dim;
   ad.pk = p.prefix_k; ad.pv = p.prefix_v; ad.num_prefix = st->d.num_prefix; ad.dprefix_part = w.dprefix;
   ad.ds = w.ds; ad.ds_off = w.ds_off;
+  // b_qkv's column sums come from the attention kernels' own tiles (unless
+  // the GLM 2-D rotation changes dq and dk after them)
+  const bool fused_bqkv = train_w && w.ds && w.bias_part && !st->d.rotary_2d;
+  if (fused_bqkv) {
+    ad.bias_part = w.bias_part;
+    ad.tile_base = w.tile_base;
+  }
   const double pairs = bi.pairs + (double)st->d.num_prefix * T;
   LAUNCH(FL_PROF_ATTN_BWD, 8.0 * H * pairs, (double)T * H * E * 8, attn_bwd(dt, ad, s));
   if (st->d.rotary_2d)  // dq and dk rotated back: first half by p1, second by the block position
@@ -660,7 +680,11 @@ int block_backward(fl_stack* st, const BatchInfo& bi, const Plan& plan, const Wo
   }
   // qkv = u W_qkv^T + b_qkv
   if (train_w) {
-    if ((rc = colsum_into(st, dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s))) return rc;
+    if (fused_bqkv)
+      LAUNCH(FL_PROF_COLSUM, 0, 4.0 * w.bias_rows * 3 * H,
+             colsum_finish(w.bias_part, w.bias_rows, 3 * H, gr.b_qkv, s));
+    else if ((rc = colsum_into(st, dt, w.dqkv, 3 * H, T, 3 * H, gr.b_qkv, w, s)))
+      return rc;
     g = GemmDesc();
     g.A = w.dqkv; g.B = a.u; g.C = gr.w_qkv; g.M = 3 * H; g.N = H; g.K = T; g.lda = 3 * H; g.ldb = H; g.ldc = H;
     LAUNCH(FL_PROF_GEMM_TN_ACC, gemm_flops(3 * H, H, T), gemm_bytes(3 * H, H, T, E, 8),

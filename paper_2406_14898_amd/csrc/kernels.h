@@ -153,6 +153,12 @@ struct AttnDesc {
   // recomputes S and dP instead of reading dS.
   void* ds = nullptr;
   int64_t* ds_off = nullptr;
+  // With ds: per 64-row tile of each sequence, the column sums of the stored
+  // dq | dk | dv rows (fp32 [tile rows][3 hidden]; tile rows numbered
+  // sequence after sequence, tile_base (device int32 [S + 1] scratch)
+  // receives each sequence's first); null: not formed.
+  float* bias_part = nullptr;
+  int32_t* tile_base = nullptr;
 };
 // Tiles of stored dS a backward over these (host) sequence bounds needs:
 // per sequence and head, one per (64-query tile, 64-key tile) pair holding a
