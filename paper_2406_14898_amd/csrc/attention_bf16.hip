@@ -586,6 +586,8 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
   const int s = wc.s, h = wc.h, k0 = (pre ? u : u - ntp) * BK;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
   if (!pre && k0 >= si.L) return;
+  // the bias-sum row of this tile, read now rather than at the epilogue
+  const int bias_row = (DS && a.bias_part && !pre) ? a.tile_base[s] + k0 / kRows : 0;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
@@ -806,7 +808,7 @@ __global__ void __launch_bounds__(256, 2) dkdv_kernel(AttnDesc a) {
       __syncthreads();
       for (int c = tid; c < 2 * D; c += 256) {
         const float t = ((red[c] + red[2 * D + c]) + red[4 * D + c]) + red[6 * D + c];
-        a.bias_part[(long)(a.tile_base[s] + k0 / kRows) * 3 * H + (c < D ? H : 2 * H) + h * D + c % D] = t;
+        a.bias_part[(long)bias_row * 3 * H + (c < D ? H : 2 * H) + h * D + c % D] = t;
       }
     }
   }
@@ -849,6 +851,9 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
   const int s = wc.s, h = wc.h, q0 = wc.tile * BM;
   const SeqB si = seqb(a.cu_seqlens, a.prefix_len, s);
   if (q0 >= si.L) return;
+  // the bias-sum row of this workgroup's first query tile, read now rather
+  // than at the epilogue
+  const int bias_row0 = a.bias_part ? a.tile_base[s] + q0 / kRows : 0;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
@@ -978,7 +983,7 @@ __global__ void __launch_bounds__(256, 2) dq_ds_kernel(AttnDesc a) {
   if (a.bias_part && qt < nt) {
     // over the wave's 16 lanes of a column (row16_sum): lane 16 g + 15 holds
     // columns 16 dt + 4 g .. + 3 of the whole 64-row tile
-    float* out = a.bias_part + (long)(a.tile_base[s] + qt) * 3 * H + h * D;
+    float* out = a.bias_part + (long)(bias_row0 + w) * 3 * H + h * D;
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt) {
       f32x4 t;
