@@ -167,7 +167,20 @@ __device__ __forceinline__ void wg_barrier() {
 // Epilogue of one 256 x 256 tile from the wave accumulators acc[i][j]
 // (wave tile rows 128 (wave & 1) + 16 j, columns 64 (wave >> 1) + 16 i), with
 // the LDS at stg (at least 128 KB, free: every wave is past its operand
-// reads) as staging.
+// reads) as staging.  The accumulators of one 128-row half of the tile go to
+// LDS as fp32 ([128][256]); then a lane owns eight consecutive columns
+// (group cg = lane % 32) and the two halves of a wave take alternate rows,
+// so bias, residual, GeLU-input and output rows are read and written
+// contiguously, 16 bytes per lane, two rows per wave instruction (a lane of
+// the matrix core holds 4 columns of 16 different rows, which as direct
+// stores cost more than the reduction for K = 4096; a CU's store
+// instructions cost about the same at 8 and at 16 bytes per lane, so the
+// wide form halves the row loop's memory instructions).  Staging puts
+// 16-byte chunk c of row r at c ^ (r & 15) ^ ((c >> 4) & 1): the row writes
+// of the matrix-core lanes and the 16-lane reads of even (or odd) chunks
+// both hit 16 distinct bank groups.
+__device__ __forceinline__ int stg_swz(int r, int c) { return c ^ (r & 15) ^ ((c >> 4) & 1); }
+
 template <int EPI, int BATCH>
 __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc)[kWTN][kWTM], float* stg, int tm,
                                               int m0, int n0, int tid) {
@@ -175,28 +188,20 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
-  auto barrier = [&]() { wg_barrier(); };
-  // Epilogue, staged through LDS so that every global access is a full row
-  // segment: the accumulators of one 128-row half of the tile go to LDS as
-  // fp32 ([128][256], 16-byte chunk c of row r at c ^ (r & 15)); then each
-  // wave owns whole rows, a lane four consecutive columns, and bias,
-  // residual, GeLU input and output rows are read and written contiguously
-  // (a lane of the matrix core holds 4 columns of 16 different rows, which
-  // as direct stores cost more than the reduction for K = 4096).
-  const int n = n0 + 4 * lane;
-  float bias[4] = {0.f, 0.f, 0.f, 0.f};
-  // EPI_GELU_BWD with colsum: this lane's four columns summed over its rows
-  // (the stored, rounded values), in row order
-  float csum[4] = {0.f, 0.f, 0.f, 0.f};
+  const int sh = lane >> 5, cg = lane & 31;
+  const int n = n0 + 8 * cg;
+  float bias[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  // EPI_GELU_BWD with colsum: this lane's eight columns over its rows (the
+  // stored, rounded values), in row order
+  float csum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) {
-    Vec4<bf16> b;
+    Vec8<bf16> b;
     b.load(p.bias + n);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) bias[e] = b.get(e);
+    for (int e = 0; e < 8; ++e) bias[e] = b.get(e);
   }
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
-    constexpr int kRows = 128 / kWaves;
     const int mbase = m0 + half * 128 + wave;
     if (wm == half) {
 #pragma unroll
@@ -205,22 +210,22 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
 #pragma unroll
         for (int i = 0; i < kWTN; ++i) {
           const int c = (wn * 64 + 16 * i + 4 * fg) >> 2;
-          st16(stg + r * 256 + ((c ^ (r & 15)) << 2), __builtin_bit_cast(u32x4, acc[i][j]));
+          st16(stg + r * 256 + (stg_swz(r, c) << 2), __builtin_bit_cast(u32x4, acc[i][j]));
         }
       }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    barrier();
-    // Rows wave + 8 q, in batches whose global loads (residual, GeLU input,
-    // fp32 accumulator) are issued together before their first use.
-    constexpr int kBatch = BATCH;
+    wg_barrier();
+    // Rows wave + 8 q, q = 2 t + sh (t = 0..7), in batches of row pairs
+    // whose global loads are issued together before their first use.
+    constexpr int kB = BATCH / 2 > 0 ? BATCH / 2 : 1;
 #pragma unroll
-    for (int q0 = 0; q0 < kRows; q0 += kBatch) {
-      Vec4<bf16> ext[kBatch];
-      Vec4<float> cacc[kBatch];
+    for (int t0 = 0; t0 < 8; t0 += kB) {
+      Vec8<bf16> ext[kB];
+      Vec8<float> cacc[kB];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const long m = mbase + (q0 + u) * kWaves;
+      for (int u = 0; u < kB; ++u) {
+        const long m = mbase + (2 * (t0 + u) + sh) * kWaves;
         if (m < p.M) {
           if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) ext[u].load(p.R + m * p.ldr + n);
           if constexpr (EPI == EPI_GELU_BWD) ext[u].load(p.Z + m * p.ldz + n);
@@ -228,39 +233,46 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
         }
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int r = wave + (q0 + u) * kWaves;
-        const long m = mbase + (q0 + u) * kWaves;
+      for (int u = 0; u < kB; ++u) {
+        const int q = 2 * (t0 + u) + sh;
+        const int r = wave + q * kWaves;
+        const long m = mbase + q * kWaves;
         if (m >= p.M) break;
-        const u32x4 raw = ld16(stg + r * 256 + ((lane ^ (r & 15)) << 2));
-        float v[4];
+        const u32x4 raw0 = ld16(stg + r * 256 + (stg_swz(r, 2 * cg) << 2));
+        const u32x4 raw1 = ld16(stg + r * 256 + (stg_swz(r, 2 * cg + 1) << 2));
+        float v[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]) + bias[e];
+        for (int e = 0; e < 4; ++e) {
+          v[e] = __uint_as_float(raw0[e]) + bias[e];
+          v[4 + e] = __uint_as_float(raw1[e]) + bias[4 + e];
+        }
         if constexpr (EPI == EPI_ACC_F32) {
-          float o[4] = {cacc[u].get(0) + v[0], cacc[u].get(1) + v[1], cacc[u].get(2) + v[2], cacc[u].get(3) + v[3]};
+          float o[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = cacc[u].get(e) + v[e];
           cacc[u].set(o);
           cacc[u].store(static_cast<float*>(p.C) + m * p.ldc + n);
         } else {
           if constexpr (EPI == EPI_BIAS_RES || EPI == EPI_RES) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += p.res_scale * ext[u].get(e);
+            for (int e = 0; e < 8; ++e) v[e] += p.res_scale * ext[u].get(e);
           }
           if constexpr (EPI == EPI_GELU_BWD) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] *= gelu2_grad(ext[u].get(e));
+            for (int e = 0; e < 8; ++e) v[e] *= gelu2_grad(ext[u].get(e));
           }
-        Vec4<bf16> o;
+          Vec8<bf16> o;
           o.set(v);
           if (EPI != EPI_BIAS_GELU || p.C) o.store(static_cast<bf16*>(p.C) + m * p.ldc + n);
           if constexpr (EPI == EPI_GELU_BWD) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) csum[e] += o.get(e);
+            for (int e = 0; e < 8; ++e) csum[e] += o.get(e);
           }
           if constexpr (EPI == EPI_BIAS_GELU) {
-            float g[4];
+            float g[8];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) g[e] = gelu2(v[e]);
-            Vec4<bf16> og;
+            for (int e = 0; e < 8; ++e) g[e] = gelu2(v[e]);
+            Vec8<bf16> og;
             og.set(g);
             og.store(p.C2 + m * p.ldc2 + n);
           }
@@ -269,24 +281,26 @@ __device__ __forceinline__ void tile_epilogue(const G2Args& p, const f32x4 (&acc
     }
     // the second half, or the next tile's loads, overwrite the staging area
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    barrier();
+    wg_barrier();
   }
   if constexpr (EPI == EPI_GELU_BWD) {
     if (p.colsum) {
-      // the eight waves' partial column sums, added in wave order (the
-      // operand tiles are free: every wave has passed the barrier above)
+      // the sixteen half-waves' partial column sums, added in (wave, half)
+      // order (the operand tiles are free: every wave passed the barrier)
       float* cs = stg;
-      st16(cs + wave * kBN + 4 * lane, __builtin_bit_cast(u32x4, f32x4{csum[0], csum[1], csum[2], csum[3]}));
+      float* mine = cs + (wave * 2 + sh) * kBN + 8 * cg;
+      st16(mine, __builtin_bit_cast(u32x4, f32x4{csum[0], csum[1], csum[2], csum[3]}));
+      st16(mine + 4, __builtin_bit_cast(u32x4, f32x4{csum[4], csum[5], csum[6], csum[7]}));
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();
+      wg_barrier();
       if (tid < kBN) {
         float t = 0.f;
 #pragma unroll
-        for (int w2 = 0; w2 < kWaves; ++w2) t += cs[w2 * kBN + tid];
+        for (int w2 = 0; w2 < 2 * kWaves; ++w2) t += cs[w2 * kBN + tid];
         p.colsum[(long)tm * p.N + n0 + tid] = t;
       }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier();  // the next tile's loads overwrite cs
+      wg_barrier();  // the next tile's loads overwrite cs
     }
   }
 }
