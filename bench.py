@@ -10,9 +10,10 @@ seeded synthetic draws with the workload's shapes and distributions.
 
 Prints one JSON line: tokens/s of the whole step, the fraction of the bf16
 matrix-core peak it reaches, a per-kernel-class breakdown (HIP events around
-every launch during the timed steps), the roofline entry of the dominant
-kernel class, and the CPU oracle timed on a bounded sample of the same
-workload on this host's cores.
+every launch of one untimed step after the warmup), the roofline entry of the
+dominant kernel class (its launches timed with events during the timed
+steps, the only ones that carry events there), and the CPU oracle timed on a
+bounded sample of the same workload on this host's cores.
 """
 
 from __future__ import annotations
@@ -353,6 +354,19 @@ def total_layers(w: synth.Workload) -> int:
     return w.shape.num_layers + (2 if w.vocab else 0)
 
 
+# Stored softmax-gradient cap of the engine's backward (above it, dq
+# recomputes S and dP).
+ATTN_DS_MAX_BYTES = 8 << 30
+
+
+def attn_ds_stored(w, b, F):
+    """Whether the engine's attention backward stores dS for this batch."""
+    if not w.backward or w.dtype != "bf16":
+        return False
+    prefix = b.prefix_len if w.mask == "prefix" else None
+    return F.fl_test_attention_ds_bytes(b.cu_seqlens, prefix, w.shape.num_heads, w.num_prefix) <= ATTN_DS_MAX_BYTES
+
+
 def vocab_padded(w: synth.Workload) -> int:
     return (w.vocab + 255) // 256 * 256
 
@@ -612,8 +626,9 @@ SECONDARY_WORKLOADS = (
 
 def secondary_run(name: str, seed: int, steps: int, warmup: int) -> dict:
     """A short timed run of another server-stack workload (same device
-    draws, launch timing on): tokens/s, ms per step, algorithmic MFMA
-    utilisation and the GEMMs' MFMA utilisation."""
+    draws): tokens/s, ms per step, algorithmic MFMA utilisation and the
+    GEMMs' MFMA utilisation (their launch times from one more, untimed step
+    with launch timing on)."""
     import torch
 
     from paper_2406_14898_amd import BatchDesc, ServerStack
@@ -639,7 +654,13 @@ def secondary_run(name: str, seed: int, steps: int, warmup: int) -> dict:
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
+    # launch timing in one untimed step (the GEMM classes' times), then the
+    # timed steps without events
     F.fl_stack_profile(ss.handle, 1)
+    step()
+    torch.cuda.synchronize()
+    prof = F.profile_table(ss.handle)
+    F.fl_stack_profile(ss.handle, 0)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(steps):
@@ -647,8 +668,6 @@ def secondary_run(name: str, seed: int, steps: int, warmup: int) -> dict:
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    prof = F.profile_table(ss.handle)
-    F.fl_stack_profile(ss.handle, 0)
     ss.close()
     del inp, params, grads, x, dy, y, dx, saved, ws
     torch.cuda.empty_cache()
@@ -775,8 +794,8 @@ def main() -> int:
 
     upd_events = []
 
-    def step(timed=True):
-        fwd_bwd(timed)
+    def step(marks=False):
+        fwd_bwd(marks)
         if arena is not None:
             e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             e[0].record(stream)
@@ -784,13 +803,54 @@ def main() -> int:
             e[1].record(stream)
             upd_events.append(e)
 
+    def collect():
+        table = {}
+        for h in handles:
+            for k, r in F.profile_table(h).items():
+                e = table.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+                for f in e:
+                    e[f] += r[f]
+        return table
+
     for i in range(args.warmup):
-        step(timed=False)
+        step()
         torch.cuda.synchronize()
         print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    # Per-class breakdown from one more (untimed) step with every launch
+    # between two events; the timed steps then bracket only the dominant
+    # class, whose live launch times give roofline.achieved (two events per
+    # launch cost 0.3-0.5 % of a step when every launch carries them).
+    prof, prof_steps, dom_mask = {}, 0, 0
+    if not args.no_profile:
+        for h in handles:
+            F.fl_stack_profile(h, True)
+        client_marks.clear()
+        step(marks=True)
+        torch.cuda.synchronize()
+        prof, prof_steps = collect(), 1
+        for h in handles:
+            F.fl_stack_profile(h, False)
+        if w.vocab:
+            # client-side calls timed with events on the same stream
+            H, Vp = sh.hidden, vocab_padded(w)
+            work = {"lm_head_fwd": (2.0 * T * Vp * H, 0.0),
+                    "lm_head_bwd": ((2.0 if w.frozen else 4.0) * T * Vp * H, 0.0),
+                    "embedding_fwd": (0.0, 2.0 * T * H * (2 if w.dtype == "bf16" else 4)),
+                    "embedding_bwd": (0.0, T * H * ((2 if w.dtype == "bf16" else 4) + 8.0))}
+            for name, a, e in client_marks:
+                r = prof.setdefault(name, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+                r["launches"] += 1
+                r["ms"] += a.elapsed_time(e)
+                r["flops"] += work[name][0]
+                r["bytes"] += work[name][1]
+        engine_classes = {F.fl_profile_class_name(c): c for c in range(F.FL_PROF_NUM_CLASSES)}
+        dom_engine = max((k for k in prof if k in engine_classes), key=lambda k: prof[k]["ms"], default=None)
+        if dom_engine is not None:
+            dom_mask = 1 << engine_classes[dom_engine]
+        print(f"[bench] breakdown step done; timing {dom_engine} live", file=sys.stderr, flush=True)
     upd_events.clear()
     for h in handles:
-        F.fl_stack_profile(h, not args.no_profile)
+        F.fl_stack_profile_classes(h, dom_mask)
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     clock = ClockSampler(sclk_path()).start()
@@ -802,26 +862,9 @@ def main() -> int:
     sclk = clock.stop()
     ms = marks[0].elapsed_time(marks[-1]) / args.steps
     per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
-    prof = {}
+    live = collect() if dom_mask else {}
     for h in handles:
-        for k, r in F.profile_table(h).items():
-            e = prof.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
-            for f in e:
-                e[f] += r[f]
         F.fl_stack_profile(h, False)
-    if w.vocab and not args.no_profile:
-        # client-side calls timed with events on the same stream
-        H, Vp = sh.hidden, vocab_padded(w)
-        work = {"lm_head_fwd": (2.0 * T * Vp * H, 0.0),
-                "lm_head_bwd": ((2.0 if w.frozen else 4.0) * T * Vp * H, 0.0),
-                "embedding_fwd": (0.0, 2.0 * T * H * (2 if w.dtype == "bf16" else 4)),
-                "embedding_bwd": (0.0, T * H * ((2 if w.dtype == "bf16" else 4) + 8.0))}
-        for name, a, e in client_marks:
-            r = prof.setdefault(name, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
-            r["launches"] += 1
-            r["ms"] += a.elapsed_time(e)
-            r["flops"] += work[name][0]
-            r["bytes"] += work[name][1]
     print(f"[bench] timed {args.steps} steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
 
     flops = algorithmic_flops(w, b)
@@ -830,7 +873,7 @@ def main() -> int:
     kernels = {}
     for name, r in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
         per_ms = r["ms"] / r["launches"]
-        ent = {"launches": r["launches"], "ms_per_step": round(r["ms"] / args.steps, 3),
+        ent = {"launches": r["launches"], "ms_per_step": round(r["ms"] / prof_steps, 3),
                "avg_launch_us": round(per_ms * 1e3, 2)}
         if r["flops"] > 0:
             ent["tflops"] = round(r["flops"] / (r["ms"] / 1e3) / 1e12, 1)
@@ -838,15 +881,20 @@ def main() -> int:
             ent["gbs"] = round(r["bytes"] / (r["ms"] / 1e3) / 1e9, 1)
         kernels[name] = ent
     # hardware flops: every launch's own count (forward recompute launches
-    # included); the attention backward also recomputes S and dP twice (dk/dv
-    # and dq kernels): 14 H per pair against the 8 H counted as algorithmic
-    hw_flops = sum(r["flops"] * (14.0 / 8.0 if k == "attn_bwd" else 1.0) for k, r in prof.items()) / args.steps
+    # included); the attention backward computes S and dP once and dq from the
+    # stored dS (10 H per pair against the 8 H counted as algorithmic), or,
+    # when that store would pass its cap, recomputes S and dP for dq (14 H)
+    attn_hw = 10.0 / 8.0 if attn_ds_stored(w, b, F) else 14.0 / 8.0
+    hw_flops = (sum(r["flops"] * (attn_hw if k == "attn_bwd" else 1.0) for k, r in prof.items()) / prof_steps
+                if prof_steps else 0.0)
     gemm_ms = sum(prof[k]["ms"] for k in GEMM_CLASSES if k in prof)
     gemm_fl = sum(prof[k]["flops"] for k in GEMM_CLASSES if k in prof)
     roofline = None
     if prof:
-        dom = max(prof, key=lambda k: prof[k]["ms"])
-        r = prof[dom]
+        # the dominant class of the breakdown step, with its launches timed live
+        # during the timed steps
+        dom = max(live, key=lambda k: live[k]["ms"]) if live else max(prof, key=lambda k: prof[k]["ms"])
+        r = live.get(dom, prof[dom])
         avg_s = r["ms"] / r["launches"] / 1e3
         if dom in MFMA_CLASSES:
             ach = r["flops"] / r["launches"] / avg_s / 1e12

@@ -352,6 +352,10 @@ int fl_average_replicas(int32_t num_replicas, float* const* params, void* const*
 #define FL_PROF_PREFIX_GRAD 13      /* P-tuning v2 prefix gradients: sum over sequences */
 #define FL_PROF_NUM_CLASSES 14
 int fl_stack_profile(fl_stack* stack, int enable);
+/* The same for a subset of the classes: bit c of class_mask times the
+ * launches of class c (the others run without events); 0 turns timing off.
+ * fl_stack_profile(stack, 1) times every class. */
+int fl_stack_profile_classes(fl_stack* stack, uint32_t class_mask);
 /* Totals for one class over the records since profiling was enabled:
  * launch count, summed event time (ms), algorithmic flops and bytes.
  * Waits for the recorded events. */

@@ -83,7 +83,7 @@ struct fl_stack {
     hipEvent_t a, b;
     double flops, bytes;
   };
-  bool prof = false;
+  uint32_t prof_mask = 0;  // bit c: launches of class c are timed
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
 };
@@ -108,7 +108,7 @@ hipError_t take_event(fl_stack* st, hipEvent_t* e) {
 // with two events on stream s and records the launch's algorithmic work.
 template <class Fn>
 hipError_t timed(fl_stack* st, hipStream_t s, int cls, double flops, double bytes, Fn&& launch) {
-  if (!st->prof) return launch();
+  if (!((st->prof_mask >> cls) & 1u)) return launch();
   fl_stack::Rec r{cls, nullptr, nullptr, flops, bytes};
   hipError_t e = take_event(st, &r.a);
   if (e != hipSuccess) return e;
@@ -758,8 +758,8 @@ int scratch_base(void** out) {
 struct ProfOff {
   fl_stack* st;
   bool was;
-  explicit ProfOff(fl_stack* s) : st(s), was(s->prof) { st->prof = false; }
-  ~ProfOff() { st->prof = was; }
+  explicit ProfOff(fl_stack* s) : st(s), was(s->prof_mask) { st->prof_mask = 0; }
+  ~ProfOff() { st->prof_mask = was; }
 };
 
 }  // namespace
@@ -803,17 +803,22 @@ int fl_stack_destroy(fl_stack* st) {
   return FL_OK;
 }
 
-int fl_stack_profile(fl_stack* st, int enable) {
+int fl_stack_profile_classes(fl_stack* st, uint32_t class_mask) {
   if (!st) return fail(FL_ERR_NULL, "stack is NULL");
-  if (enable) {
+  class_mask &= (1u << FL_PROF_NUM_CLASSES) - 1u;
+  if (class_mask) {
     for (auto& r : st->recs) {
       st->pool.push_back(r.a);
       st->pool.push_back(r.b);
     }
     st->recs.clear();
   }
-  st->prof = enable != 0;
+  st->prof_mask = class_mask;
   return FL_OK;
+}
+
+int fl_stack_profile(fl_stack* st, int enable) {
+  return fl_stack_profile_classes(st, enable ? (1u << FL_PROF_NUM_CLASSES) - 1u : 0u);
 }
 
 int fl_stack_profile_read(fl_stack* st, int cls, int64_t* launches, double* ms, double* flops, double* bytes) {

@@ -41,7 +41,7 @@ EXPORTS = (
     "fl_adam_step", "fl_average_replicas",
     "fl_client_create", "fl_client_destroy", "fl_client_workspace_bytes", "fl_embedding_forward",
     "fl_embedding_backward", "fl_lm_head_forward", "fl_lm_head_backward",
-    "fl_stack_profile", "fl_stack_profile_read", "fl_profile_class_name",
+    "fl_stack_profile", "fl_stack_profile_classes", "fl_stack_profile_read", "fl_profile_class_name",
     "fl_test_gemm", "fl_test_layernorm_fwd", "fl_test_layernorm_bwd", "fl_test_layernorm_bwd_fused",
     "fl_test_colsum",
     "fl_test_rope", "fl_test_attention_fwd", "fl_test_attention_bwd", "fl_test_attention_ds_bytes",
@@ -119,6 +119,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "fl_lm_head_forward": [vp, vp, vp, vp, vp, P(i32), i64, vp, vp, vp, sz, vp],
         "fl_lm_head_backward": [vp, vp, vp, vp, i64, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp],
         "fl_stack_profile": [vp, ctypes.c_int],
+        "fl_stack_profile_classes": [vp, ctypes.c_uint32],
         "fl_stack_profile_read": [vp, ctypes.c_int, P(i64), P(ctypes.c_double), P(ctypes.c_double),
                                   P(ctypes.c_double)],
         "fl_test_gemm": [ctypes.c_int] * 3 + [vp] * 3 + [ctypes.c_int] * 3 + [i64] * 3 + [vp, vp, i64, vp, i64, vp,
@@ -362,6 +363,11 @@ def fl_lm_head_backward(handle: int, h, w, T: int, grad_scale: float, dh, dw, wo
 
 def fl_stack_profile(handle: int, enable: bool) -> None:
     _check(load().fl_stack_profile(handle, int(enable)))
+
+
+def fl_stack_profile_classes(handle: int, class_mask: int) -> None:
+    """Time only the launches of the classes whose bits are set (0: off)."""
+    _check(load().fl_stack_profile_classes(handle, int(class_mask) & 0xffffffff))
 
 
 def fl_profile_class_name(cls: int) -> str:

@@ -320,3 +320,29 @@ def test_launch_profile_accounts_every_launch():
     attn = sum(r["flops"] for k, r in prof.items() if k.startswith("attn"))
     assert gemm == pytest.approx(alg["gemm"], rel=1e-9)
     assert attn == pytest.approx(alg["attention"], rel=1e-9)
+
+
+def test_launch_profile_of_chosen_classes():
+    """Timing a subset of the classes (the benchmark's timed steps time only
+    the dominant one): launches of the other classes carry no record, the
+    chosen class's count equals a full profile's, and a zero mask turns
+    timing off."""
+    b = synth.make_batch(2, 2, (30, 170), "causal", seed=15)
+    layers, x, dy = _inputs(b, "bf16", seed=15)
+    g = GpuStack(SHAPE, layers, "bf16")
+    names = {F.fl_profile_class_name(c): c for c in range(F.FL_PROF_NUM_CLASSES)}
+    F.fl_stack_profile(g.ss.handle, True)
+    g.run(b, x, dy)
+    full = F.profile_table(g.ss.handle)
+    mask = (1 << names["gemm_tn_acc"]) | (1 << names["attn_fwd"])
+    F.fl_stack_profile_classes(g.ss.handle, mask)
+    g.run(b, x, dy)
+    some = F.profile_table(g.ss.handle)
+    F.fl_stack_profile_classes(g.ss.handle, 0)
+    g.run(b, x, dy)
+    none = F.profile_table(g.ss.handle)
+    g.close()
+    assert set(some) == {"gemm_tn_acc", "attn_fwd"}
+    assert all(some[k]["launches"] == full[k]["launches"] and some[k]["ms"] > 0 for k in some)
+    # records stay until the next enabling call; disabling adds none
+    assert none == some
