@@ -36,7 +36,9 @@ namespace {
 constexpr int kBM = 256, kBN = 256, kBK = 64, kStages = 2, kThr = 512, kWaves = 8;
 // waves: 2 along M x 4 along N, each 128 x 64 (8 x 4 tiles of 16 x 16)
 constexpr int kWTM = 8, kWTN = 4;
-constexpr int kTileElems = 256 * kBK;  // one operand tile per stage (32 KB)
+// LDS region of one operand tile: the MN-contiguous layout pads each 1 KB
+// DMA block to 1056 bytes (33 KB in all)
+constexpr int kRegionElems = 16896, kMBlock = 528, kMCol = 8 * kMBlock, kKBlock = 520;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
@@ -66,17 +68,6 @@ struct G2Args {
   float* colsum;
 };
 
-// K-contiguous tile: row r holds 8 chunks of 8; chunk q of row r sits at
-// slot q ^ swz_k(r).  With this swizzle the fragment reads (16 consecutive
-// rows, one chunk each) are free of LDS bank conflicts on gfx950 (measured
-// with SQ_LDS_BANK_CONFLICT; (r ^ (r >> 3)) & 7, for instance, doubles the
-// read time).
-__device__ __forceinline__ int swz_k(int row) { return row & 7; }
-// MN-contiguous blocks: k-row k holds 8 chunks; chunk q sits at q ^ swz_m(k).
-// A transpose read serves 32 lanes per cycle: k-rows kb .. kb+3 and
-// kb+8 .. kb+11, 32 bytes each; k bits 1 and 3 move those eight segments
-// onto disjoint banks.
-__device__ __forceinline__ int swz_m(int k) { return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2); }
 
 __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_inst_base, uint32_t voff) {
   dma_lds<16>(rs, lds_inst_base, voff);
@@ -84,45 +75,59 @@ __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_inst_base, uint32_t
 
 // Per-lane source byte offsets (reduction index 0) of DMA instruction inst
 // (0..31) of an operand tile.
-// K-contiguous tile [256 rows][64]: instruction inst fills rows 8 inst ..
-// 8 inst + 7, 128 bytes each.
+// K-contiguous tile [256 rows][64]: 32 DMA blocks of 8 rows of 128 bytes at a
+// stride of 1040 bytes, every row read in address order (as below).  Row
+// r = 16 q + t sits in block b = (t & 7) + 8 (q >> 2), row 2 (q & 3) + (t >> 3):
+// the 16 rows that one 16-lane fragment read touches (one 16-row group q)
+// sit in 8 blocks (16-byte shifts 16 b) at two row parities, i.e. on 16
+// distinct bank groups.  Instruction inst fills block inst.
 __device__ __forceinline__ uint32_t k_src(long ld, int inst, int lane) {
-  const int lin = inst * 64 + lane;
-  const int row = lin >> 3, q = (lin & 7) ^ swz_k(row);
-  return (uint32_t)(row * ld + q * 8) * 2u;
+  const int slot = lane >> 3;
+  const int row = 16 * (4 * (inst >> 3) + (slot >> 1)) + (inst & 7) + 8 * (slot & 1);
+  return (uint32_t)(row * ld + (lane & 7) * 8) * 2u;
 }
-// MN-contiguous tile: 4 column blocks of [64 k][64 columns] (8 KB each);
-// instruction inst fills k-rows 8 (inst % 8) .. + 7 of block inst / 8.
+// MN-contiguous tile: 4 column blocks of 64 columns (kMCol elements each),
+// each 8 DMA blocks b of 8 k-rows of 128 bytes, at a stride of 1056 bytes.
+// Every k-row is one DMA row segment read in address order: the texture
+// addresser handles a permuted segment several times slower (counted as
+// SQ_VMEM_TA_ADDR_FIFO_FULL), so bank spreading comes from where whole rows
+// go instead of a swizzle inside them.  k-row k (k = c + 4 s0 + 8 p + 16 s1 +
+// 32 h, each digit a bit) sits in block b = c + 4 h, row r = p + 2 s0 + 4 s1.
+// A transpose read serves 32 lanes per cycle: k-rows kb .. kb+3 and
+// kb+8 .. kb+11 (kb = 0, 4, 16, 20, + 32), 32 bytes each; these sit in four
+// blocks (32-byte shifts 32 b) at two row parities: eight distinct bank
+// groups.  Instruction inst fills block inst % 8 of column block inst / 8.
 __device__ __forceinline__ uint32_t m_src(long ld, int inst, int lane) {
-  const int blk = inst >> 3, krow = (inst & 7) * 8 + (lane >> 3);
-  const int q = (lane & 7) ^ swz_m(krow);
-  return (uint32_t)((long)krow * ld + blk * 64 + q * 8) * 2u;
+  const int blk = inst >> 3, b = inst & 7;
+  const int krow = (b & 3) + 4 * ((lane >> 4) & 1) + 8 * ((lane >> 3) & 1) + 16 * (lane >> 5) + 32 * (b >> 2);
+  return (uint32_t)((long)krow * ld + blk * 64 + (lane & 7) * 8) * 2u;
 }
+// LDS byte offset, inside an operand region, of DMA instruction inst
+__device__ __forceinline__ uint32_t k_dst(int inst) { return (uint32_t)inst * (2u * kKBlock); }
+__device__ __forceinline__ uint32_t m_dst(int inst) { return (uint32_t)((inst >> 3) * kMCol + (inst & 7) * kMBlock) * 2u; }
 
 // Per-lane fragment bases (element offsets inside one operand tile).
-// K-contiguous: fragment j of a wave (rows row0 + 16 j), reduction half c =
-// base(c) + 1024 j, base(1) = base(0) ^ 32.
+// K-contiguous: fragment j of a wave (rows row0 + 16 j, row0 a multiple of
+// 64), reduction half c: lane (fr, fg) reads chunk fg + 4 c of row
+// row0 + 16 j + fr.
 __device__ __forceinline__ int frag_k_base(int row0, int fr, int fg) {
-  const int row = row0 + fr;
-  return row * 64 + ((fg ^ swz_k(row)) * 8);
+  return (fr & 7) * kKBlock + 64 * (fr >> 3) + 8 * fg + 8 * kKBlock * (row0 >> 6);
 }
-// MN-contiguous: fragment j (columns col0 + 16 j), reduction half c: the
-// 16-column group j % 4 of block col0/64 + j/4 sits at chunk pair
-// 2 (j % 4) ^ swz_m(k); k = 32 c + 8 g + s/4 (+ 4 for the second read).  The
-// per-lane base holds the swizzled pair for j % 4 == 0; other groups XOR it.
+// MN-contiguous: fragment j (columns col0 + 16 j), reduction half c: lane s
+// of a 16-lane group points at k-row 8 g + s / 4 (block s / 4, row
+// (g & 1) + 4 (g >> 1)), columns 4 (s % 4) of group j % 4 of column block
+// col0 / 64 + j / 4; the second read is k + 4 (row + 2), half c = k + 32
+// (block + 4).
 __device__ __forceinline__ int frag_m_base(int col0, int fr, int fg) {
-  const int k = 8 * fg + (fr >> 2);
-  const int chunk = ((fr & 3) >> 1) ^ swz_m(k);
-  return (col0 >> 6) * 4096 + k * 64 + chunk * 8 + 4 * (fr & 1);
+  return (col0 >> 6) * kMCol + (fr >> 2) * kMBlock + ((fg & 1) + 4 * (fg >> 1)) * 64 + 4 * (fr & 3);
 }
 __device__ __forceinline__ bf16x8 frag_k(const bf16* tile, int base, int c, int j) {
-  return __builtin_bit_cast(bf16x8, ld16(tile + (base ^ (32 * c)) + 1024 * j));
+  return __builtin_bit_cast(bf16x8, ld16(tile + base + 8 * kKBlock * (j >> 2) + 128 * (j & 3) + 32 * c));
 }
 __device__ __forceinline__ bf16x8 frag_m(const bf16* tile, int base, int c, int j) {
-  // column group j % 4 -> chunk-pair XOR 2 (j % 4) (16 elements per pair)
-  const bf16* p = tile + (base ^ (16 * (j & 3))) + 4096 * (j >> 2) + 2048 * c;
+  const bf16* p = tile + base + 16 * (j & 3) + kMCol * (j >> 2) + 4 * kMBlock * c;
   i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p));
-  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 256));
+  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(p + 128));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
@@ -314,7 +319,7 @@ constexpr int epi_batch() { return (EPI == EPI_BIAS_RES || EPI == EPI_RES) ? 16 
 
 template <bool AK, bool BKc, int EPI, int BATCH = epi_batch<EPI>()>
 __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
-  __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kTileElems];  // [stage][A/B]
+  __shared__ __attribute__((aligned(1024))) bf16 smem[kStages][2][kRegionElems];  // [stage][A/B]
 
   const int tiles_m = (p.M + kBM - 1) / kBM, tiles_n = p.N / kBN;
   const int ntiles = tiles_m * tiles_n;
@@ -367,11 +372,13 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   } else {
     rb = buf_rsrc(p.B + n0, (uint32_t)(((long)p.nb * p.ldb - n0) * 2));
   }
-  // DMA bookkeeping.  Instruction i (0..3) of this wave fills 1 KB of an
-  // operand tile at byte (8 i + wave) * 1024; its per-lane source offset is
-  // fixed up to the stage's reduction offset, added per stage.
+  // DMA bookkeeping.  Instruction i (0..3) of this wave is instruction
+  // 8 i + wave of an operand tile (k_dst / m_dst); its per-lane source offset
+  // is fixed up to the stage's reduction offset, added per stage.
   const uint32_t lds0 = FL_LDS_ADDR(&smem[0][0][0]);
-  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + wave * 1024);
+  const uint32_t lds_a = __builtin_amdgcn_readfirstlane(lds0 + (AK ? k_dst(wave) : m_dst(wave)));
+  const uint32_t lds_b =
+      __builtin_amdgcn_readfirstlane(lds0 + kRegionElems * 2 + (BKc ? k_dst(wave) : m_dst(wave)));
   uint32_t voa[4], vob[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -383,11 +390,11 @@ __global__ void __launch_bounds__(kThr) gemm_bf16_kernel(G2Args p) {
   auto kstep_b = [&](int k0) { return BKc ? (uint32_t)k0 * 2u : (uint32_t)((long)k0 * p.ldb * 2); };
   // DMA instruction g (0..7: A 0..3, B 0..3) of stage kt
   auto dma_one = [&](int kt, int g) {
-    const uint32_t slot_off = (uint32_t)(kt & (kStages - 1)) * (2 * kTileElems * 2);
+    const uint32_t slot_off = (uint32_t)(kt & (kStages - 1)) * (2 * kRegionElems * 2);
     if (g < 4)
-      dma16(ra, lds_wave + slot_off + g * 8192, voa[g] + kstep_a(kt * kBK));
+      dma16(ra, lds_a + slot_off + (AK ? k_dst(8 * g) : m_dst(8 * g)), voa[g] + kstep_a(kt * kBK));
     else
-      dma16(rb, lds_wave + slot_off + kTileElems * 2 + (g - 4) * 8192, vob[g - 4] + kstep_b(kt * kBK));
+      dma16(rb, lds_b + slot_off + (BKc ? k_dst(8 * (g - 4)) : m_dst(8 * (g - 4))), vob[g - 4] + kstep_b(kt * kBK));
   };
   auto issue = [&](int kt) {
 #pragma unroll
