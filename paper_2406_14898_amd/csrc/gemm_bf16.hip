@@ -4,23 +4,23 @@
 // path:
 //   * 256 x 256 output tile per workgroup, 8 waves (two per SIMD, so one
 //     wave's LDS waits are covered by the other's matrix-core work) of
-//     128 x 64, reduction stages of 64 double-buffered in LDS (128 KB): a
+//     128 x 64, reduction stages of 64 double-buffered in LDS (132 KB): a
 //     DMA row segment is one full 128-byte line;
 //   * operands go from HBM/L2 straight into LDS with buffer loads in LDS-DMA
 //     mode (no VGPR staging).  Buffer resources bound each operand, so rows
 //     or reduction indices past the end read as zero (ragged token tails);
-//   * each operand stays in LDS in (blocks of) its global layout.
-//     K-contiguous tiles are [256 rows][64] and feed the matrix core with
-//     16-byte reads; MN-contiguous tiles are 4 column blocks of [64 k][64] and
-//     feed it with transpose reads (ds_read_b64_tr_b16: lane j of a 16-lane
-//     group receives four consecutive-k values of column j when lane s points
-//     at (k0 + s/4, c0 + 4 (s % 4)));
-//   * layouts are chosen so that every fragment address is one per-lane base
-//     plus a compile-time offset (the swizzle of K-contiguous rows depends on
-//     the lane only), which keeps the address arithmetic out of the VGPR
-//     budget;
-//   * an LDS-DMA lane always writes to base + 16 * lane, so swizzles are
-//     applied to the source addresses;
+//   * each operand tile is a set of 1 KB DMA blocks of 8 rows (K-contiguous:
+//     rows of 64 reduction indices, read by 16-byte fragment reads;
+//     MN-contiguous: k-rows of 64 columns, read by transpose reads
+//     (ds_read_b64_tr_b16: lane j of a 16-lane group receives four
+//     consecutive-k values of column j when lane s points at
+//     (k0 + s/4, c0 + 4 (s % 4)))).  Rows keep their global order inside;
+//     which rows share a block, and the blocks' 16- or 32-byte offsets in
+//     the bank map, keep the fragment reads free of bank conflicts;
+//   * every fragment address is one per-lane base plus a compile-time
+//     offset, which keeps the address arithmetic out of the VGPR budget;
+//   * an LDS-DMA lane always writes to base + 16 * lane, so the placement is
+//     chosen through the source addresses;
 //   * one barrier per stage, placed between the two 32-wide halves: the
 //     second half's fragments are already in registers when the barrier
 //     releases the slot, so the next stage's loads and fragment reads overlap
