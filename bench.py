@@ -41,7 +41,8 @@ MFMA_CLASSES = ("gemm_nt_bias", "gemm_nt_bias_res", "gemm_nt_bias_gelu", "gemm_t
 GEMM_CLASSES = MFMA_CLASSES[:6]   # the block GEMMs
 # Fragments of the kernel names rocprofv3 prints for each launch class of the
 # bf16 path (a class may launch several kernels), and the sources they are
-# built from (a stored counter reading is stale once these change).
+# built from (a stored counter reading is stale once their code, comments
+# aside, changes).
 CLASS_KERNELS = {
     # (the epilogue's row-batch template argument follows the epilogue code)
     "gemm_nt_bias": ("gemm_bf16_kernel<true, true, 1,",),
@@ -83,13 +84,30 @@ PAPER_CONTEXT = {
 }
 
 
+# String literals (kept: inline assembly lives in them), then // and /* */
+# comments (dropped), for hashing the code the compiler sees.
+_C_TOKENS = None
+
+
+def code_text(src: str) -> str:
+    """C/C++ source with comments removed and every run of whitespace made one
+    space, so that editing a comment leaves the hash of the code unchanged."""
+    import re
+    global _C_TOKENS
+    if _C_TOKENS is None:
+        _C_TOKENS = re.compile(r'"(?:\\.|[^"\\\n])*"|//[^\n]*|/\*.*?\*/', re.S)
+    kept = _C_TOKENS.sub(lambda m: m.group(0) if m.group(0).startswith('"') else " ", src)
+    return " ".join(kept.split())
+
+
 def class_source_hash(cls: str) -> str:
     import hashlib
     files = next(v for k, v in CLASS_SOURCES.items() if cls.startswith(k))
     h = hashlib.sha256()
     for f in files:
-        with open(os.path.join(CSRC, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
+            h.update(code_text(fh.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()[:16]
 
 

@@ -127,6 +127,26 @@ def test_committed_traffic_goes_stale_with_the_sources(tmp_path, monkeypatch):
     assert bench.committed_traffic("layernorm_fwd", "w") is None  # not measured
 
 
+def test_source_hash_ignores_comments_but_not_code(tmp_path, monkeypatch):
+    base = ('#pragma once\n// a kernel\n__global__ void k(float* p) { /* one */ p[0] = 1.0f; }\n'
+            'asm volatile("s_nop 0 // kept: inside a string" ::: "memory");\n')
+    variants = {
+        "same": base.replace("// a kernel", "// the kernel, reworded").replace("/* one */", "/* two\n lines */"),
+        "code": base.replace("1.0f", "2.0f"),
+        "asm": base.replace("s_nop 0 //", "s_nop 1 //"),
+    }
+    monkeypatch.setattr(bench, "CSRC", str(tmp_path))
+    monkeypatch.setattr(bench, "CLASS_SOURCES", {"": ("k.hip",)})
+
+    def h(text):
+        (tmp_path / "k.hip").write_text(text)
+        return bench.class_source_hash("anything")
+    h0 = h(base)
+    assert h(variants["same"]) == h0
+    assert h(variants["code"]) != h0
+    assert h(variants["asm"]) != h0     # a string literal is code, even with // inside
+
+
 @pytest.mark.parametrize("text,mhz", [("0: 500Mhz\n1: 1938Mhz *\n2: 2400Mhz\n", 1938.0),
                                       ("S: 112Mhz *\n0: 500Mhz\n1: 2400Mhz\n", 112.0),
                                       ("0: 500Mhz\n1: 2400Mhz\n", None)])
