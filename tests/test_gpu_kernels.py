@@ -122,6 +122,20 @@ def test_gemm_tn_accumulates(dt):
     assert rel_l2(host(C), ref) < (1e-5 if dt == "f32" else 5e-3)
 
 
+@pytest.mark.parametrize("K", [1, 63, 64, 65, 128, 129, 192])
+def test_gemm_tn_short_reductions(K):
+    """bf16 weight gradient over 1-3 reduction stages: the prologue and peeled
+    last stage of the loop, where only some waves issue the operand loads."""
+    M, N = 256, 512
+    A, B = rnd((K, M), 60 + K), rnd((K, N), 61 + K)
+    C0 = rnd((M, N), 62, dt="f32")
+    ref = C0.astype(np.float64) + A.astype(np.float64).T @ B.astype(np.float64)
+    C = torch.from_numpy(C0).cuda()
+    F.fl_test_gemm(F.FL_BF16, F.FL_GEMM_TN, F.FL_EPI_ACC_F32, dev(A, "bf16"), dev(B, "bf16"), C, M, N, K, M, N, N)
+    sync()
+    assert rel_l2(host(C), ref) < 5e-3
+
+
 SPLIT_CASES = [  # (layout, epi, M, N, K): 1-4 tiles, K of 128+ stages, so the launch splits the reduction
     (F.FL_GEMM_NT, F.FL_EPI_BIAS_RES, 300, 512, 8192),
     (F.FL_GEMM_NT, F.FL_EPI_BIAS_GELU, 200, 256, 8256),
