@@ -61,6 +61,7 @@ extern "C" {
 #define FL_ERR_ALIGN (-8)       /* a device pointer is not 16-byte aligned */
 #define FL_ERR_HIP (-9)         /* a HIP runtime call or kernel launch failed */
 #define FL_ERR_ARG (-10)        /* other invalid argument */
+#define FL_ERR_NOMEM (-11)      /* a host allocation for a handle failed */
 
 #define FL_BF16 0
 #define FL_F32 1
@@ -145,7 +146,8 @@ typedef struct fl_layer_grads {
 typedef struct fl_stack fl_stack;
 
 /* Creates a handle for a stack shape (validated; FL_ERR_SHAPE if
- * unsupported).  Host-only: no HIP call.  On its first device call the
+ * unsupported; FL_ERR_NOMEM if the handle cannot be allocated).  Host-only:
+ * no HIP call.  On its first device call the
  * handle creates a few events and a small pinned host staging area used to
  * upload per-call batch descriptors; it never owns device memory. */
 int fl_stack_create(const fl_stack_desc* desc, fl_stack** out);
@@ -247,7 +249,8 @@ typedef struct {
   float ln_eps;    /* eps of the optional final LayerNorm (> 0 when one is used; ChatGLM-6B: 1e-5) */
 } fl_client_desc;
 
-/* FL_ERR_SHAPE for an unsupported descriptor. */
+/* FL_ERR_SHAPE for an unsupported descriptor, FL_ERR_NOMEM if the handle
+ * cannot be allocated. */
 int fl_client_create(const fl_client_desc* desc, fl_client** out);
 int fl_client_destroy(fl_client* client);
 /* Workspace for T tokens (1 <= T <= 2^26): the logits [T, vocab rounded up

@@ -23,6 +23,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <new>
 #include <vector>
 
 #include "../../include/flglm.h"
@@ -298,7 +299,9 @@ int fl_client_create(const fl_client_desc* desc, fl_client** out) {
   if (desc->hidden < 256 || desc->hidden % 256 || desc->hidden > 16384)
     return set_error(FL_ERR_SHAPE, "hidden must be a multiple of 256 in [256, 16384]");
   if (!(desc->ln_eps >= 0.f) || !std::isfinite(desc->ln_eps)) return set_error(FL_ERR_SHAPE, "ln_eps must be >= 0");
-  fl_client* c = new fl_client;
+  // no exception may leave a C entry point: a failed allocation is an error code
+  fl_client* c = new (std::nothrow) fl_client;
+  if (!c) return set_error(FL_ERR_NOMEM, "out of host memory for the client handle");
   c->d = *desc;
   c->E = desc->dtype == FL_BF16 ? 2 : 4;
   c->vpad = (desc->vocab + kVocabTile - 1) / kVocabTile * kVocabTile;

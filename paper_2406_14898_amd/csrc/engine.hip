@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -776,7 +777,9 @@ int fl_stack_create(const fl_stack_desc* desc, fl_stack** out) {
   *out = nullptr;
   int rc = validate_desc(desc);
   if (rc) return rc;
-  fl_stack* st = new fl_stack();
+  // no exception may leave a C entry point: a failed allocation is an error code
+  fl_stack* st = new (std::nothrow) fl_stack();
+  if (!st) return fail(FL_ERR_NOMEM, "out of host memory for the stack handle");
   st->d = *desc;
   st->E = desc->dtype == FL_BF16 ? 2 : 4;
   st->hd = desc->hidden / desc->num_heads;

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflglm.so
 FL_OK = 0
 FL_ERR_NULL, FL_ERR_SHAPE, FL_ERR_SEQLENS, FL_ERR_CLIENTS, FL_ERR_PREFIX = -1, -2, -3, -4, -5
 FL_ERR_WORKSPACE, FL_ERR_ALIAS, FL_ERR_ALIGN, FL_ERR_HIP, FL_ERR_ARG = -6, -7, -8, -9, -10
+FL_ERR_NOMEM = -11
 FL_BF16, FL_F32 = 0, 1
 FL_MASK_CAUSAL, FL_MASK_PREFIX = 0, 1
 FL_GEMM_NT, FL_GEMM_NN, FL_GEMM_TN = 0, 1, 2
