@@ -160,10 +160,15 @@ def _check(rc: int) -> None:
 
 
 def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (None and integer addresses pass through).
+    Every tensor argument of the library is device memory: a host tensor is
+    refused here instead of handing its address to a kernel."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if getattr(t, "is_cuda", True) is False:
+        raise FlglmError(FL_ERR_ARG, f"tensor on {t.device}: the library takes device memory")
     return t.data_ptr()
 
 

@@ -325,3 +325,13 @@ def test_attention_ds_tiles_count_visible_tile_pairs(seed):
                 tiles += bool(m[64 * qt:64 * qt + 64, 64 * kt:64 * kt + 64].any())
     off_bytes = ((S + 1) * 8 + 255) // 256 * 256
     assert F.fl_test_attention_ds_bytes(cu, prefix, nh, num_prefix) == off_bytes + nh * tiles * 64 * 64 * 2
+
+
+def test_host_tensors_are_refused_before_the_library():
+    """Every tensor argument is device memory: a host tensor raises FL_ERR_ARG
+    in the binding, so no host address ever reaches a kernel."""
+    import torch
+    with pytest.raises(F.FlglmError) as e:
+        F._ptr(torch.zeros(4))
+    assert e.value.code == F.FL_ERR_ARG
+    assert F._ptr(None) is None and F._ptr(4096) == 4096
