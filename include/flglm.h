@@ -34,6 +34,9 @@
  *   - `stream` is a hipStream_t (NULL = the default stream).  All device work
  *     is asynchronous on that stream; execution errors surface at the
  *     caller's next synchronisation.  One stream per handle at a time.
+ *   - A handle is not thread-safe: its upload ring and launch records are
+ *     unsynchronised host state, so calls on one handle must not run
+ *     concurrently from several threads (use one handle per thread).
  *   - Element type of activations and weights is the handle's dtype (bf16 or
  *     fp32); statistics, softmax and all accumulation are fp32; weight
  *     gradients are fp32 and are accumulated (+=), never zeroed.
